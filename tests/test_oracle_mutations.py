@@ -1,0 +1,61 @@
+"""The oracle's pins must catch plausible mistakes.  Each test plants one
+mistake in the oracle (on the CPU, via monkeypatch) and checks that a pin
+from the other test files fails."""
+
+import numpy as np
+import pytest
+
+from oracle import attention, encoding, paged
+from tests import test_oracle_attention as ta
+from tests import test_oracle_encoding as te
+from tests import test_oracle_transitions as tt
+
+
+def test_rounding_instead_of_truncation_is_caught(monkeypatch, golden_dir):
+    def rounded_hi(words):
+        w = np.asarray(words, dtype=np.uint16).astype(np.uint32)
+        return np.minimum((w + 0x80) >> 8, 0xFF).astype(np.uint8)
+    monkeypatch.setattr(encoding, "hi_byte", rounded_hi)
+    with pytest.raises(AssertionError):
+        te.test_golden_words(golden_dir)
+    with pytest.raises(AssertionError):
+        te.test_refinement_is_exact_for_every_word()
+
+
+def test_reading_the_wrong_pair_member_is_caught(monkeypatch):
+    orig = encoding.base_word
+
+    def member0_block_words(pool, bt_row, tag_row, i):
+        phys = int(bt_row[i])
+        if int(tag_row[i]) == paged.TARGET:
+            return pool[phys].copy()
+        return orig(paged.packed_bytes(pool, phys)[:, :, 0])
+    monkeypatch.setattr(paged, "block_words", member0_block_words)
+    with pytest.raises(AssertionError):
+        ta.test_decode_matches_brute_force("bf16", 0.5)
+    with pytest.raises(AssertionError):
+        ta.test_prefill_with_base_prefix_matches_causal_sdpa_on_truncated_words()
+
+
+def test_wrong_widening_is_caught(monkeypatch):
+    def bad_widen(words, dtype):
+        w = np.asarray(words, dtype=np.uint16)
+        return (w.astype(np.uint32) << np.uint32(15)).view(np.float32).astype(np.float64)
+    monkeypatch.setattr(encoding, "words_to_f64", bad_widen)
+    with pytest.raises(AssertionError):
+        ta.test_decode_matches_torch_sdpa(4)
+
+
+def test_unnormalised_softmax_is_caught(monkeypatch):
+    def bad(scores, values):
+        return np.exp(scores - np.max(scores, axis=-1, keepdims=True)) @ values
+    monkeypatch.setattr(attention, "_softmax_weighted", bad)
+    with pytest.raises(AssertionError):
+        ta.test_zero_query_gives_mean_of_values()
+
+
+def test_dropped_low_byte_in_refine_is_caught(monkeypatch):
+    monkeypatch.setattr(encoding, "refine_word",
+                        lambda hi, lo: (np.asarray(hi, np.uint16) << np.uint16(8)).astype(np.uint16))
+    with pytest.raises(AssertionError):
+        tt.test_round_trip_restores_every_byte()
