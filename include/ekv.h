@@ -1,0 +1,224 @@
+/*
+ * ekv.h -- C ABI of libekv, the MI355X (gfx950) mixed-fidelity paged KV
+ * attention library.
+ *
+ * Method: ElasticKV ("Does Execution Require Target KV Fidelity? A
+ * Mixed-Fidelity KV Runtime for LLM Serving").  Every KV element exists in
+ * one of two executable states:
+ *
+ *   TARGET -- the native 16-bit word (bf16 or fp16);
+ *   BASE   -- the high-order byte of that word, executed with a zero low
+ *             byte; the low byte (the refinement bits) restores TARGET
+ *             exactly (paper §3, opening paragraph; App. B.2, App. B.3).
+ *
+ * Memory layout (all in device memory, all owned by the caller):
+ *
+ *   pool        uint16 [num_blocks][2][num_kv_heads][page_size][head_dim]
+ *               plane 0 = K, plane 1 = V.  A physical block holds
+ *               page_size tokens of every KV head (paged KV, §2.1).
+ *   block_table int32  [batch][max_blocks]: logical block i of sequence s
+ *               lives in physical block block_table[s][i].
+ *   tags        uint8  [batch][max_blocks]: 0 = TARGET, 1 = BASE; equal
+ *               for the two members of a pair.
+ *
+ * Pairs (§3.1): logical blocks (2j, 2j+1) of one sequence.  A BASE pair is
+ * packed into ONE physical block -- the block that held member 0 -- and both
+ * block-table entries point at it.  Inside it, each plane's bytes are
+ * uint8 [num_kv_heads][member][page_size][head_dim], so for every
+ * (plane, head) the 4 KiB that a TARGET block uses for that head hold
+ * [BASE bytes of member 0 | BASE bytes of member 1].  TARGET pairs keep the
+ * native layout.  Only pairs of two full blocks can be BASE.
+ *
+ * Refinement bytes of one pair ("lo" buffers) are exactly one block's
+ * worth: uint8 [2][num_kv_heads][member][page_size][head_dim].
+ *
+ * Conventions shared by every call:
+ *   - Every call that takes a hipStream_t is asynchronous on that stream and
+ *     never synchronises; errors detected on the host are returned before
+ *     anything is enqueued; a launch failure returns EKV_ERR_HIP.
+ *   - The library allocates no device memory.  Scratch space is passed in
+ *     by the caller (see ekv_decode_workspace_bytes).
+ *   - Host-side checks cover shapes and pointers.  Checks that need the
+ *     contents of device arrays (a tag that differs inside a pair, an
+ *     already-BASE pair in a demotion list) are done by the ekv_check_*
+ *     functions on host mirrors; the device calls assume valid lists.
+ *   - Supported: head_dim 128, page_size 16, dtype bf16 or fp16,
+ *     num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}.  Other shapes return
+ *     EKV_ERR_UNSUPPORTED.
+ *   - ekv_last_error() returns a text describing the last failure on the
+ *     calling thread.
+ */
+#ifndef EKV_H
+#define EKV_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#include <hip/hip_runtime_api.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t ekv_status;
+enum {
+  EKV_OK = 0,
+  EKV_ERR_INVALID = 1,      /* bad argument or transition list */
+  EKV_ERR_UNSUPPORTED = 2,  /* valid but not implemented for this shape */
+  EKV_ERR_HIP = 3           /* a HIP runtime call failed */
+};
+
+enum { EKV_DTYPE_BF16 = 0, EKV_DTYPE_FP16 = 1, EKV_DTYPE_FP32 = 2 };
+
+/* Batch execution mode (§3.2; App. B.3): NATIVE for TARGET-only batches;
+ * STRUCTURED when every sequence is TARGET* BASE* TARGET* (described by its
+ * boundaries); GENERAL when some sequence needs the explicit tag table. */
+enum { EKV_MODE_NATIVE = 0, EKV_MODE_STRUCTURED = 1, EKV_MODE_GENERAL = 2 };
+
+enum { EKV_TAG_TARGET = 0, EKV_TAG_BASE = 1 };
+
+typedef struct {
+  void* kv;               /* device pool, layout above */
+  int32_t num_blocks;
+  int32_t num_kv_heads;
+  int32_t page_size;      /* 16 */
+  int32_t head_dim;       /* 128 */
+  int32_t dtype;          /* EKV_DTYPE_BF16 or EKV_DTYPE_FP16 */
+} ekv_pool;
+
+typedef struct {
+  int32_t batch;
+  int32_t num_q_heads;
+  int32_t max_blocks;          /* row length of block_table and tags */
+  int32_t mode;                /* EKV_MODE_*, as returned by ekv_lower */
+  int32_t max_seq_len;         /* upper bound on seq_lens[] (0: max_blocks*page_size) */
+  const int32_t* seq_lens;     /* device int32 [batch] */
+  const int32_t* block_table;  /* device int32 [batch][max_blocks] */
+  const uint8_t* tags;         /* device uint8 [batch][max_blocks]; may be NULL in NATIVE mode */
+  const int32_t* boundaries;   /* device int32 [batch][2] or NULL (NULL: tags for every sequence) */
+} ekv_batch;
+
+/* Text for a status code (static storage). */
+const char* ekv_status_string(ekv_status s);
+
+/* Message for the last failing call on this thread (static thread-local storage). */
+const char* ekv_last_error(void);
+
+/* Library version as "major.minor.patch". */
+const char* ekv_version(void);
+
+/*
+ * Dispatch metadata lowering (§3.2; App. B.3), host only.
+ * h_tags [batch][max_blocks], h_seq_lens [batch]: host mirrors.
+ * Writes *mode_out (EKV_MODE_*) and h_boundaries_out [batch][2]: for a
+ * sequence whose visible pair modes read TARGET* BASE* TARGET*, the pair
+ * range [b0, b1) that is BASE (b0 == b1 when none); (-1, -1) for any other
+ * sequence.  Only the ceil(len/page_size) blocks holding tokens are read.
+ * Errors: EKV_ERR_INVALID on NULL pointers, negative sizes, a length beyond
+ * max_blocks*page_size, or a pair whose two tags differ.
+ */
+ekv_status ekv_lower(const uint8_t* h_tags, const int32_t* h_seq_lens, int32_t batch,
+                     int32_t max_blocks, int32_t page_size, int32_t* mode_out,
+                     int32_t* h_boundaries_out);
+
+/*
+ * Bytes of device scratch that ekv_attn_decode needs for this pool and
+ * batch (split-KV partial results).  Returns 0 for unsupported shapes.
+ */
+size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch);
+
+/*
+ * Decode attention, one query token per sequence (§3.2; App. B.3): for
+ * sequence s and query head h (KV head h / (Hq/Hkv)),
+ *   out[s][h] = softmax(scale * q[s][h] . K_s^T) V_s
+ * over the seq_lens[s] cached tokens, each KV block read in its mode: TARGET
+ * words as they are, BASE bytes placed in the high byte with a zero low
+ * byte.  batch->mode selects the native path (no tag is read) or the
+ * elastic path; in the elastic path a sequence with boundaries[s][0] >= 0
+ * uses its boundaries and any other sequence reads its tags.
+ *   q    device [batch][num_q_heads][head_dim], pool dtype
+ *   out  device [batch][num_q_heads][head_dim], out_dtype = pool dtype or EKV_DTYPE_FP32
+ *   ws   device scratch of at least ekv_decode_workspace_bytes() bytes
+ * A sequence of length 0 yields zeros.
+ * Errors: EKV_ERR_INVALID (NULL pointers, sizes, workspace too small,
+ * NATIVE mode expected but tags needed), EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.
+ */
+ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const void* q,
+                           void* out, int32_t out_dtype, float scale, void* ws, size_t ws_bytes,
+                           hipStream_t stream);
+
+/*
+ * Chunked-prefill attention (§3.2; App. A): sequence s contributes the new
+ * rows q[cu_q[s] .. cu_q[s+1]) whose K/V have already been appended; row i
+ * of the chunk sees keys 0 .. seq_lens[s] - n_s + i (causal, inclusive),
+ * where n_s = cu_q[s+1] - cu_q[s] and seq_lens[s] counts the whole context.
+ * The prefix may mix TARGET and BASE blocks; the chunk's blocks are TARGET.
+ *   q    device [total_q][num_q_heads][head_dim], pool dtype
+ *   cu_q device int32 [batch+1], nondecreasing, cu_q[0] = 0, cu_q[batch] = total_q
+ *   out  device [total_q][num_q_heads][head_dim], out_dtype = pool dtype or EKV_DTYPE_FP32
+ *   max_q_len  upper bound on every n_s (sizes the launch)
+ * Errors: as ekv_attn_decode.
+ */
+ekv_status ekv_attn_prefill(const ekv_pool* pool, const ekv_batch* batch, const void* q,
+                            const int32_t* cu_q, int32_t total_q, int32_t max_q_len, void* out,
+                            int32_t out_dtype, float scale, hipStream_t stream);
+
+/*
+ * Append new K/V rows as TARGET (§3.2: new KV is written in TARGET form).
+ * Row i goes to token slot slots[i] = physical_block * page_size + offset.
+ *   slots device int32 [n]; k, v device [n][num_kv_heads][head_dim], pool dtype.
+ * Slots must be distinct and lie in TARGET blocks.
+ * Errors: EKV_ERR_INVALID, EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.
+ */
+ekv_status ekv_append_kv(const ekv_pool* pool, const int32_t* slots, const void* k,
+                         const void* v, int32_t n, hipStream_t stream);
+
+/*
+ * Demotion TARGET -> BASE (§3.1; §3.4 "Transition protocols"; App. B.2).
+ * For each listed pair i = (s, j) (device int32 pairs[n][2]), with
+ * b0 = block_table[s][2j] and b1 = block_table[s][2j+1]: the high bytes of
+ * both blocks are packed into b0 in place; if lo_out is not NULL the low
+ * bytes go to lo_out[i] (device uint8 [n][one block's bytes]); then
+ * block_table[s][2j+1] = b0, both tags = BASE and freed_out[i] = b1 (device
+ * int32 [n]).  b1's bytes are not touched.  The caller returns freed_out[]
+ * to its free pool only after the stream has passed this call.
+ * Errors: EKV_ERR_INVALID, EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.
+ */
+ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs,
+                      int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,
+                      int32_t* freed_out, uint8_t* lo_out, hipStream_t stream);
+
+/*
+ * Refinement BASE -> TARGET (§3.1; §3.3; App. B.2).  For each listed pair
+ * i = (s, j) with packed block P = block_table[s][2j] and the reacquired
+ * block Q = new_blocks[i] (device int32 [n]): member 0 is restored in place
+ * into P and member 1 into Q from the high bytes in P and the refinement
+ * bytes lo_in[i] (uint8 [n][one block's bytes], device memory or pinned
+ * host memory mapped for the device); then block_table[s][2j+1] = Q and
+ * both tags = TARGET.  No attention call may read these pairs concurrently
+ * on another stream.
+ * Errors: EKV_ERR_INVALID, EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.
+ */
+ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
+                      const int32_t* new_blocks, int32_t* block_table, uint8_t* tags,
+                      int32_t batch, int32_t max_blocks, const uint8_t* lo_in, hipStream_t stream);
+
+/*
+ * Host-side validation of a transition list against host mirrors (App. B.1:
+ * only demotable TARGET pairs and promotable BASE pairs are offered).
+ * kind 0 = demotion (pairs must be TARGET), 1 = refinement (pairs must be
+ * BASE and h_new_blocks [n] must be distinct ids in [0, num_blocks) that no
+ * visible logical block uses).  Each pair must be distinct, in range and
+ * made of two full blocks.  Returns EKV_OK or EKV_ERR_INVALID.
+ */
+ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,
+                                const int32_t* h_block_table, const uint8_t* h_tags,
+                                const int32_t* h_seq_lens, int32_t batch, int32_t max_blocks,
+                                int32_t page_size, int32_t num_blocks,
+                                const int32_t* h_new_blocks);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* EKV_H */

@@ -1,0 +1,344 @@
+// C ABI of libekv: argument checks, dispatch-metadata lowering, split-KV
+// planning, and kernel dispatch.  Declarations and contracts: include/ekv.h.
+#include <algorithm>
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstdlib>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "ekv.h"
+#include "common.h"
+#include "launch.h"
+
+namespace {
+
+thread_local std::string g_last_error;
+
+ekv_status fail(ekv_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+ekv_status fail(ekv_status s, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_last_error = buf;
+  return s;
+}
+
+ekv_status hip_status(hipError_t e, const char* what) {
+  if (e == hipSuccess) return EKV_OK;
+  return fail(EKV_ERR_HIP, "%s: %s", what, hipGetErrorString(e));
+}
+
+bool supported_group(int g) { return g == 1 || g == 2 || g == 4 || g == 8 || g == 16; }
+
+ekv_status check_pool(const ekv_pool* p) {
+  if (!p) return fail(EKV_ERR_INVALID, "pool is NULL");
+  if (!p->kv) return fail(EKV_ERR_INVALID, "pool->kv is NULL");
+  if (p->num_blocks <= 0 || p->num_kv_heads <= 0)
+    return fail(EKV_ERR_INVALID, "pool sizes must be positive");
+  if (p->head_dim != ekv::kHeadDim || p->page_size != ekv::kPage)
+    return fail(EKV_ERR_UNSUPPORTED, "only head_dim 128 and page_size 16 are supported");
+  if (p->dtype != EKV_DTYPE_BF16 && p->dtype != EKV_DTYPE_FP16)
+    return fail(EKV_ERR_UNSUPPORTED, "pool dtype must be bf16 or fp16");
+  if (p->num_kv_heads > 64) return fail(EKV_ERR_UNSUPPORTED, "at most 64 KV heads");
+  return EKV_OK;
+}
+
+ekv_status check_attention_batch(const ekv_pool* p, const ekv_batch* b, int* group) {
+  if (!b) return fail(EKV_ERR_INVALID, "batch is NULL");
+  if (b->batch < 0 || b->max_blocks <= 0 || b->num_q_heads <= 0)
+    return fail(EKV_ERR_INVALID, "batch sizes must be positive");
+  if (b->num_q_heads % p->num_kv_heads)
+    return fail(EKV_ERR_INVALID, "num_q_heads must be a multiple of num_kv_heads");
+  *group = b->num_q_heads / p->num_kv_heads;
+  if (!supported_group(*group)) return fail(EKV_ERR_UNSUPPORTED, "group size %d not supported", *group);
+  if (b->batch > 0 && (!b->seq_lens || !b->block_table))
+    return fail(EKV_ERR_INVALID, "seq_lens and block_table are required");
+  if (b->mode < EKV_MODE_NATIVE || b->mode > EKV_MODE_GENERAL)
+    return fail(EKV_ERR_INVALID, "unknown mode %d", b->mode);
+  if (b->mode == EKV_MODE_STRUCTURED && !b->boundaries && !b->tags)
+    return fail(EKV_ERR_INVALID, "structured mode needs boundaries (or tags)");
+  if (b->mode == EKV_MODE_GENERAL && !b->tags)
+    return fail(EKV_ERR_INVALID, "general mode needs the tag table");
+  if ((long long)b->max_seq_len > (long long)b->max_blocks * ekv::kPage || b->max_seq_len < 0)
+    return fail(EKV_ERR_INVALID, "max_seq_len exceeds max_blocks * page_size");
+  return EKV_OK;
+}
+
+int max_seq_blocks(const ekv_batch* b) {
+  const int len = b->max_seq_len > 0 ? b->max_seq_len : b->max_blocks * ekv::kPage;
+  return (len + ekv::kPage - 1) / ekv::kPage;
+}
+
+// Blocks per split: the smallest power of two >= 8 that keeps the launch at
+// or under ~16k work items (64 per CU), unless EKV_SPLIT_BLOCKS overrides.
+int plan_split_blocks(int batch, int hkv, int nblk_max) {
+  if (const char* env = getenv("EKV_SPLIT_BLOCKS")) {
+    const int v = atoi(env);
+    if (v > 0) return v;
+  }
+  const long long items = (long long)batch * hkv;
+  int sb = 8;
+  while (sb < 1024 && items * ((nblk_max + sb - 1) / sb) > 16384) sb *= 2;
+  return sb;
+}
+
+struct DecodePlan {
+  int split_blocks, max_splits;
+  size_t o_bytes, ml_offset, total;
+};
+
+DecodePlan plan_decode(const ekv_pool* p, const ekv_batch* b) {
+  DecodePlan d{};
+  const int nblk = std::max(1, max_seq_blocks(b));
+  d.split_blocks = plan_split_blocks(b->batch, p->num_kv_heads, nblk);
+  d.max_splits = std::max(1, (nblk + d.split_blocks - 1) / d.split_blocks);
+  const size_t rows = (size_t)b->batch * b->num_q_heads * d.max_splits;
+  d.o_bytes = rows * ekv::kHeadDim * sizeof(float);
+  d.ml_offset = (d.o_bytes + 255) & ~(size_t)255;
+  d.total = d.ml_offset + rows * 2 * sizeof(float);
+  return d;
+}
+
+float log2e_scale(float scale) { return scale * 1.4426950408889634f; }
+
+}  // namespace
+
+extern "C" {
+
+const char* ekv_status_string(ekv_status s) {
+  switch (s) {
+    case EKV_OK: return "ok";
+    case EKV_ERR_INVALID: return "invalid argument";
+    case EKV_ERR_UNSUPPORTED: return "unsupported";
+    case EKV_ERR_HIP: return "HIP runtime error";
+    default: return "unknown status";
+  }
+}
+
+const char* ekv_last_error(void) { return g_last_error.c_str(); }
+
+const char* ekv_version(void) { return "0.1.0"; }
+
+ekv_status ekv_lower(const uint8_t* h_tags, const int32_t* h_seq_lens, int32_t batch,
+                     int32_t max_blocks, int32_t page_size, int32_t* mode_out,
+                     int32_t* h_boundaries_out) {
+  if (!mode_out || batch < 0 || max_blocks <= 0 || page_size <= 0)
+    return fail(EKV_ERR_INVALID, "ekv_lower: bad sizes or NULL mode_out");
+  if (batch > 0 && (!h_tags || !h_seq_lens || !h_boundaries_out))
+    return fail(EKV_ERR_INVALID, "ekv_lower: NULL array");
+  bool any_base = false, any_irregular = false;
+  for (int s = 0; s < batch; ++s) {
+    const int len = h_seq_lens[s];
+    if (len < 0 || (long long)len > (long long)max_blocks * page_size)
+      return fail(EKV_ERR_INVALID, "ekv_lower: sequence %d length %d out of range", s, len);
+    const int nblk = (len + page_size - 1) / page_size;
+    const uint8_t* row = h_tags + (size_t)s * max_blocks;
+    int first = -1, last = -1, count = 0;
+    for (int j = 0; 2 * j < nblk; ++j) {
+      const uint8_t a = row[2 * j];
+      const uint8_t b = (2 * j + 1 < nblk) ? row[2 * j + 1] : a;
+      if (a > 1 || b > 1) return fail(EKV_ERR_INVALID, "ekv_lower: tag value out of range");
+      if (a != b) return fail(EKV_ERR_INVALID, "ekv_lower: pair %d of sequence %d has mixed tags", j, s);
+      if (a) {
+        if (first < 0) first = j;
+        last = j;
+        ++count;
+      }
+    }
+    int32_t* out = h_boundaries_out + 2 * s;
+    if (count == 0) {
+      out[0] = out[1] = 0;
+    } else if (count == last - first + 1) {
+      any_base = true;
+      out[0] = first;
+      out[1] = last + 1;
+    } else {
+      any_base = any_irregular = true;
+      out[0] = out[1] = -1;
+    }
+  }
+  *mode_out = !any_base ? EKV_MODE_NATIVE : (any_irregular ? EKV_MODE_GENERAL : EKV_MODE_STRUCTURED);
+  return EKV_OK;
+}
+
+size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch) {
+  int group = 0;
+  if (check_pool(pool) != EKV_OK || check_attention_batch(pool, batch, &group) != EKV_OK) return 0;
+  return plan_decode(pool, batch).total;
+}
+
+ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out,
+                           int32_t out_dtype, float scale, void* ws, size_t ws_bytes,
+                           hipStream_t stream) {
+  ekv_status st = check_pool(pool);
+  if (st != EKV_OK) return st;
+  int group = 0;
+  if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
+  if (batch->batch == 0) return EKV_OK;
+  if (!q || !out) return fail(EKV_ERR_INVALID, "q and out are required");
+  if (out_dtype != pool->dtype && out_dtype != EKV_DTYPE_FP32)
+    return fail(EKV_ERR_INVALID, "out_dtype must be the pool dtype or fp32");
+  if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
+  const DecodePlan plan = plan_decode(pool, batch);
+  if (!ws || ws_bytes < plan.total)
+    return fail(EKV_ERR_INVALID, "workspace of %zu bytes needed, %zu given", plan.total, ws_bytes);
+  ekv::DecodeArgs a{};
+  a.pool = static_cast<const uint16_t*>(pool->kv);
+  a.q = static_cast<const uint16_t*>(q);
+  a.seq_lens = batch->seq_lens;
+  a.bt = batch->block_table;
+  a.tags = batch->tags;
+  a.bounds = batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries;
+  a.ws_o = static_cast<float*>(ws);
+  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.ml_offset);
+  a.out = out;
+  a.batch = batch->batch;
+  a.num_kv_heads = pool->num_kv_heads;
+  a.num_q_heads = batch->num_q_heads;
+  a.max_blocks = batch->max_blocks;
+  a.split_blocks = plan.split_blocks;
+  a.max_splits = plan.max_splits;
+  a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
+  a.scale_log2 = log2e_scale(scale);
+  return hip_status(ekv::launch_decode(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
+                    "ekv_attn_decode launch");
+}
+
+ekv_status ekv_attn_prefill(const ekv_pool* pool, const ekv_batch* batch, const void* q,
+                            const int32_t* cu_q, int32_t total_q, int32_t max_q_len, void* out,
+                            int32_t out_dtype, float scale, hipStream_t stream) {
+  ekv_status st = check_pool(pool);
+  if (st != EKV_OK) return st;
+  int group = 0;
+  if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
+  if (total_q < 0 || max_q_len < 0) return fail(EKV_ERR_INVALID, "negative sizes");
+  if (batch->batch == 0 || total_q == 0) return EKV_OK;
+  if (!q || !out || !cu_q) return fail(EKV_ERR_INVALID, "q, cu_q and out are required");
+  if (out_dtype != pool->dtype && out_dtype != EKV_DTYPE_FP32)
+    return fail(EKV_ERR_INVALID, "out_dtype must be the pool dtype or fp32");
+  if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
+  if (max_q_len == 0) return EKV_OK;
+  ekv::PrefillArgs a{};
+  a.pool = static_cast<const uint16_t*>(pool->kv);
+  a.q = static_cast<const uint16_t*>(q);
+  a.cu_q = cu_q;
+  a.seq_lens = batch->seq_lens;
+  a.bt = batch->block_table;
+  a.tags = batch->tags;
+  a.bounds = batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries;
+  a.out = out;
+  a.batch = batch->batch;
+  a.num_kv_heads = pool->num_kv_heads;
+  a.num_q_heads = batch->num_q_heads;
+  a.max_blocks = batch->max_blocks;
+  a.max_q_len = max_q_len;
+  a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
+  a.scale_log2 = log2e_scale(scale);
+  return hip_status(ekv::launch_prefill(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
+                    "ekv_attn_prefill launch");
+}
+
+ekv_status ekv_append_kv(const ekv_pool* pool, const int32_t* slots, const void* k, const void* v,
+                         int32_t n, hipStream_t stream) {
+  ekv_status st = check_pool(pool);
+  if (st != EKV_OK) return st;
+  if (n < 0) return fail(EKV_ERR_INVALID, "negative n");
+  if (n == 0) return EKV_OK;
+  if (!slots || !k || !v) return fail(EKV_ERR_INVALID, "slots, k and v are required");
+  ekv::AppendArgs a{static_cast<uint16_t*>(pool->kv), slots, static_cast<const uint16_t*>(k),
+                    static_cast<const uint16_t*>(v), n, pool->num_kv_heads};
+  return hip_status(ekv::launch_append(a, stream), "ekv_append_kv launch");
+}
+
+static ekv_status check_transition_args(const ekv_pool* pool, int32_t n, const int32_t* pairs,
+                                        int32_t* block_table, uint8_t* tags, int32_t batch,
+                                        int32_t max_blocks) {
+  ekv_status st = check_pool(pool);
+  if (st != EKV_OK) return st;
+  if (n < 0 || batch < 0 || max_blocks < 2) return fail(EKV_ERR_INVALID, "bad sizes");
+  if (n > 0 && (!pairs || !block_table || !tags))
+    return fail(EKV_ERR_INVALID, "pairs, block_table and tags are required");
+  if (n > 65535) return fail(EKV_ERR_UNSUPPORTED, "at most 65535 pairs per call");
+  return EKV_OK;
+}
+
+ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int32_t* block_table,
+                      uint8_t* tags, int32_t batch, int32_t max_blocks, int32_t* freed_out,
+                      uint8_t* lo_out, hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (n == 0) return EKV_OK;
+  if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
+  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), pairs, nullptr, block_table, tags,
+                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks};
+  return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
+}
+
+ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
+                      const int32_t* new_blocks, int32_t* block_table, uint8_t* tags, int32_t batch,
+                      int32_t max_blocks, const uint8_t* lo_in, hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (n == 0) return EKV_OK;
+  if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
+  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), pairs, new_blocks, block_table, tags,
+                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks};
+  return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
+}
+
+ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,
+                                const int32_t* h_block_table, const uint8_t* h_tags,
+                                const int32_t* h_seq_lens, int32_t batch, int32_t max_blocks,
+                                int32_t page_size, int32_t num_blocks,
+                                const int32_t* h_new_blocks) {
+  if (kind != 0 && kind != 1) return fail(EKV_ERR_INVALID, "kind must be 0 (demote) or 1 (refine)");
+  if (n < 0 || batch < 0 || max_blocks < 2 || page_size <= 0 || num_blocks <= 0)
+    return fail(EKV_ERR_INVALID, "bad sizes");
+  if (n == 0) return EKV_OK;
+  if (!h_pairs || !h_block_table || !h_tags || !h_seq_lens)
+    return fail(EKV_ERR_INVALID, "NULL host mirror");
+  const uint8_t want = kind == 0 ? EKV_TAG_TARGET : EKV_TAG_BASE;
+  std::vector<uint8_t> seen((size_t)batch * max_blocks, 0);
+  for (int i = 0; i < n; ++i) {
+    const int s = h_pairs[2 * i], j = h_pairs[2 * i + 1];
+    if (s < 0 || s >= batch || j < 0 || 2 * j + 1 >= max_blocks)
+      return fail(EKV_ERR_INVALID, "pair %d (%d,%d) out of range", i, s, j);
+    if ((long long)2 * page_size * (j + 1) > h_seq_lens[s])
+      return fail(EKV_ERR_INVALID, "pair %d (%d,%d) is not two full blocks", i, s, j);
+    uint8_t& mark = seen[(size_t)s * max_blocks + 2 * j];
+    if (mark) return fail(EKV_ERR_INVALID, "pair (%d,%d) listed twice", s, j);
+    mark = 1;
+    const uint8_t* row = h_tags + (size_t)s * max_blocks;
+    if (row[2 * j] != want || row[2 * j + 1] != want)
+      return fail(EKV_ERR_INVALID, "pair (%d,%d) is not in the expected state", s, j);
+    const int32_t* bt = h_block_table + (size_t)s * max_blocks;
+    for (int m = 0; m < 2; ++m)
+      if (bt[2 * j + m] < 0 || bt[2 * j + m] >= num_blocks)
+        return fail(EKV_ERR_INVALID, "pair (%d,%d) maps outside the pool", s, j);
+  }
+  if (kind == 1) {
+    if (!h_new_blocks) return fail(EKV_ERR_INVALID, "refinement needs new blocks");
+    std::vector<uint8_t> used((size_t)num_blocks, 0);
+    for (int s = 0; s < batch; ++s) {
+      const int nblk = (h_seq_lens[s] + page_size - 1) / page_size;
+      for (int i = 0; i < nblk && i < max_blocks; ++i) {
+        const int b = h_block_table[(size_t)s * max_blocks + i];
+        if (b >= 0 && b < num_blocks) used[b] = 1;
+      }
+    }
+    for (int i = 0; i < n; ++i) {
+      const int b = h_new_blocks[i];
+      if (b < 0 || b >= num_blocks) return fail(EKV_ERR_INVALID, "new block %d out of range", b);
+      if (used[b]) return fail(EKV_ERR_INVALID, "new block %d is in use", b);
+      used[b] = 1;
+    }
+  }
+  return EKV_OK;
+}
+
+}  // extern "C"

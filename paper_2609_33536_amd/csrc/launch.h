@@ -1,0 +1,67 @@
+// Host-side launchers of the libekv kernels (internal header).  The C ABI in
+// api.hip validates arguments and calls these; each launcher only enqueues.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace ekv {
+
+struct DecodeArgs {
+  const uint16_t* pool;      // [NB][2][Hkv][16][128]
+  const uint16_t* q;         // [B][Hq][128]
+  const int32_t* seq_lens;   // [B]
+  const int32_t* bt;         // [B][max_blocks]
+  const uint8_t* tags;       // [B][max_blocks] or null
+  const int32_t* bounds;     // [B][2] or null
+  float* ws_o;               // [B][Hq][max_splits][128]
+  float* ws_ml;              // [B][Hq][max_splits][2]
+  void* out;                 // [B][Hq][128]
+  int32_t batch, num_kv_heads, num_q_heads, max_blocks;
+  int32_t split_blocks, max_splits, out_fp32;
+  float scale_log2;          // softmax scale * log2(e)
+};
+
+// dtype: 0 bf16, 1 fp16.  elastic: false = native path (tags never read).
+hipError_t launch_decode(const DecodeArgs& a, int dtype, int group, bool elastic, hipStream_t st);
+
+struct TransitionArgs {
+  uint16_t* pool;
+  const int32_t* pairs;      // [n][2] = (s, j)
+  const int32_t* new_blocks; // refine: [n]
+  int32_t* bt;               // [B][max_blocks]
+  uint8_t* tags;             // [B][max_blocks]
+  int32_t* freed;            // demote: [n]
+  uint8_t* lo;               // demote: lo_out (nullable); refine: lo_in
+  int32_t n, num_kv_heads, max_blocks;
+};
+
+hipError_t launch_demote(const TransitionArgs& a, hipStream_t st);
+hipError_t launch_refine(const TransitionArgs& a, hipStream_t st);
+
+struct AppendArgs {
+  uint16_t* pool;
+  const int32_t* slots;
+  const uint16_t* k;
+  const uint16_t* v;
+  int32_t n, num_kv_heads;
+};
+
+hipError_t launch_append(const AppendArgs& a, hipStream_t st);
+
+struct PrefillArgs {
+  const uint16_t* pool;
+  const uint16_t* q;         // [total][Hq][128]
+  const int32_t* cu_q;       // [B+1]
+  const int32_t* seq_lens;   // [B]
+  const int32_t* bt;
+  const uint8_t* tags;
+  const int32_t* bounds;
+  void* out;                 // [total][Hq][128]
+  int32_t batch, num_kv_heads, num_q_heads, max_blocks, max_q_len, out_fp32;
+  float scale_log2;
+};
+
+hipError_t launch_prefill(const PrefillArgs& a, int dtype, int group, bool elastic, hipStream_t st);
+
+}  // namespace ekv

@@ -1,0 +1,164 @@
+// Fidelity transitions (paper §3.1; §3.4 "Transition protocols"; App. B.2)
+// and the TARGET append of new KV (§3.2).
+//
+// Demotion packs the high bytes of a TARGET pair into member 0's block and
+// emits the low bytes; refinement rebuilds both members' words from the
+// packed high bytes and the stored low bytes.  In the packed layout every
+// (plane, head) 4 KiB tile of the kept block holds exactly the bytes of the
+// same (plane, head) tiles of the two members, so one wave owns one tile
+// end to end: it reads everything it needs into registers, waits for all
+// its loads to land, then overwrites the tile.  No two waves touch the
+// same bytes, which is what makes the in-place rewrite race-free.
+//
+// Block-table and tag updates run in a second, tiny kernel after the data
+// kernel on the same stream, so no data wave can observe a half-updated
+// table.
+#include "common.h"
+#include "launch.h"
+
+namespace ekv {
+namespace {
+
+// 16-bit words -> their high / low bytes (4 words per u32x2).
+__device__ __forceinline__ uint32_t hi_bytes(u32x2 w) { return perm(w.y, w.x, 0x07050301u); }
+__device__ __forceinline__ uint32_t lo_bytes(u32x2 w) { return perm(w.y, w.x, 0x06040200u); }
+// (hi byte, lo byte) pairs -> 16-bit words: 4 words from one dword of each.
+__device__ __forceinline__ u32x2 join_words(uint32_t hi, uint32_t lo) {
+  return u32x2{perm(hi, lo, 0x05010400u), perm(hi, lo, 0x07030602u)};
+}
+
+__device__ __forceinline__ void wait_all_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+__global__ __launch_bounds__(64) void demote_kernel(TransitionArgs a) {
+  const int tile = blockIdx.x;   // plane * Hkv + head
+  const int i = blockIdx.y;
+  const int lane = threadIdx.x;
+  const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  const int32_t* row = a.bt + (size_t)s * a.max_blocks;
+  const size_t block_words = (size_t)2 * a.num_kv_heads * kTileWords;
+  uint16_t* t0 = a.pool + (size_t)row[2 * j] * block_words + (size_t)tile * kTileWords;
+  const uint16_t* t1 = a.pool + (size_t)row[2 * j + 1] * block_words + (size_t)tile * kTileWords;
+
+  u32x4 w0[4], w1[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    w0[r] = *reinterpret_cast<const u32x4*>(t0 + 8 * lane + 512 * r);
+    w1[r] = *reinterpret_cast<const u32x4*>(t1 + 8 * lane + 512 * r);
+  }
+  wait_all_loads();
+  uint8_t* packed = reinterpret_cast<uint8_t*>(t0);
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int off = 8 * lane + 512 * r;   // word index within the tile = byte index within a member
+    *reinterpret_cast<u32x2*>(packed + off) = u32x2{hi_bytes(w0[r].xy), hi_bytes(w0[r].zw)};
+    *reinterpret_cast<u32x2*>(packed + kTileBytes / 2 + off) = u32x2{hi_bytes(w1[r].xy), hi_bytes(w1[r].zw)};
+  }
+  if (a.lo) {
+    uint8_t* lo = a.lo + (size_t)i * (2 * block_words) + (size_t)tile * kTileBytes;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const int off = 8 * lane + 512 * r;
+      *reinterpret_cast<u32x2*>(lo + off) = u32x2{lo_bytes(w0[r].xy), lo_bytes(w0[r].zw)};
+      *reinterpret_cast<u32x2*>(lo + kTileBytes / 2 + off) = u32x2{lo_bytes(w1[r].xy), lo_bytes(w1[r].zw)};
+    }
+  }
+}
+
+__global__ __launch_bounds__(256) void demote_commit_kernel(TransitionArgs a) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.n) return;
+  const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  int32_t* row = a.bt + (size_t)s * a.max_blocks;
+  uint8_t* tg = a.tags + (size_t)s * a.max_blocks;
+  const int b0 = row[2 * j];
+  a.freed[i] = row[2 * j + 1];
+  row[2 * j + 1] = b0;
+  tg[2 * j] = 1;
+  tg[2 * j + 1] = 1;
+}
+
+__global__ __launch_bounds__(64) void refine_kernel(TransitionArgs a) {
+  const int tile = blockIdx.x;
+  const int i = blockIdx.y;
+  const int lane = threadIdx.x;
+  const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  const size_t block_words = (size_t)2 * a.num_kv_heads * kTileWords;
+  uint16_t* tp = a.pool + (size_t)a.bt[(size_t)s * a.max_blocks + 2 * j] * block_words + (size_t)tile * kTileWords;
+  uint16_t* tq = a.pool + (size_t)a.new_blocks[i] * block_words + (size_t)tile * kTileWords;
+  const uint8_t* packed = reinterpret_cast<const uint8_t*>(tp);
+  const uint8_t* lo = a.lo + (size_t)i * (2 * block_words) + (size_t)tile * kTileBytes;
+
+  u32x2 h0[4], h1[4], l0[4], l1[4];
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int off = 8 * lane + 512 * r;
+    h0[r] = *reinterpret_cast<const u32x2*>(packed + off);
+    h1[r] = *reinterpret_cast<const u32x2*>(packed + kTileBytes / 2 + off);
+    l0[r] = *reinterpret_cast<const u32x2*>(lo + off);
+    l1[r] = *reinterpret_cast<const u32x2*>(lo + kTileBytes / 2 + off);
+  }
+  wait_all_loads();
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const int off = 8 * lane + 512 * r;
+    const u32x2 a0 = join_words(h0[r].x, l0[r].x), b0 = join_words(h0[r].y, l0[r].y);
+    const u32x2 a1 = join_words(h1[r].x, l1[r].x), b1 = join_words(h1[r].y, l1[r].y);
+    *reinterpret_cast<u32x4*>(tp + off) = u32x4{a0.x, a0.y, b0.x, b0.y};
+    *reinterpret_cast<u32x4*>(tq + off) = u32x4{a1.x, a1.y, b1.x, b1.y};
+  }
+}
+
+__global__ __launch_bounds__(256) void refine_commit_kernel(TransitionArgs a) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= a.n) return;
+  const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  a.bt[(size_t)s * a.max_blocks + 2 * j + 1] = a.new_blocks[i];
+  uint8_t* tg = a.tags + (size_t)s * a.max_blocks;
+  tg[2 * j] = 0;
+  tg[2 * j + 1] = 0;
+}
+
+// One wave per new token: 2*Hkv rows of 256 B, 16 lanes per row.
+__global__ __launch_bounds__(64) void append_kernel(AppendArgs a) {
+  const int i = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int slot = a.slots[i];
+  const int blk = slot / kPage, off = slot % kPage;
+  const int hkv = a.num_kv_heads;
+  const size_t block_words = (size_t)2 * hkv * kTileWords;
+  const int c = lane & 15;
+  for (int r = lane >> 4; r < 2 * hkv; r += 4) {
+    const int plane = r / hkv, h = r % hkv;
+    const uint16_t* src = (plane ? a.v : a.k) + ((size_t)i * hkv + h) * kHeadDim + 8 * c;
+    uint16_t* dst = a.pool + (size_t)blk * block_words + (size_t)r * kTileWords + off * kHeadDim + 8 * c;
+    *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(src);
+  }
+}
+
+}  // namespace
+
+hipError_t launch_demote(const TransitionArgs& a, hipStream_t st) {
+  if (a.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(demote_kernel, dim3(2 * a.num_kv_heads, a.n), dim3(64), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(demote_commit_kernel, dim3((a.n + 255) / 256), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_refine(const TransitionArgs& a, hipStream_t st) {
+  if (a.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(refine_kernel, dim3(2 * a.num_kv_heads, a.n), dim3(64), 0, st, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return e;
+  hipLaunchKernelGGL(refine_commit_kernel, dim3((a.n + 255) / 256), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
+
+hipError_t launch_append(const AppendArgs& a, hipStream_t st) {
+  if (a.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(append_kernel, dim3(a.n), dim3(64), 0, st, a);
+  return hipGetLastError();
+}
+
+}  // namespace ekv

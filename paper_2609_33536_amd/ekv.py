@@ -1,0 +1,179 @@
+"""ctypes binding of libekv (argument marshalling only).
+
+Every function here forwards to the C ABI declared in ``include/ekv.h``;
+all computation happens in the library's HIP kernels.  Device arrays are
+passed as torch CUDA tensors (torch is used for device memory and streams
+only); host mirrors as NumPy arrays.  A missing or unbuilt library raises
+``EkvError`` -- there is no fallback path.
+"""
+
+import ctypes
+import os
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libekv.so")
+
+OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
+DTYPE_BF16, DTYPE_FP16, DTYPE_FP32 = 0, 1, 2
+MODE_NATIVE, MODE_STRUCTURED, MODE_GENERAL = 0, 1, 2
+HEAD_DIM, PAGE = 128, 16
+
+
+class EkvError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"ekv status {status}: {msg}")
+        self.status = status
+
+
+class Pool(ctypes.Structure):
+    _fields_ = [("kv", ctypes.c_void_p), ("num_blocks", ctypes.c_int32),
+                ("num_kv_heads", ctypes.c_int32), ("page_size", ctypes.c_int32),
+                ("head_dim", ctypes.c_int32), ("dtype", ctypes.c_int32)]
+
+
+class Batch(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("num_q_heads", ctypes.c_int32),
+                ("max_blocks", ctypes.c_int32), ("mode", ctypes.c_int32),
+                ("max_seq_len", ctypes.c_int32), ("seq_lens", ctypes.c_void_p),
+                ("block_table", ctypes.c_void_p), ("tags", ctypes.c_void_p),
+                ("boundaries", ctypes.c_void_p)]
+
+
+# name -> (restype, argtypes), in the order of include/ekv.h
+_P, _I, _U, _F, _S = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t, ctypes.c_float, ctypes.c_void_p
+SIGNATURES = {
+    "ekv_status_string": (ctypes.c_char_p, [_I]),
+    "ekv_last_error": (ctypes.c_char_p, []),
+    "ekv_version": (ctypes.c_char_p, []),
+    "ekv_lower": (_I, [_P, _P, _I, _I, _I, _P, _P]),
+    "ekv_decode_workspace_bytes": (_U, [ctypes.POINTER(Pool), ctypes.POINTER(Batch)]),
+    "ekv_attn_decode": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _F, _P, _U, _S]),
+    "ekv_attn_prefill": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _I, _P, _I, _F, _S]),
+    "ekv_append_kv": (_I, [ctypes.POINTER(Pool), _P, _P, _P, _I, _S]),
+    "ekv_demote": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _I, _I, _P, _P, _S]),
+    "ekv_refine": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _P, _S]),
+    "ekv_check_transition": (_I, [_I, _P, _I, _P, _P, _P, _I, _I, _I, _I, _P]),
+}
+
+_lib = None
+
+
+def lib():
+    """The loaded library; raises EkvError if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise EkvError(ERR_HIP, f"{LIB_PATH} not built (run __graft_entry__.build())")
+        handle = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in SIGNATURES.items():
+            fn = getattr(handle, name)
+            fn.restype, fn.argtypes = res, args
+        _lib = handle
+    return _lib
+
+
+def _check(status):
+    if status != OK:
+        L = lib()
+        raise EkvError(status, f"{L.ekv_status_string(status).decode()}: {L.ekv_last_error().decode()}")
+
+
+def _ptr(t):
+    """Device pointer of a contiguous torch tensor, or None."""
+    if t is None:
+        return None
+    if not t.is_contiguous():
+        raise EkvError(ERR_INVALID, "tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _host(a, dtype):
+    a = np.ascontiguousarray(a, dtype=dtype)
+    return a, a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _stream(stream):
+    import torch
+    s = stream if stream is not None else torch.cuda.current_stream()
+    return ctypes.c_void_p(s.cuda_stream)
+
+
+def dtype_code(torch_dtype):
+    import torch
+    return {torch.bfloat16: DTYPE_BF16, torch.float16: DTYPE_FP16, torch.float32: DTYPE_FP32}[torch_dtype]
+
+
+def make_pool(kv, num_kv_heads, dtype_name="bf16"):
+    """Describe a device pool tensor of 16-bit words [NB][2][Hkv][16][128]."""
+    nb = kv.numel() // (2 * num_kv_heads * PAGE * HEAD_DIM)
+    code = {"bf16": DTYPE_BF16, "fp16": DTYPE_FP16}[dtype_name]
+    return Pool(_ptr(kv), nb, num_kv_heads, PAGE, HEAD_DIM, code)
+
+
+def make_batch(seq_lens, block_table, tags, boundaries, num_q_heads, mode, max_seq_len=0):
+    """Describe a batch; the tensors are device int32/uint8 arrays."""
+    bsz, max_blocks = block_table.shape
+    return Batch(bsz, num_q_heads, max_blocks, mode, int(max_seq_len), _ptr(seq_lens),
+                 _ptr(block_table), _ptr(tags), _ptr(boundaries))
+
+
+def lower(tags, seq_lens, page=PAGE):
+    """Host lowering: returns (mode, boundaries int32 [B][2])."""
+    tags, tp = _host(tags, np.uint8)
+    seq_lens, sp = _host(seq_lens, np.int32)
+    bsz, max_blocks = tags.shape
+    bounds = np.zeros((bsz, 2), dtype=np.int32)
+    mode = ctypes.c_int32(-1)
+    _check(lib().ekv_lower(tp, sp, bsz, max_blocks, page, ctypes.byref(mode),
+                           bounds.ctypes.data_as(ctypes.c_void_p)))
+    return mode.value, bounds
+
+
+def decode_workspace_bytes(pool, batch):
+    return lib().ekv_decode_workspace_bytes(ctypes.byref(pool), ctypes.byref(batch))
+
+
+def attn_decode(pool, batch, q, out, scale, ws, stream=None):
+    _check(lib().ekv_attn_decode(ctypes.byref(pool), ctypes.byref(batch), _ptr(q), _ptr(out),
+                                 dtype_code(out.dtype), scale, _ptr(ws), ws.numel() * ws.element_size(),
+                                 _stream(stream)))
+
+
+def attn_prefill(pool, batch, q, cu_q, max_q_len, out, scale, stream=None):
+    _check(lib().ekv_attn_prefill(ctypes.byref(pool), ctypes.byref(batch), _ptr(q), _ptr(cu_q),
+                                  q.shape[0], int(max_q_len), _ptr(out), dtype_code(out.dtype), scale,
+                                  _stream(stream)))
+
+
+def append_kv(pool, slots, k, v, stream=None):
+    _check(lib().ekv_append_kv(ctypes.byref(pool), _ptr(slots), _ptr(k), _ptr(v), slots.numel(),
+                               _stream(stream)))
+
+
+def demote(pool, pairs, block_table, tags, freed_out, lo_out=None, stream=None):
+    bsz, max_blocks = block_table.shape
+    _check(lib().ekv_demote(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(block_table),
+                            _ptr(tags), bsz, max_blocks, _ptr(freed_out), _ptr(lo_out), _stream(stream)))
+
+
+def refine(pool, pairs, new_blocks, block_table, tags, lo_in, stream=None):
+    bsz, max_blocks = block_table.shape
+    _check(lib().ekv_refine(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(new_blocks),
+                            _ptr(block_table), _ptr(tags), bsz, max_blocks, _ptr(lo_in), _stream(stream)))
+
+
+def check_transition(kind, pairs, block_table, tags, seq_lens, num_blocks, new_blocks=None, page=PAGE):
+    """Host validation of a demotion (kind 0) or refinement (kind 1) list.
+    Returns (ok: bool, message: str)."""
+    pairs, pp = _host(np.asarray(pairs).reshape(-1, 2), np.int32)
+    bt, bp = _host(block_table, np.int32)
+    tg, tgp = _host(tags, np.uint8)
+    sl, sp = _host(seq_lens, np.int32)
+    nbp = None
+    if new_blocks is not None:
+        nbk, nbp = _host(new_blocks, np.int32)
+    status = lib().ekv_check_transition(kind, pp, pairs.shape[0], bp, tgp, sp, bt.shape[0],
+                                        bt.shape[1], page, num_blocks, nbp)
+    return status == OK, (lib().ekv_last_error().decode() if status != OK else "")

@@ -1,0 +1,151 @@
+"""Host-side state of a mixed-fidelity paged KV pool and its device arrays.
+
+``HostMirror`` is the host copy of the per-block state the paper keeps in
+its block-state table (App. B.1): block table, fidelity tags, sequence
+lengths and the free-block pool.  It validates transition lists through
+``ekv_check_transition``, applies the same table updates the device
+kernels make, and returns freed blocks to the pool only when the caller
+says the GPU work has completed (App. B.2: commit after completion).
+
+Free-pool order (the paper fixes none): unused ids start in ascending
+order; freed blocks are appended in list order at commit; refinement takes
+new blocks from the head.
+
+``PagedKV`` couples a mirror with the device tensors and drives the C ABI
+through :mod:`ekv`.
+"""
+
+from collections import deque
+
+import numpy as np
+
+from . import ekv
+
+
+class HostMirror:
+    def __init__(self, block_table, seq_lens, num_blocks, free_ids, tags=None, page=ekv.PAGE):
+        self.bt = np.array(block_table, dtype=np.int32, copy=True)
+        self.seq_lens = np.array(seq_lens, dtype=np.int32, copy=True)
+        self.tags = (np.zeros_like(self.bt, dtype=np.uint8) if tags is None
+                     else np.array(tags, dtype=np.uint8, copy=True))
+        self.num_blocks = int(num_blocks)
+        self.page = page
+        self.free = deque(int(b) for b in sorted(free_ids))
+
+    def _validate(self, kind, pairs, new_blocks=None):
+        ok, msg = ekv.check_transition(kind, pairs, self.bt, self.tags, self.seq_lens,
+                                       self.num_blocks, new_blocks, self.page)
+        if not ok:
+            raise ekv.EkvError(ekv.ERR_INVALID, msg)
+
+    def plan_demote(self, pairs):
+        """Validate and apply a demotion list; returns the blocks it frees
+        (not yet back in the free pool)."""
+        pairs = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
+        self._validate(0, pairs)
+        freed = np.empty(len(pairs), dtype=np.int32)
+        for i, (s, j) in enumerate(pairs):
+            freed[i] = self.bt[s, 2 * j + 1]
+            self.bt[s, 2 * j + 1] = self.bt[s, 2 * j]
+            self.tags[s, 2 * j] = self.tags[s, 2 * j + 1] = 1
+        return freed
+
+    def commit_freed(self, freed):
+        """Return demoted pairs' released blocks once the GPU has finished."""
+        self.free.extend(int(b) for b in freed)
+
+    def plan_refine(self, pairs):
+        """Validate a refinement list, take one block per pair from the free
+        pool and apply the table update; returns the new blocks."""
+        pairs = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
+        n = len(pairs)
+        if n > len(self.free):
+            raise ekv.EkvError(ekv.ERR_INVALID, "not enough free blocks for refinement")
+        new = np.array([self.free.popleft() for _ in range(n)], dtype=np.int32)
+        try:
+            self._validate(1, pairs, new)
+        except ekv.EkvError:
+            self.free.extendleft(reversed(new.tolist()))
+            raise
+        for i, (s, j) in enumerate(pairs):
+            self.bt[s, 2 * j + 1] = new[i]
+            self.tags[s, 2 * j] = self.tags[s, 2 * j + 1] = 0
+        return new
+
+    def lower(self):
+        return ekv.lower(self.tags, self.seq_lens, self.page)
+
+
+class PagedKV:
+    """Device pool + block table + tags + lengths, with a HostMirror."""
+
+    def __init__(self, pool_words, block_table, seq_lens, free_ids, num_kv_heads, dtype="bf16",
+                 device="cuda"):
+        import torch
+        kv = pool_words if isinstance(pool_words, torch.Tensor) else torch.from_numpy(
+            np.ascontiguousarray(pool_words).view(np.int16))
+        self.kv = kv.to(device).contiguous()
+        self.num_kv_heads = num_kv_heads
+        self.dtype = dtype
+        nb = self.kv.numel() // (2 * num_kv_heads * ekv.PAGE * ekv.HEAD_DIM)
+        self.mirror = HostMirror(block_table, seq_lens, nb, free_ids)
+        self.bt = torch.from_numpy(self.mirror.bt.copy()).to(device)
+        self.tags = torch.from_numpy(self.mirror.tags.copy()).to(device)
+        self.seq_lens = torch.from_numpy(self.mirror.seq_lens.copy()).to(device)
+        self.bounds = torch.zeros((len(self.mirror.seq_lens), 2), dtype=torch.int32, device=device)
+        self.pool = ekv.make_pool(self.kv, num_kv_heads, dtype)
+        self.device = device
+        self.mode = ekv.MODE_NATIVE
+
+    @property
+    def block_bytes(self):
+        return 2 * self.num_kv_heads * ekv.PAGE * ekv.HEAD_DIM * 2
+
+    def relower(self):
+        """Recompute the dispatch metadata from the host mirror and upload it."""
+        import torch
+        self.mode, bounds = self.mirror.lower()
+        self.bounds.copy_(torch.from_numpy(bounds))
+        return self.mode
+
+    def batch(self, num_q_heads, mode=None, use_boundaries=True, max_seq_len=None):
+        mode = self.mode if mode is None else mode
+        if max_seq_len is None:
+            max_seq_len = int(self.mirror.seq_lens.max()) if len(self.mirror.seq_lens) else 0
+        return ekv.make_batch(self.seq_lens, self.bt, self.tags,
+                              self.bounds if use_boundaries else None, num_q_heads, mode, max_seq_len)
+
+    def demote(self, pairs, emit_lo=True, stream=None):
+        """Enqueue a demotion; returns (freed ids on device, lo bytes, host freed ids).
+        The freed ids return to the free pool at :meth:`commit`."""
+        import torch
+        host_freed = self.mirror.plan_demote(pairs)
+        n = len(host_freed)
+        pairs_d = torch.from_numpy(np.asarray(pairs, dtype=np.int32).reshape(-1, 2).copy()).to(self.device)
+        freed = torch.empty(n, dtype=torch.int32, device=self.device)
+        lo = torch.empty((n, self.block_bytes), dtype=torch.uint8, device=self.device) if emit_lo else None
+        ekv.demote(self.pool, pairs_d, self.bt, self.tags, freed, lo, stream)
+        ev = torch.cuda.Event()
+        ev.record(stream)
+        self._pending = getattr(self, "_pending", []) + [(ev, host_freed)]
+        return freed, lo, host_freed
+
+    def commit(self):
+        """Return blocks freed by completed demotions to the free pool."""
+        keep = []
+        for ev, ids in getattr(self, "_pending", []):
+            ev.synchronize()
+            self.mirror.commit_freed(ids)
+        self._pending = keep
+
+    def refine(self, pairs, lo, stream=None):
+        """Enqueue a refinement of BASE pairs from their refinement bytes."""
+        import torch
+        new = self.mirror.plan_refine(pairs)
+        pairs_d = torch.from_numpy(np.asarray(pairs, dtype=np.int32).reshape(-1, 2).copy()).to(self.device)
+        new_d = torch.from_numpy(new).to(self.device)
+        ekv.refine(self.pool, pairs_d, new_d, self.bt, self.tags, lo, stream)
+        return new
+
+    def append(self, slots, k, v, stream=None):
+        ekv.append_kv(self.pool, slots, k, v, stream)
