@@ -123,9 +123,21 @@ ekv_status ekv_lower(const uint8_t* h_tags, const int32_t* h_seq_lens, int32_t b
 
 /*
  * Bytes of device scratch that ekv_attn_decode needs for this pool and
- * batch (split-KV partial results).  Returns 0 for unsupported shapes.
+ * batch: split-KV partial results plus one merge counter per (sequence,
+ * KV head).  Returns 0 for unsupported shapes.
  */
 size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch);
+
+/*
+ * Prepare a decode workspace for first use: fills ws_bytes bytes of ws
+ * with zeros on the stream (a kernel, not a memset).  The merge counters
+ * must read zero when a decode starts; every decode call leaves them at
+ * zero, so this is needed once after allocation (or after ws was used for
+ * anything else).  A zero-filled allocation needs no call.
+ * Errors: EKV_ERR_INVALID (NULL ws with nonzero size, size not a multiple
+ * of 4), EKV_ERR_HIP.
+ */
+ekv_status ekv_decode_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream);
 
 /*
  * Decode attention, one query token per sequence (§3.2; App. B.3): for
@@ -138,7 +150,9 @@ size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch);
  * uses its boundaries and any other sequence reads its tags.
  *   q    device [batch][num_q_heads][head_dim], pool dtype
  *   out  device [batch][num_q_heads][head_dim], out_dtype = pool dtype or EKV_DTYPE_FP32
- *   ws   device scratch of at least ekv_decode_workspace_bytes() bytes
+ *   ws   device scratch of at least ekv_decode_workspace_bytes() bytes,
+ *        prepared by ekv_decode_workspace_init (or zero-filled) before its
+ *        first use; calls sharing one ws must be ordered on one stream
  * A sequence of length 0 yields zeros.
  * Errors: EKV_ERR_INVALID (NULL pointers, sizes, workspace too small,
  * NATIVE mode expected but tags needed), EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.

@@ -75,21 +75,23 @@ int max_seq_blocks(const ekv_batch* b) {
 }
 
 // Blocks per split: the smallest power of two >= 8 that keeps the launch at
-// or under ~16k work items (64 per CU), unless EKV_SPLIT_BLOCKS overrides.
+// or under ~8k work items (32 per CU), unless EKV_SPLIT_BLOCKS overrides;
+// never more than kMaxSplitBlocks.
 int plan_split_blocks(int batch, int hkv, int nblk_max) {
   if (const char* env = getenv("EKV_SPLIT_BLOCKS")) {
     const int v = atoi(env);
-    if (v > 0) return v;
+    if (v > 0) return std::min((v + 1) & ~1, ekv::kMaxSplitBlocks);   // even: pairs never straddle splits
   }
   const long long items = (long long)batch * hkv;
   int sb = 8;
-  while (sb < 1024 && items * ((nblk_max + sb - 1) / sb) > 16384) sb *= 2;
+  while (sb < ekv::kMaxSplitBlocks && items * ((nblk_max + sb - 1) / sb) > 8192) sb *= 2;
   return sb;
 }
 
+// Workspace: [merge counters u32 B*Hkv | (m, l) f32 rows | o f32 rows], 256-B aligned parts.
 struct DecodePlan {
   int split_blocks, max_splits;
-  size_t o_bytes, ml_offset, total;
+  size_t ml_offset, o_offset, total;
 };
 
 DecodePlan plan_decode(const ekv_pool* p, const ekv_batch* b) {
@@ -98,9 +100,10 @@ DecodePlan plan_decode(const ekv_pool* p, const ekv_batch* b) {
   d.split_blocks = plan_split_blocks(b->batch, p->num_kv_heads, nblk);
   d.max_splits = std::max(1, (nblk + d.split_blocks - 1) / d.split_blocks);
   const size_t rows = (size_t)b->batch * b->num_q_heads * d.max_splits;
-  d.o_bytes = rows * ekv::kHeadDim * sizeof(float);
-  d.ml_offset = (d.o_bytes + 255) & ~(size_t)255;
-  d.total = d.ml_offset + rows * 2 * sizeof(float);
+  auto align = [](size_t x) { return (x + 255) & ~(size_t)255; };
+  d.ml_offset = align((size_t)b->batch * p->num_kv_heads * sizeof(uint32_t));
+  d.o_offset = align(d.ml_offset + rows * 2 * sizeof(float));
+  d.total = d.o_offset + rows * ekv::kHeadDim * sizeof(float);
   return d;
 }
 
@@ -172,6 +175,13 @@ size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch) 
   return plan_decode(pool, batch).total;
 }
 
+ekv_status ekv_decode_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
+  if (!ws && ws_bytes) return fail(EKV_ERR_INVALID, "ws is NULL");
+  if (ws_bytes % 4) return fail(EKV_ERR_INVALID, "ws_bytes must be a multiple of 4");
+  return hip_status(ekv::launch_zero_u32(static_cast<uint32_t*>(ws), ws_bytes / 4, stream),
+                    "ekv_decode_workspace_init launch");
+}
+
 ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out,
                            int32_t out_dtype, float scale, void* ws, size_t ws_bytes,
                            hipStream_t stream) {
@@ -194,8 +204,9 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
   a.bt = batch->block_table;
   a.tags = batch->tags;
   a.bounds = batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries;
-  a.ws_o = static_cast<float*>(ws);
+  a.counters = static_cast<uint32_t*>(ws);
   a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.ml_offset);
+  a.ws_o = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.o_offset);
   a.out = out;
   a.batch = batch->batch;
   a.num_kv_heads = pool->num_kv_heads;
@@ -204,6 +215,8 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
   a.split_blocks = plan.split_blocks;
   a.max_splits = plan.max_splits;
   a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
+  a.slots = 3;
+  if (const char* env = getenv("EKV_DECODE_SLOTS")) a.slots = std::max(3, std::min(6, atoi(env)));
   a.scale_log2 = log2e_scale(scale);
   return hip_status(ekv::launch_decode(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
                     "ekv_attn_decode launch");

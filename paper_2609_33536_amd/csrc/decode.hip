@@ -7,15 +7,23 @@
 // an online softmax, and accumulates O^T += V^T P^T with 16x16x16 MFMAs.
 //
 // Lane (n, g) = (lane & 15, lane >> 4):
-//   QK   A operand: token n of the block, head-dim chunk 4*step + g (8 elems)
+//   QK   A operand: token n of the block, head-dim chunk 4*g + step (8 elems)
 //        B operand: query head n of the group, same chunk (zero if n >= G)
 //        result:    scores of head n for tokens 4g .. 4g+3
 //   PV   A operand: V[4g+i][8n + j] for i = 0..3 (MFMA j = 0..7)
 //        B operand: the lane's own 4 probabilities (no shuffle needed)
 //        result:    O[head n][d], d = 32g + 8r + j, r = 0..3
-// so each lane loads 4 x 16 B of K and 4 x 16 B of V per TARGET block (half
-// that per BASE block), every load instruction of the wave reading whole
-// 256 B token rows (V) or 64 B row segments (K).
+// K/V move HBM -> LDS with direct-to-LDS loads (global_load_lds_dwordx4),
+// each instruction one coalesced 1 KiB, into a per-wave ring of NSLOT 8 KiB
+// slots.  A slot holds the (K, V) 4 KiB tiles of one physical block for this
+// KV head: either one TARGET block or one whole packed BASE pair (the pair
+// layout puts both members' bytes in exactly one tile per plane), so every
+// slot costs the same 8 load instructions and bytes whatever its mode, and
+// NSLOT-1 slots stay in flight while one is consumed.  The lane -> address
+// map of the loads stores each 16 B chunk at an XOR-swizzled position so
+// the MFMA-layout ds_read_b128 / ds_read_b64 reads below hit distinct banks.
+// The compiler does not track LDS written by these loads, so the ring waits
+// on the load counter itself (s_waitcnt vmcnt) before reading a slot.
 //
 // TARGET blocks are used as stored.  BASE blocks are read from the packed
 // pair block (member i & 1) and widened in registers: byte -> high byte of
@@ -27,137 +35,344 @@
 //
 // P is split into a 16-bit head and a 16-bit remainder and both are
 // multiplied with V, so the PV product carries ~16 significant bits of P.
+//
+// Splits of one (sequence, KV head) write fp32 partials (o, max, sum); the
+// wave that finishes last -- found with a per-(sequence, KV head) counter in
+// the workspace -- merges them and writes the output, then resets the
+// counter to zero for the next call.
 #include "common.h"
 #include "launch.h"
 
 namespace ekv {
 namespace {
 
-struct Tile {
-  u32x4 k[4];   // TARGET: 4 x 8 words; BASE: .xy = 8 bytes
-  u32x4 v[4];
+constexpr int kSlotBytes = 2 * kTileBytes;   // K tile + V tile
+
+// XOR swizzle of 16-byte chunks inside an LDS tile.
+//  TARGET tile: 16 token rows x 16 chunks; chunk c of token t sits at c ^ t.
+//  BASE tile: 2 members x 16 rows x 8 chunks; chunk q of token t at q ^ tau(t).
+__device__ __forceinline__ int tau(int t) { return (t & 7) ^ (t >> 3); }
+
+// Byte offsets, within a 4 KiB plane tile in HBM, of the 16 B each lane
+// fetches with load instruction r (LDS destination: r * 1 KiB + 16 * lane).
+struct DmaOffsets {
+  uint32_t tgt[4], base[4];
 };
 
-template <bool BASE>
-__device__ __forceinline__ void load_tile(Tile& t, const uint16_t* ktile, const uint16_t* vtile,
-                                          int member, int n, int g) {
-  if constexpr (BASE) {
-    const uint8_t* kb = reinterpret_cast<const uint8_t*>(ktile) + member * (kTileBytes / 2);
-    const uint8_t* vb = reinterpret_cast<const uint8_t*>(vtile) + member * (kTileBytes / 2);
+__device__ __forceinline__ DmaOffsets dma_offsets(int lane) {
+  DmaOffsets o;
 #pragma unroll
-    for (int st = 0; st < 4; ++st) {
-      u32x2 x = *reinterpret_cast<const u32x2*>(kb + n * kHeadDim + 8 * (4 * st + g));
-      t.k[st] = u32x4{x.x, x.y, 0u, 0u};
-    }
+  for (int r = 0; r < 4; ++r) {
+    const int p = 64 * r + lane;                 // LDS chunk written by this lane
+    const int t = p >> 4, pos = p & 15;
+    o.tgt[r] = t * (2 * kHeadDim) + 16 * (pos ^ t);
+    const int m = p >> 7, tb = (p >> 3) & 15, posb = p & 7;
+    o.base[r] = m * (kTileBytes / 2) + tb * kHeadDim + 16 * (posb ^ tau(tb));
+  }
+  return o;
+}
+
+typedef __attribute__((address_space(3))) void* lds_ptr;
+
+__device__ __forceinline__ void dma_tile(const char* src, const uint32_t (&off)[4], char* dst) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off[r]),
+                                     (lds_ptr)(dst + 1024 * r), 16, 0, 0);
+}
+
+// Wait until at most `ahead` slots (8 loads each) are still in flight.
+__device__ __forceinline__ void wait_slots(int ahead) {
+  switch (ahead) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
+  }
+}
+
+struct SplitState {
+  f32x4 o[8];
+  float m;   // reference max, log2 units (same in the 4 lanes of a head)
+  float l;   // running sum, partial per lane
+};
+
+// max / sum over the four lanes of one head (lanes l, l^16, l^32, l^48)
+__device__ __forceinline__ float head_max(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+
+__device__ __forceinline__ float head_sum(float x) {
+  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
+}
+
+// PV A operand for MFMA j (head-dim row 8n + j): the lane's 4 tokens, as
+// 16-bit words.  TARGET rows hold 8 words per token, BASE rows 8 bytes.
+template <bool BASE>
+__device__ __forceinline__ u32x2 v_operand(const u32x4 (&v)[4], int j) {
+  if constexpr (BASE) {
+    const int b = j & 3;
+    const uint32_t sel = 0x0Cu | ((uint32_t)b << 8) | (0x0Cu << 16) | ((uint32_t)(4 + b) << 24);
+    const int w = j >> 2;
+    return u32x2{perm(v[1][w], v[0][w], sel), perm(v[3][w], v[2][w], sel)};
+  } else {
+    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
+    return u32x2{perm(v[1][j >> 1], v[0][j >> 1], sel), perm(v[3][j >> 1], v[2][j >> 1], sel)};
+  }
+}
+
+// Scores of one 16-token group: S^T = K Q^T, lane gets tokens 4g..4g+3 of head n.
+template <typename T, bool BASE>
+__device__ __forceinline__ f32x4 qk_scores(const u32x4 (&k)[4], const u32x4 (&qop)[4]) {
+  f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int st = 0; st < 4; ++st) {
+    u32x4 kop;
+    if constexpr (BASE) kop = expand_base8(k[st].xy);
+    else kop = k[st];
+    s = Mma<T>::qk(kop, qop[st], s);
+  }
+  return s;
+}
+
+// Online-softmax update for NG 16-token groups of one slot followed by
+// O += V^T P^T.  The reference max only moves (and O, l are rescaled) when
+// some head's block max exceeds it by more than 2^8; otherwise P <= 2^8.
+// P is split into a 16-bit head and remainder, stacked along k of one
+// 16x16x32 MFMA against the duplicated V operand.
+template <typename T, bool BASE, int NG>
+__device__ __forceinline__ void softmax_pv(SplitState& st, f32x4 (&s)[NG], u32x4 (&v)[NG][4], int tok0,
+                                           int len, float scale_log2, int g) {
+  float sc[NG][4];
+#pragma unroll
+  for (int q = 0; q < NG; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sc[q][i] = s[q][i] * scale_log2;
+  if (tok0 + NG * kPage > len) {   // the sequence ends inside this slot (a TARGET block)
+#pragma unroll
+    for (int q = 0; q < NG; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (tok0 + q * kPage + 4 * g + i >= len) {
+          sc[q][i] = -__builtin_inff();
+          v[q][i] = u32x4{0u, 0u, 0u, 0u};
+        }
+  }
+  float mx = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
+#pragma unroll
+  for (int q = 1; q < NG; ++q) mx = fmaxf(mx, fmaxf(fmaxf(sc[q][0], sc[q][1]), fmaxf(sc[q][2], sc[q][3])));
+  mx = head_max(mx);
+  if (__builtin_amdgcn_ballot_w64(mx > st.m + 8.0f)) {
+    const float m_new = fmaxf(st.m, mx);
+    const float alpha = fast_exp2(st.m - m_new);
+    st.l *= alpha;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) st.o[j] *= alpha;
+    st.m = m_new;
+  }
+#pragma unroll
+  for (int q = 0; q < NG; ++q) {
+    float p[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sc[q][i] - st.m);
+    st.l += (p[0] + p[1]) + (p[2] + p[3]);
+    uint16_t ph[4], pl[4];
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      u32x2 x = *reinterpret_cast<const u32x2*>(vb + (4 * g + i) * kHeadDim + 8 * n);
-      t.v[i] = u32x4{x.x, x.y, 0u, 0u};
+      float back, dummy;
+      ph[i] = Mma<T>::round(p[i], &back);
+      pl[i] = Mma<T>::round(p[i] - back, &dummy);
     }
+    const u32x4 pb = {(uint32_t)ph[0] | ((uint32_t)ph[1] << 16), (uint32_t)ph[2] | ((uint32_t)ph[3] << 16),
+                      (uint32_t)pl[0] | ((uint32_t)pl[1] << 16), (uint32_t)pl[2] | ((uint32_t)pl[3] << 16)};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      const u32x2 a = v_operand<BASE>(v[q], j);
+      st.o[j] = Mma<T>::qk(u32x4{a.x, a.y, a.x, a.y}, pb, st.o[j]);
+    }
+  }
+}
+
+__device__ __forceinline__ void store_agent_f2(float* p, float a, float b) {
+  const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
+  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ float2 load_agent_f2(const float* p) {
+  const uint64_t v = __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED,
+                                       __HIP_MEMORY_SCOPE_AGENT);
+  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
+}
+
+template <typename T>
+__device__ __forceinline__ void store_row8(void* out, size_t idx, f32x4 a, f32x4 b, bool fp32) {
+  if (fp32) {
+    float* dst = reinterpret_cast<float*>(out) + idx;
+    *reinterpret_cast<f32x4*>(dst) = a;
+    *reinterpret_cast<f32x4*>(dst + 4) = b;
   } else {
-#pragma unroll
-    for (int st = 0; st < 4; ++st)
-      t.k[st] = *reinterpret_cast<const u32x4*>(ktile + n * kHeadDim + 8 * (4 * st + g));
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      t.v[i] = *reinterpret_cast<const u32x4*>(vtile + (4 * g + i) * kHeadDim + 8 * n);
+    float x;
+    uint32_t w[4];
+    w[0] = (uint32_t)Mma<T>::round(a[0], &x) | ((uint32_t)Mma<T>::round(a[1], &x) << 16);
+    w[1] = (uint32_t)Mma<T>::round(a[2], &x) | ((uint32_t)Mma<T>::round(a[3], &x) << 16);
+    w[2] = (uint32_t)Mma<T>::round(b[0], &x) | ((uint32_t)Mma<T>::round(b[1], &x) << 16);
+    w[3] = (uint32_t)Mma<T>::round(b[2], &x) | ((uint32_t)Mma<T>::round(b[3], &x) << 16);
+    *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(out) + idx) = u32x4{w[0], w[1], w[2], w[3]};
   }
 }
 
 template <typename T>
-struct SplitState {
-  f32x4 o[8];
-  float m;   // running max, log2 units (same in the 4 lanes of a head)
-  float l;   // running sum, partial per lane
-};
-
-template <typename T, bool BASE>
-__device__ __forceinline__ void consume_tile(SplitState<T>& st, Tile& t, const u32x4 (&qop)[4],
-                                             int tok0, int len, float scale_log2) {
-  // scores S^T[token][head]
-  f32x4 s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int k = 0; k < 4; ++k) {
-    u32x4 kop;
-    if constexpr (BASE) kop = expand_base8(u32x2{t.k[k].x, t.k[k].y});
-    else kop = t.k[k];
-    s = Mma<T>::qk(kop, qop[k], s);
-  }
-  float sc[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) sc[i] = (tok0 + i < len) ? s[i] * scale_log2 : -__builtin_inff();
-  float mx = fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3]));
-  mx = fmaxf(mx, __shfl_xor(mx, 16));
-  mx = fmaxf(mx, __shfl_xor(mx, 32));
-  const float m_new = fmaxf(st.m, mx);
-  const float alpha = fast_exp2(st.m - m_new);
-  float p[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sc[i] - m_new);
-  st.l = st.l * alpha + ((p[0] + p[1]) + (p[2] + p[3]));
-  st.m = m_new;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) st.o[j] *= alpha;
-
-  // P = head + remainder, both as 16-bit operands
-  uint16_t ph[4], pl[4];
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    float back, dummy;
-    ph[i] = Mma<T>::round(p[i], &back);
-    pl[i] = Mma<T>::round(p[i] - back, &dummy);
-  }
-  const u32x2 phi = {(uint32_t)ph[0] | ((uint32_t)ph[1] << 16), (uint32_t)ph[2] | ((uint32_t)ph[3] << 16)};
-  const u32x2 plo = {(uint32_t)pl[0] | ((uint32_t)pl[1] << 16), (uint32_t)pl[2] | ((uint32_t)pl[3] << 16)};
-
-  // tokens past the end of the sequence may hold anything: zero their V
-  if (len - (tok0 & ~15) < kPage) {
-#pragma unroll
-    for (int i = 0; i < 4; ++i)
-      if (tok0 + i >= len) t.v[i] = u32x4{0u, 0u, 0u, 0u};
-  }
-
-#pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    u32x2 vop;
-    if constexpr (BASE) {
-      // byte j of the lane's 8-byte row segment, for tokens 4g .. 4g+3
-      const int b = j & 3;
-      const uint32_t sel = 0x0Cu | ((uint32_t)b << 8) | (0x0Cu << 16) | ((uint32_t)(4 + b) << 24);
-      const uint32_t w0 = (j < 4) ? t.v[0].x : t.v[0].y;
-      const uint32_t w1 = (j < 4) ? t.v[1].x : t.v[1].y;
-      const uint32_t w2 = (j < 4) ? t.v[2].x : t.v[2].y;
-      const uint32_t w3 = (j < 4) ? t.v[3].x : t.v[3].y;
-      vop = u32x2{perm(w1, w0, sel), perm(w3, w2, sel)};
-    } else {
-      // 16-bit element j of the lane's 8-element row segment
-      const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-      vop = u32x2{perm(t.v[1][j >> 1], t.v[0][j >> 1], sel), perm(t.v[3][j >> 1], t.v[2][j >> 1], sel)};
-    }
-    st.o[j] = Mma<T>::pv(vop, phi, st.o[j]);
-    st.o[j] = Mma<T>::pv(vop, plo, st.o[j]);
+__device__ __forceinline__ void store_pair(void* out, size_t idx, float a, float b, bool fp32) {
+  if (fp32) {
+    *reinterpret_cast<float2*>(reinterpret_cast<float*>(out) + idx) = make_float2(a, b);
+  } else {
+    float x;
+    *reinterpret_cast<uint32_t*>(reinterpret_cast<uint16_t*>(out) + idx) =
+        (uint32_t)Mma<T>::round(a, &x) | ((uint32_t)Mma<T>::round(b, &x) << 16);
   }
 }
 
-template <typename T, int G, bool ELASTIC>
-__global__ __launch_bounds__(64) void decode_split_kernel(DecodeArgs a) {
+
+__device__ __forceinline__ f32x4 load_agent_f4(const float* p) {
+  const float2 a = load_agent_f2(p), b = load_agent_f2(p + 2);
+  return f32x4{a.x, a.y, b.x, b.y};
+}
+
+__device__ __forceinline__ float wave_max(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
+  return x;
+}
+
+__device__ __forceinline__ float wave_sum(float x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+// Merge the nsplit (<= 64) partials of the G heads of one (sequence, KV
+// head): out = sum_k w_k o_k / sum_k w_k l_k with w_k = exp2(m_k - max m).
+// Lane k holds split k's weight; for the numerators lane (c, par) =
+// (lane & 31, lane >> 5) owns head-dim columns 4c..4c+3 of the splits with
+// parity par, and keeps up to 16 coherent loads in flight at a time.
+template <typename T, int G>
+__device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int lane) {
+  constexpr int kB = G >= 16 ? 1 : 16 / G;     // split pairs per batch
+  float wk[G], inv_den[G];
+  f32x4 num[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float* ml = a.ws_ml + 2 * (head0 + h) * a.max_splits;
+    const float2 mlk = lane < nsplit ? load_agent_f2(ml + 2 * lane) : make_float2(-__builtin_inff(), 0.f);
+    const float mmax = wave_max(mlk.x);
+    wk[h] = lane < nsplit ? fast_exp2(mlk.x - mmax) : 0.f;
+    inv_den[h] = 1.0f / wave_sum(wk[h] * mlk.y);
+    num[h] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  const int c = lane & 31, par = lane >> 5;
+  for (int k0 = 0; k0 < nsplit; k0 += 2 * kB) {
+    f32x4 v[G][kB];
+#pragma unroll
+    for (int h = 0; h < G; ++h) {
+      const float* o = a.ws_o + (head0 + h) * a.max_splits * kHeadDim + 4 * c;
+#pragma unroll
+      for (int b = 0; b < kB; ++b) {
+        const int k = k0 + 2 * b + par;
+        v[h][b] = k < nsplit ? load_agent_f4(o + (size_t)k * kHeadDim) : f32x4{0.f, 0.f, 0.f, 0.f};
+      }
+    }
+#pragma unroll
+    for (int h = 0; h < G; ++h)
+#pragma unroll
+      for (int b = 0; b < kB; ++b) {
+        const int k = k0 + 2 * b;
+        const float w0 = k < 64 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[h]), k)) : 0.f;
+        const float w1 = k + 1 < 64 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[h]), k + 1)) : 0.f;
+        num[h] += (par ? w1 : w0) * v[h][b];
+      }
+  }
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    f32x4 tot;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(num[h][e]), __float_as_uint(num[h][e]),
+                                                       false, false);
+      tot[e] = (__uint_as_float(sw[0]) + __uint_as_float(sw[1])) * inv_den[h];
+    }
+    if (par == 0) {
+      const size_t idx = (head0 + h) * kHeadDim + 4 * c;
+      store_pair<T>(a.out, idx, tot[0], tot[1], a.out_fp32);
+      store_pair<T>(a.out, idx + 2, tot[2], tot[3], a.out_fp32);
+    }
+  }
+}
+
+// Any number of splits, one head at a time (long sequences only).
+template <typename T>
+__device__ void merge_head_serial(const DecodeArgs& a, size_t head, int nsplit, int lane) {
+  const float* ml = a.ws_ml + 2 * head * a.max_splits;
+  const float* o = a.ws_o + head * a.max_splits * kHeadDim + 2 * lane;
+  float mmax = -__builtin_inff();
+  for (int k0 = 0; k0 < nsplit; k0 += 64)
+    if (k0 + lane < nsplit) mmax = fmaxf(mmax, load_agent_f2(ml + 2 * (k0 + lane)).x);
+  mmax = wave_max(mmax);
+  float den = 0.f, num0 = 0.f, num1 = 0.f;
+  for (int k0 = 0; k0 < nsplit; k0 += 64) {
+    float wk = 0.f;
+    if (k0 + lane < nsplit) {
+      const float2 mlk = load_agent_f2(ml + 2 * (k0 + lane));
+      wk = fast_exp2(mlk.x - mmax);
+      den += wk * mlk.y;
+    }
+    const int kn = min(64, nsplit - k0);
+    for (int k = 0; k < kn; ++k) {
+      const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk), k));
+      const float2 v = load_agent_f2(o + (size_t)(k0 + k) * kHeadDim);
+      num0 += w * v.x;
+      num1 += w * v.y;
+    }
+  }
+  const float inv = 1.0f / wave_sum(den);
+  store_pair<T>(a.out, head * kHeadDim + 2 * lane, num0 * inv, num1 * inv, a.out_fp32);
+}
+
+template <typename T, int G, bool ELASTIC, int NSLOT>
+__global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
+  __shared__ __attribute__((aligned(16))) char smem[NSLOT * kSlotBytes];
   const int s = blockIdx.z;
   const int kvh = blockIdx.y;
   const int split = blockIdx.x;
-  const int len = a.seq_lens[s];
-  const int nblk = (len + kPage - 1) / kPage;
-  const int b_begin = split * a.split_blocks;
-  if (b_begin >= nblk) return;
-  const int b_end = min(nblk, b_begin + a.split_blocks);
-  const int nsplit = (nblk + a.split_blocks - 1) / a.split_blocks;
-
   const int lane = threadIdx.x;
   const int n = lane & 15;
   const int g = lane >> 4;
+  const int len = a.seq_lens[s];
+  const int nblk = (len + kPage - 1) / kPage;
+  const int b_begin = split * a.split_blocks;
+  if (b_begin >= nblk) {
+    if (nblk == 0 && split == 0) {   // empty sequence: zero output
+      for (int h = 0; h < G; ++h)
+        store_pair<T>(a.out, ((size_t)s * a.num_q_heads + kvh * G + h) * kHeadDim + 2 * lane, 0.f, 0.f,
+                      a.out_fp32);
+    }
+    return;
+  }
+  const int b_end = min(nblk, b_begin + a.split_blocks);
+  const int nsplit = (nblk + a.split_blocks - 1) / a.split_blocks;
+
   const int hkv = a.num_kv_heads;
-  const size_t block_words = (size_t)2 * hkv * kTileWords;
-  const uint16_t* pool_k = a.pool + (size_t)kvh * kTileWords;
-  const size_t v_off = (size_t)hkv * kTileWords;
+  const size_t block_bytes = (size_t)2 * hkv * kTileBytes;
+  const char* pool = reinterpret_cast<const char*>(a.pool) + (size_t)kvh * kTileBytes;
+  const size_t v_off = (size_t)hkv * kTileBytes;
   const int32_t* btrow = a.bt + (size_t)s * a.max_blocks;
 
   u32x4 qop[4];
@@ -165,12 +380,17 @@ __global__ __launch_bounds__(64) void decode_split_kernel(DecodeArgs a) {
     const uint16_t* qrow = a.q + ((size_t)s * a.num_q_heads + (size_t)kvh * G + n) * kHeadDim;
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-      qop[k] = (n < G) ? *reinterpret_cast<const u32x4*>(qrow + 8 * (4 * k + g)) : u32x4{0u, 0u, 0u, 0u};
+      qop[k] = (n < G) ? *reinterpret_cast<const u32x4*>(qrow + 8 * (4 * g + k)) : u32x4{0u, 0u, 0u, 0u};
   }
 
-  // per-sequence mode description (wave-uniform)
+  // This split's block-table entries (and tags), one per lane, fetched once;
+  // each block's entry is then read from its lane into a scalar register,
+  // so the block loop issues no memory access other than the K/V loads.
+  const int nb_split = b_end - b_begin;   // <= kMaxSplitBlocks
+  const int bt_lane = lane < nb_split ? btrow[b_begin + lane] : 0;
   int base_lo = 0, base_hi = 0;
-  const uint8_t* tagrow = nullptr;
+  int tag_lane = 0;
+  bool use_tags = false;
   if constexpr (ELASTIC) {
     int b0 = -1, b1 = -1;
     if (a.bounds) {
@@ -180,133 +400,160 @@ __global__ __launch_bounds__(64) void decode_split_kernel(DecodeArgs a) {
     if (b0 >= 0) {
       base_lo = 2 * b0;
       base_hi = 2 * b1;
-    } else {
-      tagrow = a.tags + (size_t)s * a.max_blocks;
+    } else if (a.tags) {
+      use_tags = true;
+      tag_lane = lane < nb_split ? a.tags[(size_t)s * a.max_blocks + b_begin + lane] : 0;
     }
   }
   auto is_base = [&](int blk) -> bool {
     if constexpr (!ELASTIC) return false;
-    else return tagrow ? (tagrow[blk] != 0) : (blk >= base_lo && blk < base_hi);
-  };
-  auto issue = [&](Tile& t, int blk, bool base) {
-    const uint16_t* kt = pool_k + (size_t)btrow[blk] * block_words;
-    if (base) load_tile<true>(t, kt, kt + v_off, blk & 1, n, g);
-    else load_tile<false>(t, kt, kt + v_off, blk & 1, n, g);
+    else return use_tags ? (__builtin_amdgcn_readlane(tag_lane, blk - b_begin) != 0)
+                         : (blk >= base_lo && blk < base_hi);
   };
 
-  SplitState<T> st;
+  // per-lane LDS read offsets (see the swizzle above)
+  uint32_t rk_t[4], rv_t[4], rk_b[2], rv_b[4];
+#pragma unroll
+  for (int k = 0; k < 4; ++k) rk_t[k] = n * (2 * kHeadDim) + 16 * ((4 * g + k) ^ n);
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int t = 4 * g + i;
+    rv_t[i] = kTileBytes + t * (2 * kHeadDim) + 16 * (n ^ t);
+    rv_b[i] = kTileBytes + t * kHeadDim + 16 * ((n >> 1) ^ tau(t)) + 8 * (n & 1);
+  }
+#pragma unroll
+  for (int h = 0; h < 2; ++h) rk_b[h] = n * kHeadDim + 16 * ((2 * g + h) ^ tau(n));
+  const DmaOffsets dma = dma_offsets(lane);
+
+  SplitState st;
 #pragma unroll
   for (int j = 0; j < 8; ++j) st.o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
   st.m = -__builtin_inff();
   st.l = 0.f;
 
-  // software pipeline: the next block's loads are in flight while this one
-  // is consumed (two register buffers, unrolled by two)
-  Tile ta, tb;
-  bool base_a = is_base(b_begin), base_b = false;
-  issue(ta, b_begin, base_a);
-  for (int blk = b_begin; blk < b_end; blk += 2) {
-    const bool has_b = blk + 1 < b_end;
-    if (has_b) {
-      base_b = is_base(blk + 1);
-      issue(tb, blk + 1, base_b);
+  // Q, the block-table entries and tags must land before the ring starts:
+  // the ring's own waits count only K/V loads.
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+
+  int ib = b_begin, cb = b_begin;      // issue / consume cursors (logical blocks)
+  int issued = 0, consumed = 0;        // slots
+  int islot = 0, cslot = 0;            // ring positions
+  auto issue = [&]() {
+    const bool base = is_base(ib);
+    const char* src = pool + (size_t)__builtin_amdgcn_readlane(bt_lane, ib - b_begin) * block_bytes;
+    char* dst = smem + islot * kSlotBytes;
+    if (base) {
+      dma_tile(src, dma.base, dst);
+      dma_tile(src + v_off, dma.base, dst + kTileBytes);
+    } else {
+      dma_tile(src, dma.tgt, dst);
+      dma_tile(src + v_off, dma.tgt, dst + kTileBytes);
     }
-    if (base_a) consume_tile<T, true>(st, ta, qop, blk * kPage + 4 * g, len, a.scale_log2);
-    else consume_tile<T, false>(st, ta, qop, blk * kPage + 4 * g, len, a.scale_log2);
-    if (!has_b) break;
-    const bool has_a = blk + 2 < b_end;
-    if (has_a) {
-      base_a = is_base(blk + 2);
-      issue(ta, blk + 2, base_a);
+    ib += base ? 2 : 1;
+    ++issued;
+    islot = islot + 1 == NSLOT ? 0 : islot + 1;
+  };
+
+#pragma unroll
+  for (int k = 0; k < NSLOT - 1; ++k)
+    if (ib < b_end) issue();
+  while (cb < b_end) {
+    if (ib < b_end) issue();
+    wait_slots(issued - consumed - 1);
+    const char* sb = smem + cslot * kSlotBytes;
+    if (is_base(cb)) {
+      // one packed pair: member 0 = logical block cb, member 1 = cb + 1
+      u32x4 k[2][4], v[2][4];
+      f32x4 sc[2];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const char* mb = sb + m * (kTileBytes / 2);
+        const u32x4 k0 = *reinterpret_cast<const u32x4*>(mb + rk_b[0]);
+        const u32x4 k1 = *reinterpret_cast<const u32x4*>(mb + rk_b[1]);
+        k[m][0].xy = k0.xy;
+        k[m][1].xy = k0.zw;
+        k[m][2].xy = k1.xy;
+        k[m][3].xy = k1.zw;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mb + rv_b[i]);
+        sc[m] = qk_scores<T, true>(k[m], qop);
+      }
+      softmax_pv<T, true, 2>(st, sc, v, cb * kPage, len, a.scale_log2, g);
+      cb += 2;
+    } else {
+      u32x4 k[4], v[1][4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) k[q] = *reinterpret_cast<const u32x4*>(sb + rk_t[q]);
+#pragma unroll
+      for (int i = 0; i < 4; ++i) v[0][i] = *reinterpret_cast<const u32x4*>(sb + rv_t[i]);
+      f32x4 sc[1] = {qk_scores<T, false>(k, qop)};
+      softmax_pv<T, false, 1>(st, sc, v, cb * kPage, len, a.scale_log2, g);
+      cb += 1;
     }
-    if (base_b) consume_tile<T, true>(st, tb, qop, (blk + 1) * kPage + 4 * g, len, a.scale_log2);
-    else consume_tile<T, false>(st, tb, qop, (blk + 1) * kPage + 4 * g, len, a.scale_log2);
+    ++consumed;
+    cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
   }
 
-  float l = st.l;
-  l += __shfl_xor(l, 16);
-  l += __shfl_xor(l, 32);
-  if (n >= G) return;
-  const size_t head = (size_t)s * a.num_q_heads + (size_t)kvh * G + n;
+  const float l = head_sum(st.l);
+  const size_t head0 = (size_t)s * a.num_q_heads + (size_t)kvh * G;
   if (nsplit == 1) {
-    const float inv = 1.0f / l;
-    if (a.out_fp32) {
-      float* dst = reinterpret_cast<float*>(a.out) + head * kHeadDim + 32 * g;
+    if (n < G) {
+      const float inv = 1.0f / l;
 #pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        *reinterpret_cast<f32x4*>(dst + 8 * r) =
-            f32x4{st.o[0][r], st.o[1][r], st.o[2][r], st.o[3][r]} * inv;
-        *reinterpret_cast<f32x4*>(dst + 8 * r + 4) =
-            f32x4{st.o[4][r], st.o[5][r], st.o[6][r], st.o[7][r]} * inv;
-      }
-    } else {
-      uint16_t* dst = reinterpret_cast<uint16_t*>(a.out) + head * kHeadDim + 32 * g;
-#pragma unroll
-      for (int r = 0; r < 4; ++r) {
-        uint32_t w[4];
-#pragma unroll
-        for (int j = 0; j < 8; j += 2) {
-          float b;
-          w[j >> 1] = (uint32_t)Mma<T>::round(st.o[j][r] * inv, &b) |
-                      ((uint32_t)Mma<T>::round(st.o[j + 1][r] * inv, &b) << 16);
-        }
-        *reinterpret_cast<u32x4*>(dst + 8 * r) = u32x4{w[0], w[1], w[2], w[3]};
-      }
+      for (int r = 0; r < 4; ++r)
+        store_row8<T>(a.out, (head0 + n) * kHeadDim + 32 * g + 8 * r,
+                      f32x4{st.o[0][r], st.o[1][r], st.o[2][r], st.o[3][r]} * inv,
+                      f32x4{st.o[4][r], st.o[5][r], st.o[6][r], st.o[7][r]} * inv, a.out_fp32);
     }
     return;
   }
-  const size_t slot = head * a.max_splits + split;
-  float* dst = a.ws_o + slot * kHeadDim + 32 * g;
+
+  // Partials are written and read with agent-scope relaxed atomic accesses,
+  // which the hardware keeps coherent across the chip's L2s without any
+  // cache write-back or invalidation; the arrival is counted only after the
+  // stores have completed.
+  if (n < G) {
+    const size_t slot = (head0 + n) * a.max_splits + split;
+    float* dst = a.ws_o + slot * kHeadDim + 32 * g;
 #pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    *reinterpret_cast<f32x4*>(dst + 8 * r) = f32x4{st.o[0][r], st.o[1][r], st.o[2][r], st.o[3][r]};
-    *reinterpret_cast<f32x4*>(dst + 8 * r + 4) = f32x4{st.o[4][r], st.o[5][r], st.o[6][r], st.o[7][r]};
+    for (int r = 0; r < 4; ++r)
+#pragma unroll
+      for (int j = 0; j < 8; j += 2)
+        store_agent_f2(dst + 8 * r + j, st.o[j][r], st.o[j + 1][r]);
+    if (g == 0) store_agent_f2(a.ws_ml + 2 * slot, st.m, l);
   }
-  if (g == 0) *reinterpret_cast<float2*>(a.ws_ml + 2 * slot) = make_float2(st.m, l);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  uint32_t* counter = a.counters + (size_t)s * hkv + kvh;
+  uint32_t prev = 0;
+  if (lane == 0) prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  prev = __builtin_amdgcn_readfirstlane(prev);
+  if (prev != (uint32_t)(nsplit - 1)) return;
+  asm volatile("" ::: "memory");
+  if (lane == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+
+  if (nsplit <= 64) {
+    merge_splits<T, G>(a, head0, nsplit, lane);
+  } else {
+    for (int h = 0; h < G; ++h) merge_head_serial<T>(a, head0 + h, nsplit, lane);
+  }
 }
 
-// Merge the splits of one (sequence, query head): weights exp2(m_k - M).
-template <typename T>
-__global__ __launch_bounds__(kHeadDim) void decode_reduce_kernel(DecodeArgs a) {
-  const int h = blockIdx.x;
-  const int s = blockIdx.y;
-  const int d = threadIdx.x;
-  const int len = a.seq_lens[s];
-  const int nblk = (len + kPage - 1) / kPage;
-  const int nsplit = (nblk + a.split_blocks - 1) / a.split_blocks;
-  if (nsplit == 1) return;   // the split kernel wrote the final row
-  const size_t head = (size_t)s * a.num_q_heads + h;
-  float res = 0.f;
-  if (nsplit > 1) {
-    const float* ml = a.ws_ml + 2 * head * a.max_splits;
-    float mmax = -__builtin_inff();
-    for (int k = 0; k < nsplit; ++k) mmax = fmaxf(mmax, ml[2 * k]);
-    float num = 0.f, den = 0.f;
-    const float* o = a.ws_o + head * a.max_splits * kHeadDim + d;
-    for (int k = 0; k < nsplit; ++k) {
-      const float w = fast_exp2(ml[2 * k] - mmax);
-      den += w * ml[2 * k + 1];
-      num += w * o[(size_t)k * kHeadDim];
-    }
-    res = num / den;
-  }
-  if (a.out_fp32) {
-    reinterpret_cast<float*>(a.out)[head * kHeadDim + d] = res;
-  } else {
-    float b;
-    reinterpret_cast<uint16_t*>(a.out)[head * kHeadDim + d] = Mma<T>::round(res, &b);
-  }
+template <typename T, int G, int NSLOT>
+hipError_t launch_slots(const DecodeArgs& a, bool elastic, hipStream_t st) {
+  dim3 grid(a.max_splits, a.num_kv_heads, a.batch);
+  if (elastic) hipLaunchKernelGGL((decode_kernel<T, G, true, NSLOT>), grid, dim3(64), 0, st, a);
+  else hipLaunchKernelGGL((decode_kernel<T, G, false, NSLOT>), grid, dim3(64), 0, st, a);
+  return hipGetLastError();
 }
 
 template <typename T, int G>
 hipError_t launch_typed(const DecodeArgs& a, bool elastic, hipStream_t st) {
-  dim3 grid(a.max_splits, a.num_kv_heads, a.batch);
-  if (elastic) hipLaunchKernelGGL((decode_split_kernel<T, G, true>), grid, dim3(64), 0, st, a);
-  else hipLaunchKernelGGL((decode_split_kernel<T, G, false>), grid, dim3(64), 0, st, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess) return e;
-  hipLaunchKernelGGL((decode_reduce_kernel<T>), dim3(a.num_q_heads, a.batch), dim3(kHeadDim), 0, st, a);
-  return hipGetLastError();
+  switch (a.slots) {
+    case 3: return launch_slots<T, G, 3>(a, elastic, st);
+    case 5: return launch_slots<T, G, 5>(a, elastic, st);
+    case 6: return launch_slots<T, G, 6>(a, elastic, st);
+    default: return launch_slots<T, G, 4>(a, elastic, st);
+  }
 }
 
 template <typename T>
@@ -321,11 +568,23 @@ hipError_t launch_group(const DecodeArgs& a, int group, bool elastic, hipStream_
   }
 }
 
+__global__ void fill_zero_kernel(uint32_t* p, size_t n) {
+  for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
+    p[i] = 0u;
+}
+
 }  // namespace
 
 hipError_t launch_decode(const DecodeArgs& a, int dtype, int group, bool elastic, hipStream_t st) {
   if (a.batch == 0) return hipSuccess;
   return dtype == 0 ? launch_group<Bf16>(a, group, elastic, st) : launch_group<Fp16>(a, group, elastic, st);
+}
+
+hipError_t launch_zero_u32(uint32_t* p, size_t n, hipStream_t st) {
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)std::min<size_t>((n + 255) / 256, 1024);
+  hipLaunchKernelGGL(fill_zero_kernel, dim3(blocks), dim3(256), 0, st, p, n);
+  return hipGetLastError();
 }
 
 }  // namespace ekv

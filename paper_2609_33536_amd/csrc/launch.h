@@ -16,14 +16,17 @@ struct DecodeArgs {
   const int32_t* bounds;     // [B][2] or null
   float* ws_o;               // [B][Hq][max_splits][128]
   float* ws_ml;              // [B][Hq][max_splits][2]
+  uint32_t* counters;        // [B][Hkv] split-merge counters, zero between calls
   void* out;                 // [B][Hq][128]
   int32_t batch, num_kv_heads, num_q_heads, max_blocks;
   int32_t split_blocks, max_splits, out_fp32;
+  int32_t slots;             // LDS ring depth per wave (3..6)
   float scale_log2;          // softmax scale * log2(e)
 };
 
 // dtype: 0 bf16, 1 fp16.  elastic: false = native path (tags never read).
 hipError_t launch_decode(const DecodeArgs& a, int dtype, int group, bool elastic, hipStream_t st);
+hipError_t launch_zero_u32(uint32_t* p, size_t n, hipStream_t st);
 
 struct TransitionArgs {
   uint16_t* pool;

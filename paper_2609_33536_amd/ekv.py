@@ -49,6 +49,7 @@ SIGNATURES = {
     "ekv_version": (ctypes.c_char_p, []),
     "ekv_lower": (_I, [_P, _P, _I, _I, _I, _P, _P]),
     "ekv_decode_workspace_bytes": (_U, [ctypes.POINTER(Pool), ctypes.POINTER(Batch)]),
+    "ekv_decode_workspace_init": (_I, [_P, _U, _S]),
     "ekv_attn_decode": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _F, _P, _U, _S]),
     "ekv_attn_prefill": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _I, _P, _I, _F, _S]),
     "ekv_append_kv": (_I, [ctypes.POINTER(Pool), _P, _P, _P, _I, _S]),
@@ -133,6 +134,16 @@ def lower(tags, seq_lens, page=PAGE):
 
 def decode_workspace_bytes(pool, batch):
     return lib().ekv_decode_workspace_bytes(ctypes.byref(pool), ctypes.byref(batch))
+
+
+def decode_workspace(pool, batch, device="cuda"):
+    """A zero-filled decode workspace (its merge counters start at zero)."""
+    import torch
+    return torch.zeros(decode_workspace_bytes(pool, batch), dtype=torch.uint8, device=device)
+
+
+def decode_workspace_init(ws, stream=None):
+    _check(lib().ekv_decode_workspace_init(_ptr(ws), ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def attn_decode(pool, batch, q, out, scale, ws, stream=None):

@@ -101,11 +101,17 @@ class PagedKV:
     def block_bytes(self):
         return 2 * self.num_kv_heads * ekv.PAGE * ekv.HEAD_DIM * 2
 
+    def _upload(self, arr):
+        """Host array -> device through a fresh pinned buffer (stream-ordered,
+        does not block the host on earlier GPU work)."""
+        import torch
+        return torch.from_numpy(np.ascontiguousarray(arr)).pin_memory().to(self.device, non_blocking=True)
+
     def relower(self):
         """Recompute the dispatch metadata from the host mirror and upload it."""
         import torch
         self.mode, bounds = self.mirror.lower()
-        self.bounds.copy_(torch.from_numpy(bounds))
+        self.bounds.copy_(torch.from_numpy(bounds).pin_memory(), non_blocking=True)
         return self.mode
 
     def batch(self, num_q_heads, mode=None, use_boundaries=True, max_seq_len=None):
@@ -121,7 +127,7 @@ class PagedKV:
         import torch
         host_freed = self.mirror.plan_demote(pairs)
         n = len(host_freed)
-        pairs_d = torch.from_numpy(np.asarray(pairs, dtype=np.int32).reshape(-1, 2).copy()).to(self.device)
+        pairs_d = self._upload(np.asarray(pairs, dtype=np.int32).reshape(-1, 2))
         freed = torch.empty(n, dtype=torch.int32, device=self.device)
         lo = torch.empty((n, self.block_bytes), dtype=torch.uint8, device=self.device) if emit_lo else None
         ekv.demote(self.pool, pairs_d, self.bt, self.tags, freed, lo, stream)
@@ -130,20 +136,26 @@ class PagedKV:
         self._pending = getattr(self, "_pending", []) + [(ev, host_freed)]
         return freed, lo, host_freed
 
-    def commit(self):
-        """Return blocks freed by completed demotions to the free pool."""
+    def commit(self, wait=True):
+        """Return blocks freed by completed demotions to the free pool.  With
+        wait=False only demotions whose GPU work has already finished are
+        committed."""
         keep = []
         for ev, ids in getattr(self, "_pending", []):
-            ev.synchronize()
-            self.mirror.commit_freed(ids)
+            if wait:
+                ev.synchronize()
+            if wait or ev.query():
+                self.mirror.commit_freed(ids)
+            else:
+                keep.append((ev, ids))
         self._pending = keep
 
     def refine(self, pairs, lo, stream=None):
         """Enqueue a refinement of BASE pairs from their refinement bytes."""
         import torch
         new = self.mirror.plan_refine(pairs)
-        pairs_d = torch.from_numpy(np.asarray(pairs, dtype=np.int32).reshape(-1, 2).copy()).to(self.device)
-        new_d = torch.from_numpy(new).to(self.device)
+        pairs_d = self._upload(np.asarray(pairs, dtype=np.int32).reshape(-1, 2))
+        new_d = self._upload(new)
         ekv.refine(self.pool, pairs_d, new_d, self.bt, self.tags, lo, stream)
         return new
 

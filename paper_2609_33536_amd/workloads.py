@@ -175,3 +175,64 @@ WORKLOADS = {
 
 def seq_lens_uniform(rng, batch, lo, hi):
     return rng.integers(lo, hi + 1, size=batch).astype(np.int32)
+
+
+def make_decode_case_torch(seq_lens, num_q_heads, num_kv_heads, *, seed, outlier_channels=0,
+                           spare_blocks=0, dtype="bf16", device="cuda", max_blocks=None):
+    """Large-workload variant of :func:`make_decode_case` that draws the
+    values on the GPU with a seeded torch generator.  Block placement and
+    lengths come from NumPy as before.  Returns device tensors for the pool
+    (16-bit words as int16 [NB][2][Hkv][16][128]) and the query, NumPy arrays
+    for the rest."""
+    import torch
+    rng = np.random.default_rng(seed)
+    seq_lens = np.asarray(seq_lens, dtype=np.int32)
+    bsz = len(seq_lens)
+    nblk = [-(-int(l) // PAGE) for l in seq_lens]
+    used = int(sum(nblk))
+    nb = used + int(spare_blocks)
+    if max_blocks is None:
+        max_blocks = max(2, max(nblk) + (max(nblk) % 2))
+    perm = rng.permutation(nb).astype(np.int32)
+    bt = np.zeros((bsz, max_blocks), dtype=np.int32)
+    pos = 0
+    for s in range(bsz):
+        bt[s, :nblk[s]] = perm[pos:pos + nblk[s]]
+        pos += nblk[s]
+    free = np.sort(perm[used:]).astype(np.int32)
+    tdtype = torch.bfloat16 if dtype == "bf16" else torch.float16
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    pool = torch.empty((nb, 2, num_kv_heads, PAGE, HEAD_DIM), dtype=tdtype, device=device)
+    scale = torch.ones((2, num_kv_heads, 1, HEAD_DIM), dtype=torch.float32, device=device)
+    for plane in range(2):
+        if outlier_channels:
+            idx = rng.choice(num_kv_heads * HEAD_DIM, size=outlier_channels, replace=False)
+            for c in idx:
+                scale[plane, c // HEAD_DIM, 0, c % HEAD_DIM] = 10.0
+    chunk = 4096
+    for b0 in range(0, nb, chunk):
+        b1 = min(nb, b0 + chunk)
+        x = torch.randn((b1 - b0, 2, num_kv_heads, PAGE, HEAD_DIM), generator=gen, device=device,
+                        dtype=torch.float32)
+        pool[b0:b1] = (x * scale).to(tdtype)
+    q = torch.randn((bsz, num_q_heads, HEAD_DIM), generator=gen, device=device,
+                    dtype=torch.float32).to(tdtype)
+    return {"pool": pool.view(torch.int16), "q": q, "block_table": bt, "seq_lens": seq_lens,
+            "free": free, "dtype": dtype, "num_kv_heads": num_kv_heads}
+
+
+def extract_sequences(pool_dev, block_table, seq_lens, seq_ids):
+    """Host copy of just the blocks of ``seq_ids``, renumbered densely:
+    returns (pool uint16 [n][2][Hkv][16][128], block_table, seq_lens)."""
+    import torch
+    page = PAGE
+    blocks = []
+    bt = np.zeros((len(seq_ids), block_table.shape[1]), dtype=np.int32)
+    for r, s in enumerate(seq_ids):
+        nblk = -(-int(seq_lens[s]) // page)
+        bt[r, :nblk] = np.arange(len(blocks), len(blocks) + nblk)
+        blocks.extend(int(b) for b in block_table[s, :nblk])
+    idx = torch.as_tensor(np.array(blocks, dtype=np.int64), device=pool_dev.device)
+    host = pool_dev.index_select(0, idx).cpu().numpy().view(np.uint16)
+    return host, bt, np.asarray(seq_lens, dtype=np.int32)[list(seq_ids)]

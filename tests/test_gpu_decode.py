@@ -50,7 +50,7 @@ def _run(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, 
         os.environ["EKV_SPLIT_BLOCKS"] = str(split_blocks)
     try:
         batch = kv.batch(hq, mode=mode, use_boundaries=use_boundaries)
-        ws = torch.empty(ekv.decode_workspace_bytes(kv.pool, batch), dtype=torch.uint8, device="cuda")
+        ws = ekv.decode_workspace(kv.pool, batch)
         print(f"decode: B={bsz} Hq={hq} Hkv={hkv} mode={mode} bounds={use_boundaries} "
               f"split={split_blocks} fp32={out_fp32} {dtype}", flush=True)
         ekv.attn_decode(kv.pool, batch, q, out, default_scale(), ws)
@@ -145,3 +145,26 @@ def test_host_rejects_bad_transitions_before_launch():
     kv.demote(c["pairs"])
     with pytest.raises(ekv.EkvError):
         kv.demote(c["pairs"])              # already BASE
+
+
+def test_workspace_reused_across_calls_and_init():
+    """The split-merge counters reset themselves: three calls on one
+    workspace (the first after ekv_decode_workspace_init on a dirty buffer)
+    all match the oracle."""
+    torch = require_gpu()
+    c = workloads.make_decode_case([3000, 100, 2048, 5000], 32, 8, seed=9, base_fraction=0.5,
+                                   spare_blocks=2)
+    kv = kvpool.PagedKV(c["pool"], c["block_table"], c["seq_lens"], c["free"], 8)
+    kv.demote(c["pairs"])
+    kv.relower()
+    opool, obt, otg, _, _ = otr.demote(c["pool"], c["block_table"], c["tags"], c["pairs"], c["seq_lens"])
+    ref = oatt.decode(c["q"], opool, obt, otg, c["seq_lens"])
+    q = words_to_tensor(c["q"], torch, "bf16")
+    batch = kv.batch(32)
+    ws = torch.full((ekv.decode_workspace_bytes(kv.pool, batch),), 0xAB, dtype=torch.uint8, device="cuda")
+    ekv.decode_workspace_init(ws)
+    for call in range(3):
+        out = torch.full((4, 32, 128), float("nan"), dtype=torch.float32, device="cuda")
+        ekv.attn_decode(kv.pool, batch, q, out, default_scale(), ws)
+        torch.cuda.synchronize()
+        check_attention(out.cpu().numpy(), ref, True)
