@@ -74,32 +74,32 @@ int max_seq_blocks(const ekv_batch* b) {
   return (len + ekv::kPage - 1) / ekv::kPage;
 }
 
-// Blocks per split: the smallest power of two >= 8 that keeps the launch at
-// or under ~8k work items (32 per CU), unless EKV_SPLIT_BLOCKS overrides;
-// never more than kMaxSplitBlocks.
-int plan_split_blocks(int batch, int hkv, int nblk_max) {
-  if (const char* env = getenv("EKV_SPLIT_BLOCKS")) {
+// Fewest pairs (32 tokens) one workgroup streams; EKV_MIN_CHUNK overrides.
+int plan_min_chunk() {
+  if (const char* env = getenv("EKV_MIN_CHUNK")) {
     const int v = atoi(env);
-    if (v > 0) return std::min((v + 1) & ~1, ekv::kMaxSplitBlocks);   // even: pairs never straddle splits
+    if (v > 0) return v;
   }
-  const long long items = (long long)batch * hkv;
-  int sb = 8;
-  while (sb < ekv::kMaxSplitBlocks && items * ((nblk_max + sb - 1) / sb) > 8192) sb *= 2;
-  return sb;
+  return 8;
 }
 
 // Workspace: [merge counters u32 B*Hkv | (m, l) f32 rows | o f32 rows], 256-B aligned parts.
+// A (sequence, KV head) of np pairs is cut into at most ceil(np / chunk) + 1
+// pieces, and chunk >= min_chunk.
 struct DecodePlan {
-  int split_blocks, max_splits;
+  int min_chunk, max_pieces;
+  long long pairs_max;
   size_t ml_offset, o_offset, total;
 };
 
 DecodePlan plan_decode(const ekv_pool* p, const ekv_batch* b) {
   DecodePlan d{};
   const int nblk = std::max(1, max_seq_blocks(b));
-  d.split_blocks = plan_split_blocks(b->batch, p->num_kv_heads, nblk);
-  d.max_splits = std::max(1, (nblk + d.split_blocks - 1) / d.split_blocks);
-  const size_t rows = (size_t)b->batch * b->num_q_heads * d.max_splits;
+  const int np_max = (nblk + 1) / 2;
+  d.min_chunk = plan_min_chunk();
+  d.max_pieces = (np_max + d.min_chunk - 1) / d.min_chunk + 1;
+  d.pairs_max = (long long)b->batch * p->num_kv_heads * np_max;
+  const size_t rows = (size_t)b->batch * b->num_q_heads * d.max_pieces;
   auto align = [](size_t x) { return (x + 255) & ~(size_t)255; };
   d.ml_offset = align((size_t)b->batch * p->num_kv_heads * sizeof(uint32_t));
   d.o_offset = align(d.ml_offset + rows * 2 * sizeof(float));
@@ -212,11 +212,18 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
   a.num_kv_heads = pool->num_kv_heads;
   a.num_q_heads = batch->num_q_heads;
   a.max_blocks = batch->max_blocks;
-  a.split_blocks = plan.split_blocks;
-  a.max_splits = plan.max_splits;
+  a.num_blocks = pool->num_blocks;
+  a.len_cap = max_seq_blocks(batch) * ekv::kPage;
+  if (batch->max_seq_len > 0) a.len_cap = std::min(a.len_cap, batch->max_seq_len);
+  if (plan.pairs_max >= (1LL << 30)) return fail(EKV_ERR_UNSUPPORTED, "batch too large for one decode call");
+  a.max_splits = plan.max_pieces;
+  a.min_chunk = plan.min_chunk;
+  a.pairs_max = plan.pairs_max;
   a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
-  a.slots = 3;
-  if (const char* env = getenv("EKV_DECODE_SLOTS")) a.slots = std::max(3, std::min(6, atoi(env)));
+  // LDS ring depth: the deepest ring that still lets 4 workgroups (one per
+  // SIMD) share a CU's 160 KiB with their window buffers.
+  a.slots = group <= 4 ? 4 : (group == 8 ? 3 : 2);
+  if (const char* env = getenv("EKV_DECODE_SLOTS")) a.slots = std::max(2, std::min(4, atoi(env)));
   a.scale_log2 = log2e_scale(scale);
   return hip_status(ekv::launch_decode(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
                     "ekv_attn_decode launch");

@@ -15,7 +15,6 @@ constexpr int kHeadDim = 128;
 constexpr int kPage = 16;
 constexpr int kTileWords = kPage * kHeadDim;   // one (plane, head) tile: 2048 words = 4 KiB
 constexpr int kTileBytes = 2 * kTileWords;
-constexpr int kMaxSplitBlocks = 64;            // one block-table entry per lane of a wave
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));

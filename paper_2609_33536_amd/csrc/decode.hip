@@ -81,19 +81,6 @@ __device__ __forceinline__ void dma_tile(const char* src, const uint32_t (&off)[
                                      (lds_ptr)(dst + 1024 * r), 16, 0, 0);
 }
 
-// Wait until at most `ahead` slots (8 loads each) are still in flight.
-__device__ __forceinline__ void wait_slots(int ahead) {
-  switch (ahead) {
-    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-    case 1: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-    case 2: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
-    case 3: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
-    case 4: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
-    case 5: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
-    default: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
-  }
-}
-
 struct SplitState {
   f32x4 o[8];
   float m;   // reference max, log2 units (same in the 4 lanes of a head)
@@ -346,72 +333,240 @@ __device__ void merge_head_serial(const DecodeArgs& a, size_t head, int nsplit, 
   store_pair<T>(a.out, head * kHeadDim + 2 * lane, num0 * inv, num1 * inv, a.out_fp32);
 }
 
+// Wait until at most n load/store instructions of this wave are in flight
+// (n rounded down to a multiple of 8 -- waiting longer is always safe).
+template <int COMMON>
+__device__ __forceinline__ void wait_vm(int n) {
+  if (n >= 63) return;
+  const int k = n >> 3;
+  if (k == COMMON) {
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(8 * COMMON) : "memory");
+    return;
+  }
+  switch (k) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(56)" ::: "memory"); break;
+  }
+}
+
+__device__ __forceinline__ int wave_sum_int(int x) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
+  return x;
+}
+
+__device__ __forceinline__ int wave_incl_scan(int x, int lane) {
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const int y = __shfl_up(x, off);
+    if (lane >= off) x += y;
+  }
+  return x;
+}
+
+__device__ __forceinline__ int clamp_len(int len, int cap) { return len < 0 ? 0 : (len > cap ? cap : len); }
+
+__device__ __forceinline__ int pairs_of(int len) { return ((len + kPage - 1) / kPage + 1) >> 1; }
+
+constexpr int kWinPairs = 32;                      // a window: at most 32 pairs = 64 blocks
+// Window buffer in LDS: block-table entries, tags (one dword each),
+// the sequence's boundaries, then the G query rows of the KV head.
+constexpr int kWinBt = 0, kWinTags = 256, kWinBounds = 512, kWinQ = 528;
+template <int G> constexpr int win_bytes() { return kWinQ + G * 2 * kHeadDim; }
+
+// Position in the flattened (sequence, KV head, pair) space.
+struct Walker {
+  int s, kvh, j;        // sequence, KV head, pair index of the next window
+  int np, nblk, len;    // of sequence s
+  int seq_base;         // flattened offset of (s, 0, 0)
+  int g;                // flattened offset of (s, kvh, j)
+  int lens_base, lens_lane;
+};
+
+struct Window {
+  int s, kvh, len, b0, b1, j0, j1, np, seq_base;
+  bool piece_start, piece_end;
+};
+
+template <int G, bool ELASTIC, int NSLOT>
+struct alignas(16) DecodeSmem {
+  char ring[NSLOT][kSlotBytes];
+  char win[NSLOT + 1][win_bytes<G>()];
+};
+
+// ---------------------------------------------------------------------------
+// Decode kernel: workgroup w streams pairs [w*chunk, (w+1)*chunk) of the
+// flattened (sequence, KV head, pair) space, where chunk = ceil(T / grid)
+// (at least a.min_chunk) and T counts every pair of every (sequence, KV
+// head).  A (sequence, KV head) that lies wholly inside one range is
+// written out directly; one cut by range ends leaves one partial per piece,
+// and the last piece to arrive merges them (after its stream has ended).
+// ---------------------------------------------------------------------------
 template <typename T, int G, bool ELASTIC, int NSLOT>
 __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
-  __shared__ __attribute__((aligned(16))) char smem[NSLOT * kSlotBytes];
-  const int s = blockIdx.z;
-  const int kvh = blockIdx.y;
-  const int split = blockIdx.x;
+  __shared__ DecodeSmem<G, ELASTIC, NSLOT> sm;
   const int lane = threadIdx.x;
   const int n = lane & 15;
   const int g = lane >> 4;
-  const int len = a.seq_lens[s];
-  const int nblk = (len + kPage - 1) / kPage;
-  const int b_begin = split * a.split_blocks;
-  if (b_begin >= nblk) {
-    if (nblk == 0 && split == 0) {   // empty sequence: zero output
-      for (int h = 0; h < G; ++h)
-        store_pair<T>(a.out, ((size_t)s * a.num_q_heads + kvh * G + h) * kHeadDim + 2 * lane, 0.f, 0.f,
-                      a.out_fp32);
-    }
-    return;
-  }
-  const int b_end = min(nblk, b_begin + a.split_blocks);
-  const int nsplit = (nblk + a.split_blocks - 1) / a.split_blocks;
-
   const int hkv = a.num_kv_heads;
-  const size_t block_bytes = (size_t)2 * hkv * kTileBytes;
-  const char* pool = reinterpret_cast<const char*>(a.pool) + (size_t)kvh * kTileBytes;
-  const size_t v_off = (size_t)hkv * kTileBytes;
-  const int32_t* btrow = a.bt + (size_t)s * a.max_blocks;
+  const int B = a.batch;
 
-  u32x4 qop[4];
-  {
-    const uint16_t* qrow = a.q + ((size_t)s * a.num_q_heads + (size_t)kvh * G + n) * kHeadDim;
+  // ---- the range of this workgroup -------------------------------------
+  int total_pairs = 0;
+  for (int c0 = 0; c0 < B; c0 += 512) {
+    int np8[8];
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
-      qop[k] = (n < G) ? *reinterpret_cast<const u32x4*>(qrow + 8 * (4 * g + k)) : u32x4{0u, 0u, 0u, 0u};
+    for (int u = 0; u < 8; ++u) {
+      const int idx = c0 + 64 * u + lane;
+      np8[u] = idx < B ? pairs_of(clamp_len(a.seq_lens[idx], a.len_cap)) : 0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) total_pairs += __builtin_amdgcn_readfirstlane(wave_sum_int(np8[u]));
+  }
+  const int T_all = hkv * total_pairs;
+  if (blockIdx.x == 0) {   // empty sequences: zero output
+    for (int c0 = 0; c0 < B; c0 += 64) {
+      const int idx = c0 + lane;
+      uint64_t empty = __builtin_amdgcn_ballot_w64(idx < B && clamp_len(a.seq_lens[idx], a.len_cap) == 0);
+      while (empty) {
+        const int s0 = c0 + __builtin_ctzll(empty);
+        empty &= empty - 1;
+        for (int e = lane; e < a.num_q_heads * kHeadDim / 2; e += 64)
+          store_pair<T>(a.out, (size_t)s0 * a.num_q_heads * kHeadDim + 2 * e, 0.f, 0.f, a.out_fp32);
+      }
+    }
+  }
+  const int chunk = max(a.min_chunk, (T_all + (int)gridDim.x - 1) / (int)gridDim.x);
+  const int start = (int)blockIdx.x * chunk;
+  if (start >= T_all) return;
+  const int end = min(T_all, start + chunk);
+
+  Walker w0;
+  {
+    int cum = 0;
+    for (int c0 = 0;; c0 += 64) {
+      const int idx = c0 + lane;
+      const int len = idx < B ? clamp_len(a.seq_lens[idx], a.len_cap) : 0;
+      const int np = pairs_of(len);
+      const int incl = wave_incl_scan(np, lane);
+      const uint64_t hit = __builtin_amdgcn_ballot_w64(hkv * (cum + incl) > start);
+      if (hit) {
+        const int l0 = __builtin_ctzll(hit);
+        w0.s = c0 + l0;
+        w0.len = __builtin_amdgcn_readlane(len, l0);
+        w0.np = __builtin_amdgcn_readlane(np, l0);
+        w0.seq_base = hkv * (cum + __builtin_amdgcn_readlane(incl, l0) - w0.np);
+        w0.lens_base = c0;
+        w0.lens_lane = len;
+        break;
+      }
+      cum += __builtin_amdgcn_readlane(incl, 63);
+    }
+    w0.nblk = (w0.len + kPage - 1) / kPage;
+    const int off = start - w0.seq_base;
+    w0.kvh = off / w0.np;
+    w0.j = off - w0.kvh * w0.np;
+    w0.g = start;
   }
 
-  // This split's block-table entries (and tags), one per lane, fetched once;
-  // each block's entry is then read from its lane into a scalar register,
-  // so the block loop issues no memory access other than the K/V loads.
-  const int nb_split = b_end - b_begin;   // <= kMaxSplitBlocks
-  const int bt_lane = lane < nb_split ? btrow[b_begin + lane] : 0;
-  int base_lo = 0, base_hi = 0;
-  int tag_lane = 0;
-  bool use_tags = false;
-  if constexpr (ELASTIC) {
-    int b0 = -1, b1 = -1;
-    if (a.bounds) {
-      b0 = a.bounds[2 * s];
-      b1 = a.bounds[2 * s + 1];
+  auto next_window = [&](Walker& w) -> Window {
+    Window x;
+    x.s = w.s;
+    x.kvh = w.kvh;
+    x.len = w.len;
+    x.np = w.np;
+    x.seq_base = w.seq_base;
+    x.j0 = w.j;
+    x.j1 = min(min(w.np, w.j + kWinPairs), w.j + (end - w.g));
+    x.b0 = 2 * x.j0;
+    x.b1 = min(w.nblk, 2 * x.j1);
+    x.piece_start = (x.j0 == 0) || (w.g == start);
+    w.g += x.j1 - x.j0;
+    w.j = x.j1;
+    x.piece_end = (x.j1 == w.np) || (w.g == end);
+    if (w.j == w.np && w.g < end) {
+      w.j = 0;
+      if (++w.kvh == hkv) {
+        w.kvh = 0;
+        w.seq_base += hkv * w.np;
+        do {   // the next sequence that has tokens (one exists: w.g < end)
+          ++w.s;
+          if (w.s - w.lens_base >= 64) {
+            w.lens_base = w.s;
+            w.lens_lane = w.s + lane < B ? clamp_len(a.seq_lens[w.s + lane], a.len_cap) : 0;
+          }
+          w.len = __builtin_amdgcn_readlane(w.lens_lane, w.s - w.lens_base);
+        } while (w.len == 0);
+        w.np = pairs_of(w.len);
+        w.nblk = (w.len + kPage - 1) / kPage;
+      }
     }
-    if (b0 >= 0) {
-      base_lo = 2 * b0;
-      base_hi = 2 * b1;
-    } else if (a.tags) {
-      use_tags = true;
-      tag_lane = lane < nb_split ? a.tags[(size_t)s * a.max_blocks + b_begin + lane] : 0;
-    }
-  }
-  auto is_base = [&](int blk) -> bool {
-    if constexpr (!ELASTIC) return false;
-    else return use_tags ? (__builtin_amdgcn_readlane(tag_lane, blk - b_begin) != 0)
-                         : (blk >= base_lo && blk < base_hi);
+    return x;
   };
 
-  // per-lane LDS read offsets (see the swizzle above)
+  // ---- per-window metadata by direct-to-LDS loads ------------------------
+  const bool have_bounds = ELASTIC && a.bounds != nullptr;
+  const bool have_tags = ELASTIC && a.tags != nullptr;
+  constexpr int kQInstr = (G * 2 * kHeadDim + 1023) / 1024;
+  const int win_ops = 1 + (have_tags ? 1 : 0) + (have_bounds ? 1 : 0) + kQInstr;
+  int ops = 0;   // direct-to-LDS load instructions issued so far (stores are not counted)
+
+  auto dma_window = [&](const Window& x, int slot) {
+    char* wb = sm.win[slot];
+    const int nb = x.b1 - x.b0;
+    const size_t row = (size_t)x.s * a.max_blocks + x.b0;
+    if (lane < nb)
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.bt + row + lane), (lds_ptr)(wb + kWinBt), 4, 0, 0);
+    if (have_tags && lane < nb)
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.tags + row + lane), (lds_ptr)(wb + kWinTags), 1, 0, 0);
+    if (have_bounds && lane < 2)
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.bounds + 2 * x.s + lane), (lds_ptr)(wb + kWinBounds), 4, 0, 0);
+    const char* qsrc = reinterpret_cast<const char*>(a.q) + ((size_t)x.s * a.num_q_heads + (size_t)x.kvh * G) * 2 * kHeadDim;
+#pragma unroll
+    for (int r = 0; r < kQInstr; ++r)
+      if (64 * r + lane < G * 16)
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(qsrc + 16 * (64 * r + lane)),
+                                         (lds_ptr)(wb + kWinQ + 1024 * r), 16, 0, 0);
+    ops += win_ops;
+  };
+
+  struct ModeInfo {
+    int base_lo, base_hi;
+    bool use_tags;
+  };
+  // read a window's block-table entry / tag (per lane) and mode description
+  auto window_mode = [&](const char* wb, int& tag_lane) -> ModeInfo {
+    ModeInfo m{0, 0, false};
+    if constexpr (ELASTIC) {
+      int b0 = -1, b1 = -1;
+      if (have_bounds) {
+        const int2 bb = *reinterpret_cast<const int2*>(wb + kWinBounds);
+        b0 = __builtin_amdgcn_readfirstlane(bb.x);
+        b1 = __builtin_amdgcn_readfirstlane(bb.y);
+      }
+      if (b0 >= 0) {
+        m.base_lo = 2 * b0;
+        m.base_hi = 2 * b1;
+      } else if (have_tags) {
+        m.use_tags = true;
+        tag_lane = *reinterpret_cast<const int*>(wb + kWinTags + 4 * lane);
+      }
+    }
+    return m;
+  };
+  auto block_is_base = [&](const ModeInfo& m, int tag_lane, int b0, int blk) -> bool {
+    if constexpr (!ELASTIC) return false;
+    else return m.use_tags ? (__builtin_amdgcn_readlane(tag_lane, blk - b0) != 0)
+                           : (blk >= m.base_lo && blk < m.base_hi);
+  };
+
+  // per-lane LDS read offsets inside a slot (see the swizzle above)
   uint32_t rk_t[4], rv_t[4], rk_b[2], rv_b[4];
 #pragma unroll
   for (int k = 0; k < 4; ++k) rk_t[k] = n * (2 * kHeadDim) + 16 * ((4 * g + k) ^ n);
@@ -425,23 +580,53 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   for (int h = 0; h < 2; ++h) rk_b[h] = n * kHeadDim + 16 * ((2 * g + h) ^ tau(n));
   const DmaOffsets dma = dma_offsets(lane);
 
-  SplitState st;
-#pragma unroll
-  for (int j = 0; j < 8; ++j) st.o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-  st.m = -__builtin_inff();
-  st.l = 0.f;
+  const size_t block_bytes = (size_t)2 * hkv * kTileBytes;
+  const size_t v_off = (size_t)hkv * kTileBytes;
 
-  // Q, the block-table entries and tags must land before the ring starts:
-  // the ring's own waits count only K/V loads.
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  // ---- issue side ------------------------------------------------------
+  Walker iwk = w0;
+  Window icur = next_window(iwk);
+  dma_window(icur, 0);
+  const int ops_w0 = ops;
+  bool i_has_next = iwk.g < end;
+  Window inext = icur;
+  int ops_inext = 0;
+  if (i_has_next) {
+    inext = next_window(iwk);
+    dma_window(inext, 1);
+    ops_inext = ops;
+  }
+  const int ops_prologue = ops;
+  int iw_idx = 0;
+  wait_vm<NSLOT - 1>(ops - ops_w0);
+  int bt_lane = *reinterpret_cast<const int*>(sm.win[0] + kWinBt + 4 * lane);
+  int itag = 0;
+  ModeInfo imode = window_mode(sm.win[0], itag);
+  int ib = icur.b0;
+  int islot = 0;
+  bool issue_done = false;
 
-  int ib = b_begin, cb = b_begin;      // issue / consume cursors (logical blocks)
-  int issued = 0, consumed = 0;        // slots
-  int islot = 0, cslot = 0;            // ring positions
-  auto issue = [&]() {
-    const bool base = is_base(ib);
-    const char* src = pool + (size_t)__builtin_amdgcn_readlane(bt_lane, ib - b_begin) * block_bytes;
-    char* dst = smem + islot * kSlotBytes;
+  auto issue_slot = [&]() {
+    if (ib >= icur.b1) {   // enter the next window (its metadata was requested one window ago)
+      icur = inext;
+      ++iw_idx;
+      const int ws = iw_idx % (NSLOT + 1);
+      wait_vm<NSLOT - 1>(ops - ops_inext);
+      bt_lane = *reinterpret_cast<const int*>(sm.win[ws] + kWinBt + 4 * lane);
+      imode = window_mode(sm.win[ws], itag);
+      i_has_next = iwk.g < end;
+      if (i_has_next) {
+        inext = next_window(iwk);
+        dma_window(inext, (iw_idx + 1) % (NSLOT + 1));
+        ops_inext = ops;
+      }
+      ib = icur.b0;
+    }
+    const bool base = block_is_base(imode, itag, icur.b0, ib);
+    int phys = __builtin_amdgcn_readlane(bt_lane, ib - icur.b0);
+    phys = (unsigned)phys < (unsigned)a.num_blocks ? phys : 0;   // never leave the pool
+    const char* src = reinterpret_cast<const char*>(a.pool) + (size_t)phys * block_bytes + (size_t)icur.kvh * kTileBytes;
+    char* dst = sm.ring[islot];
     if (base) {
       dma_tile(src, dma.base, dst);
       dma_tile(src + v_off, dma.base, dst + kTileBytes);
@@ -449,19 +634,88 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       dma_tile(src, dma.tgt, dst);
       dma_tile(src + v_off, dma.tgt, dst + kTileBytes);
     }
+    ops += 8;
     ib += base ? 2 : 1;
-    ++issued;
     islot = islot + 1 == NSLOT ? 0 : islot + 1;
+    issue_done = ib >= icur.b1 && !i_has_next;
+  };
+
+  // ---- consume side ----------------------------------------------------
+  Walker cwk = w0;
+  Window ccur = next_window(cwk);
+  int cw_idx = 0;
+  int c_ops = ops_prologue;     // instructions issued up to and including the slot being consumed
+  int ctag = 0;
+  ModeInfo cmode = window_mode(sm.win[0], ctag);
+  u32x4 qop[4];
+  auto load_q = [&](const char* wb) {
+#pragma unroll
+    for (int k = 0; k < 4; ++k)
+      qop[k] = (n < G) ? *reinterpret_cast<const u32x4*>(wb + kWinQ + n * 2 * kHeadDim + 16 * (4 * g + k))
+                       : u32x4{0u, 0u, 0u, 0u};
+  };
+  load_q(sm.win[0]);
+  int cb = ccur.b0;
+  int cslot = 0;
+  int piece_j0 = ccur.j0;
+
+  SplitState st;
+  auto reset = [&]() {
+#pragma unroll
+    for (int j = 0; j < 8; ++j) st.o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
+    st.m = -__builtin_inff();
+    st.l = 0.f;
+  };
+  reset();
+
+  // partial pieces whose merge counter is bumped after the stream (at most 2)
+  int pend_n = 0;
+  size_t pend_head0[2] = {0, 0};
+  int pend_counter[2] = {0, 0}, pend_pieces[2] = {0, 0};
+
+  auto finalize_piece = [&]() {
+    const float l = head_sum(st.l);
+    const size_t head0 = (size_t)ccur.s * a.num_q_heads + (size_t)ccur.kvh * G;
+    const int first = ccur.seq_base + ccur.kvh * ccur.np;
+    const int w_first = first / chunk, w_last = (first + ccur.np - 1) / chunk;
+    const int pieces = w_last - w_first + 1;
+    if (pieces == 1) {
+      if (n < G) {
+        const float inv = 1.0f / l;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          store_row8<T>(a.out, (head0 + n) * kHeadDim + 32 * g + 8 * r,
+                        f32x4{st.o[0][r], st.o[1][r], st.o[2][r], st.o[3][r]} * inv,
+                        f32x4{st.o[4][r], st.o[5][r], st.o[6][r], st.o[7][r]} * inv, a.out_fp32);
+      }
+    } else {
+      const int idx = (int)blockIdx.x - w_first;
+      if (n < G) {
+        const size_t slot = (head0 + n) * a.max_splits + idx;
+        float* dst = a.ws_o + slot * kHeadDim + 32 * g;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+#pragma unroll
+          for (int j = 0; j < 8; j += 2) store_agent_f2(dst + 8 * r + j, st.o[j][r], st.o[j + 1][r]);
+        if (g == 0) store_agent_f2(a.ws_ml + 2 * slot, st.m, l);
+      }
+      pend_head0[pend_n] = head0;
+      pend_counter[pend_n] = ccur.s * hkv + ccur.kvh;
+      pend_pieces[pend_n] = pieces;
+      ++pend_n;
+    }
   };
 
 #pragma unroll
   for (int k = 0; k < NSLOT - 1; ++k)
-    if (ib < b_end) issue();
-  while (cb < b_end) {
-    if (ib < b_end) issue();
-    wait_slots(issued - consumed - 1);
-    const char* sb = smem + cslot * kSlotBytes;
-    if (is_base(cb)) {
+    if (!issue_done) issue_slot();
+
+  while (true) {
+    if (!issue_done) issue_slot();
+    c_ops += 8;
+    wait_vm<NSLOT - 1>(ops - c_ops);
+    const char* sb = sm.ring[cslot];
+    if (block_is_base(cmode, ctag, ccur.b0, cb)) {
       // one packed pair: member 0 = logical block cb, member 1 = cb + 1
       u32x4 k[2][4], v[2][4];
       f32x4 sc[2];
@@ -478,7 +732,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
         for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mb + rv_b[i]);
         sc[m] = qk_scores<T, true>(k[m], qop);
       }
-      softmax_pv<T, true, 2>(st, sc, v, cb * kPage, len, a.scale_log2, g);
+      softmax_pv<T, true, 2>(st, sc, v, cb * kPage, ccur.len, a.scale_log2, g);
       cb += 2;
     } else {
       u32x4 k[4], v[1][4];
@@ -487,72 +741,73 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[0][i] = *reinterpret_cast<const u32x4*>(sb + rv_t[i]);
       f32x4 sc[1] = {qk_scores<T, false>(k, qop)};
-      softmax_pv<T, false, 1>(st, sc, v, cb * kPage, len, a.scale_log2, g);
+      softmax_pv<T, false, 1>(st, sc, v, cb * kPage, ccur.len, a.scale_log2, g);
       cb += 1;
     }
-    ++consumed;
     cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
-  }
-
-  const float l = head_sum(st.l);
-  const size_t head0 = (size_t)s * a.num_q_heads + (size_t)kvh * G;
-  if (nsplit == 1) {
-    if (n < G) {
-      const float inv = 1.0f / l;
-#pragma unroll
-      for (int r = 0; r < 4; ++r)
-        store_row8<T>(a.out, (head0 + n) * kHeadDim + 32 * g + 8 * r,
-                      f32x4{st.o[0][r], st.o[1][r], st.o[2][r], st.o[3][r]} * inv,
-                      f32x4{st.o[4][r], st.o[5][r], st.o[6][r], st.o[7][r]} * inv, a.out_fp32);
+    if (cb < ccur.b1) continue;
+    // window finished
+    if (ccur.piece_end) finalize_piece();
+    if (cwk.g >= end) break;
+    ccur = next_window(cwk);
+    ++cw_idx;
+    if (cwk.g < end) c_ops += win_ops;   // the issue side requested the window after this one
+    const char* wb = sm.win[cw_idx % (NSLOT + 1)];
+    cmode = window_mode(wb, ctag);
+    load_q(wb);
+    if (ccur.piece_start) {
+      reset();
+      piece_j0 = ccur.j0;
     }
-    return;
+    cb = ccur.b0;
   }
+  (void)piece_j0;
 
-  // Partials are written and read with agent-scope relaxed atomic accesses,
-  // which the hardware keeps coherent across the chip's L2s without any
-  // cache write-back or invalidation; the arrival is counted only after the
-  // stores have completed.
-  if (n < G) {
-    const size_t slot = (head0 + n) * a.max_splits + split;
-    float* dst = a.ws_o + slot * kHeadDim + 32 * g;
-#pragma unroll
-    for (int r = 0; r < 4; ++r)
-#pragma unroll
-      for (int j = 0; j < 8; j += 2)
-        store_agent_f2(dst + 8 * r + j, st.o[j][r], st.o[j + 1][r]);
-    if (g == 0) store_agent_f2(a.ws_ml + 2 * slot, st.m, l);
-  }
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  uint32_t* counter = a.counters + (size_t)s * hkv + kvh;
-  uint32_t prev = 0;
-  if (lane == 0) prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  prev = __builtin_amdgcn_readfirstlane(prev);
-  if (prev != (uint32_t)(nsplit - 1)) return;
-  asm volatile("" ::: "memory");
-  if (lane == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-
-  if (nsplit <= 64) {
-    merge_splits<T, G>(a, head0, nsplit, lane);
-  } else {
-    for (int h = 0; h < G; ++h) merge_head_serial<T>(a, head0 + h, nsplit, lane);
+  // ---- merges ----------------------------------------------------------
+  if (pend_n == 0) return;
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // partials have landed before they are counted
+  for (int k = 0; k < pend_n; ++k) {
+    uint32_t* counter = a.counters + pend_counter[k];
+    uint32_t prev = 0;
+    if (lane == 0) prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    prev = __builtin_amdgcn_readfirstlane(prev);
+    if (prev != (uint32_t)(pend_pieces[k] - 1)) continue;
+    asm volatile("" ::: "memory");
+    if (lane == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (pend_pieces[k] <= 64) merge_splits<T, G>(a, pend_head0[k], pend_pieces[k], lane);
+    else
+      for (int h = 0; h < G; ++h) merge_head_serial<T>(a, pend_head0[k] + h, pend_pieces[k], lane);
   }
 }
 
+// Workgroups that fit on the device at once for a kernel (one wave each).
+template <typename K>
+int resident_groups(K kernel) {
+  int dev = 0, cus = 0, per_cu = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 64, 0) != hipSuccess) return 0;
+  return cus * per_cu;
+}
+
 template <typename T, int G, int NSLOT>
-hipError_t launch_slots(const DecodeArgs& a, bool elastic, hipStream_t st) {
-  dim3 grid(a.max_splits, a.num_kv_heads, a.batch);
-  if (elastic) hipLaunchKernelGGL((decode_kernel<T, G, true, NSLOT>), grid, dim3(64), 0, st, a);
-  else hipLaunchKernelGGL((decode_kernel<T, G, false, NSLOT>), grid, dim3(64), 0, st, a);
+hipError_t launch_slots(const DecodeArgs& args, bool elastic, hipStream_t st) {
+  auto kernel = elastic ? decode_kernel<T, G, true, NSLOT> : decode_kernel<T, G, false, NSLOT>;
+  DecodeArgs a = args;
+  const int resident = resident_groups(kernel);
+  if (resident <= 0) return hipErrorInvalidDeviceFunction;
+  const long long wanted = (a.pairs_max + a.min_chunk - 1) / a.min_chunk;
+  a.grid = (int)std::max<long long>(1, std::min<long long>(resident, wanted));
+  hipLaunchKernelGGL(kernel, dim3(a.grid), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 
 template <typename T, int G>
 hipError_t launch_typed(const DecodeArgs& a, bool elastic, hipStream_t st) {
   switch (a.slots) {
-    case 3: return launch_slots<T, G, 3>(a, elastic, st);
-    case 5: return launch_slots<T, G, 5>(a, elastic, st);
-    case 6: return launch_slots<T, G, 6>(a, elastic, st);
-    default: return launch_slots<T, G, 4>(a, elastic, st);
+    case 2: return launch_slots<T, G, 2>(a, elastic, st);
+    case 4: return launch_slots<T, G, 4>(a, elastic, st);
+    default: return launch_slots<T, G, 3>(a, elastic, st);
   }
 }
 

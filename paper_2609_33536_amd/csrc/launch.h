@@ -14,13 +14,19 @@ struct DecodeArgs {
   const int32_t* bt;         // [B][max_blocks]
   const uint8_t* tags;       // [B][max_blocks] or null
   const int32_t* bounds;     // [B][2] or null
-  float* ws_o;               // [B][Hq][max_splits][128]
-  float* ws_ml;              // [B][Hq][max_splits][2]
-  uint32_t* counters;        // [B][Hkv] split-merge counters, zero between calls
+  float* ws_o;               // [B][Hq][max_splits][128] partial outputs of cut (seq, KV head)s
+  float* ws_ml;              // [B][Hq][max_splits][2]   partial (max, sum)
+  uint32_t* counters;        // [B][Hkv] merge counters, zero between calls
   void* out;                 // [B][Hq][128]
   int32_t batch, num_kv_heads, num_q_heads, max_blocks;
-  int32_t split_blocks, max_splits, out_fp32;
-  int32_t slots;             // LDS ring depth per wave (3..6)
+  int32_t num_blocks;        // pool size: table entries are clamped into it
+  int32_t len_cap;           // sequence lengths are clamped to this (max_seq_len)
+  int32_t max_splits;        // partial slots per query head (pieces of one (seq, KV head))
+  int32_t min_chunk;         // fewest pairs a workgroup streams
+  int32_t grid;              // workgroups launched (set by the launcher)
+  int64_t pairs_max;         // upper bound on the pairs of all (seq, KV head)s
+  int32_t out_fp32;
+  int32_t slots;             // LDS ring depth per wave (2..6)
   float scale_log2;          // softmax scale * log2(e)
 };
 

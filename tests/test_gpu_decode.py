@@ -20,7 +20,7 @@ from tests.gpu_util import check_attention, default_scale, host_safety_check, re
 pytestmark = pytest.mark.gpu
 
 
-def _run(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, split_blocks=None):
+def _run(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, min_chunk=None):
     """Demote on both sides, decode on the GPU, compare everything."""
     torch = require_gpu()
     dtype = case["dtype"]
@@ -45,22 +45,22 @@ def _run(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, 
     bsz = len(case["seq_lens"])
     out_dtype = torch.float32 if out_fp32 else q.dtype
     out = torch.full((bsz, hq, 128), float("nan"), dtype=out_dtype, device="cuda")
-    old = os.environ.get("EKV_SPLIT_BLOCKS")
-    if split_blocks:
-        os.environ["EKV_SPLIT_BLOCKS"] = str(split_blocks)
+    old = os.environ.get("EKV_MIN_CHUNK")
+    if min_chunk:
+        os.environ["EKV_MIN_CHUNK"] = str(min_chunk)
     try:
         batch = kv.batch(hq, mode=mode, use_boundaries=use_boundaries)
         ws = ekv.decode_workspace(kv.pool, batch)
         print(f"decode: B={bsz} Hq={hq} Hkv={hkv} mode={mode} bounds={use_boundaries} "
-              f"split={split_blocks} fp32={out_fp32} {dtype}", flush=True)
+              f"min_chunk={min_chunk} fp32={out_fp32} {dtype}", flush=True)
         ekv.attn_decode(kv.pool, batch, q, out, default_scale(), ws)
         torch.cuda.synchronize()
     finally:
-        if split_blocks:
+        if min_chunk:
             if old is None:
-                del os.environ["EKV_SPLIT_BLOCKS"]
+                del os.environ["EKV_MIN_CHUNK"]
             else:
-                os.environ["EKV_SPLIT_BLOCKS"] = old
+                os.environ["EKV_MIN_CHUNK"] = old
     ref = oatt.decode(case["q"], opool, obt, otg, case["seq_lens"], dtype)
     got = out.float().cpu().numpy()
     return check_attention(got, ref, out_fp32), kv, opool, obt, otg
@@ -104,10 +104,13 @@ def test_decode_groups_fractions_ragged(group, fraction):
     _run(c, hkv * group, hkv)
 
 
-@pytest.mark.parametrize("split_blocks", [1, 2, 3, 8, 64])
-def test_decode_split_planning(split_blocks):
-    c = workloads.make_decode_case([300, 1024, 77, 2000], 32, 8, seed=3, base_fraction=0.5, spare_blocks=2)
-    _run(c, 32, 8, split_blocks=split_blocks)
+@pytest.mark.parametrize("min_chunk", [1, 2, 3, 8, 64])
+def test_decode_work_partition(min_chunk):
+    """Ranges of 1..64 pairs per workgroup: sequences cut into many pieces
+    (both merge paths: <= 64 pieces and more), pieces spanning sequences."""
+    c = workloads.make_decode_case([300, 1024, 77, 2000, 0, 4500], 32, 8, seed=3, base_fraction=0.5,
+                                   spare_blocks=2)
+    _run(c, 32, 8, min_chunk=min_chunk)
 
 
 def test_structured_and_general_paths_agree():
