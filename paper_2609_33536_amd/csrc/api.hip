@@ -257,6 +257,7 @@ ekv_status ekv_attn_prefill(const ekv_pool* pool, const ekv_batch* batch, const 
   a.num_q_heads = batch->num_q_heads;
   a.max_blocks = batch->max_blocks;
   a.max_q_len = max_q_len;
+  a.num_blocks = pool->num_blocks;
   a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
   a.scale_log2 = log2e_scale(scale);
   return hip_status(ekv::launch_prefill(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),

@@ -40,154 +40,12 @@
 // wave that finishes last -- found with a per-(sequence, KV head) counter in
 // the workspace -- merges them and writes the output, then resets the
 // counter to zero for the next call.
+#include "attn_device.h"
 #include "common.h"
 #include "launch.h"
 
 namespace ekv {
 namespace {
-
-constexpr int kSlotBytes = 2 * kTileBytes;   // K tile + V tile
-
-// XOR swizzle of 16-byte chunks inside an LDS tile.
-//  TARGET tile: 16 token rows x 16 chunks; chunk c of token t sits at c ^ t.
-//  BASE tile: 2 members x 16 rows x 8 chunks; chunk q of token t at q ^ tau(t).
-__device__ __forceinline__ int tau(int t) { return (t & 7) ^ (t >> 3); }
-
-// Byte offsets, within a 4 KiB plane tile in HBM, of the 16 B each lane
-// fetches with load instruction r (LDS destination: r * 1 KiB + 16 * lane).
-struct DmaOffsets {
-  uint32_t tgt[4], base[4];
-};
-
-__device__ __forceinline__ DmaOffsets dma_offsets(int lane) {
-  DmaOffsets o;
-#pragma unroll
-  for (int r = 0; r < 4; ++r) {
-    const int p = 64 * r + lane;                 // LDS chunk written by this lane
-    const int t = p >> 4, pos = p & 15;
-    o.tgt[r] = t * (2 * kHeadDim) + 16 * (pos ^ t);
-    const int m = p >> 7, tb = (p >> 3) & 15, posb = p & 7;
-    o.base[r] = m * (kTileBytes / 2) + tb * kHeadDim + 16 * (posb ^ tau(tb));
-  }
-  return o;
-}
-
-typedef __attribute__((address_space(3))) void* lds_ptr;
-
-__device__ __forceinline__ void dma_tile(const char* src, const uint32_t (&off)[4], char* dst) {
-#pragma unroll
-  for (int r = 0; r < 4; ++r)
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off[r]),
-                                     (lds_ptr)(dst + 1024 * r), 16, 0, 0);
-}
-
-struct SplitState {
-  f32x4 o[8];
-  float m;   // reference max, log2 units (same in the 4 lanes of a head)
-  float l;   // running sum, partial per lane
-};
-
-// max / sum over the four lanes of one head (lanes l, l^16, l^32, l^48)
-__device__ __forceinline__ float head_max(float x) {
-  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  const float y = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-
-__device__ __forceinline__ float head_sum(float x) {
-  const auto a = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  const float y = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const auto b = __builtin_amdgcn_permlane32_swap(__float_as_uint(y), __float_as_uint(y), false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-
-// PV A operand for MFMA j (head-dim row 8n + j): the lane's 4 tokens, as
-// 16-bit words.  TARGET rows hold 8 words per token, BASE rows 8 bytes.
-template <bool BASE>
-__device__ __forceinline__ u32x2 v_operand(const u32x4 (&v)[4], int j) {
-  if constexpr (BASE) {
-    const int b = j & 3;
-    const uint32_t sel = 0x0Cu | ((uint32_t)b << 8) | (0x0Cu << 16) | ((uint32_t)(4 + b) << 24);
-    const int w = j >> 2;
-    return u32x2{perm(v[1][w], v[0][w], sel), perm(v[3][w], v[2][w], sel)};
-  } else {
-    const uint32_t sel = (j & 1) ? 0x07060302u : 0x05040100u;
-    return u32x2{perm(v[1][j >> 1], v[0][j >> 1], sel), perm(v[3][j >> 1], v[2][j >> 1], sel)};
-  }
-}
-
-// Scores of one 16-token group: S^T = K Q^T, lane gets tokens 4g..4g+3 of head n.
-template <typename T, bool BASE>
-__device__ __forceinline__ f32x4 qk_scores(const u32x4 (&k)[4], const u32x4 (&qop)[4]) {
-  f32x4 s = {0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-  for (int st = 0; st < 4; ++st) {
-    u32x4 kop;
-    if constexpr (BASE) kop = expand_base8(k[st].xy);
-    else kop = k[st];
-    s = Mma<T>::qk(kop, qop[st], s);
-  }
-  return s;
-}
-
-// Online-softmax update for NG 16-token groups of one slot followed by
-// O += V^T P^T.  The reference max only moves (and O, l are rescaled) when
-// some head's block max exceeds it by more than 2^8; otherwise P <= 2^8.
-// P is split into a 16-bit head and remainder, stacked along k of one
-// 16x16x32 MFMA against the duplicated V operand.
-template <typename T, bool BASE, int NG>
-__device__ __forceinline__ void softmax_pv(SplitState& st, f32x4 (&s)[NG], u32x4 (&v)[NG][4], int tok0,
-                                           int len, float scale_log2, int g) {
-  float sc[NG][4];
-#pragma unroll
-  for (int q = 0; q < NG; ++q)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) sc[q][i] = s[q][i] * scale_log2;
-  if (tok0 + NG * kPage > len) {   // the sequence ends inside this slot (a TARGET block)
-#pragma unroll
-    for (int q = 0; q < NG; ++q)
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (tok0 + q * kPage + 4 * g + i >= len) {
-          sc[q][i] = -__builtin_inff();
-          v[q][i] = u32x4{0u, 0u, 0u, 0u};
-        }
-  }
-  float mx = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
-#pragma unroll
-  for (int q = 1; q < NG; ++q) mx = fmaxf(mx, fmaxf(fmaxf(sc[q][0], sc[q][1]), fmaxf(sc[q][2], sc[q][3])));
-  mx = head_max(mx);
-  if (__builtin_amdgcn_ballot_w64(mx > st.m + 8.0f)) {
-    const float m_new = fmaxf(st.m, mx);
-    const float alpha = fast_exp2(st.m - m_new);
-    st.l *= alpha;
-#pragma unroll
-    for (int j = 0; j < 8; ++j) st.o[j] *= alpha;
-    st.m = m_new;
-  }
-#pragma unroll
-  for (int q = 0; q < NG; ++q) {
-    float p[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sc[q][i] - st.m);
-    st.l += (p[0] + p[1]) + (p[2] + p[3]);
-    uint16_t ph[4], pl[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float back, dummy;
-      ph[i] = Mma<T>::round(p[i], &back);
-      pl[i] = Mma<T>::round(p[i] - back, &dummy);
-    }
-    const u32x4 pb = {(uint32_t)ph[0] | ((uint32_t)ph[1] << 16), (uint32_t)ph[2] | ((uint32_t)ph[3] << 16),
-                      (uint32_t)pl[0] | ((uint32_t)pl[1] << 16), (uint32_t)pl[2] | ((uint32_t)pl[3] << 16)};
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      const u32x2 a = v_operand<BASE>(v[q], j);
-      st.o[j] = Mma<T>::qk(u32x4{a.x, a.y, a.x, a.y}, pb, st.o[j]);
-    }
-  }
-}
 
 __device__ __forceinline__ void store_agent_f2(float* p, float a, float b) {
   const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
@@ -199,35 +57,6 @@ __device__ __forceinline__ float2 load_agent_f2(const float* p) {
                                        __HIP_MEMORY_SCOPE_AGENT);
   return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
 }
-
-template <typename T>
-__device__ __forceinline__ void store_row8(void* out, size_t idx, f32x4 a, f32x4 b, bool fp32) {
-  if (fp32) {
-    float* dst = reinterpret_cast<float*>(out) + idx;
-    *reinterpret_cast<f32x4*>(dst) = a;
-    *reinterpret_cast<f32x4*>(dst + 4) = b;
-  } else {
-    float x;
-    uint32_t w[4];
-    w[0] = (uint32_t)Mma<T>::round(a[0], &x) | ((uint32_t)Mma<T>::round(a[1], &x) << 16);
-    w[1] = (uint32_t)Mma<T>::round(a[2], &x) | ((uint32_t)Mma<T>::round(a[3], &x) << 16);
-    w[2] = (uint32_t)Mma<T>::round(b[0], &x) | ((uint32_t)Mma<T>::round(b[1], &x) << 16);
-    w[3] = (uint32_t)Mma<T>::round(b[2], &x) | ((uint32_t)Mma<T>::round(b[3], &x) << 16);
-    *reinterpret_cast<u32x4*>(reinterpret_cast<uint16_t*>(out) + idx) = u32x4{w[0], w[1], w[2], w[3]};
-  }
-}
-
-template <typename T>
-__device__ __forceinline__ void store_pair(void* out, size_t idx, float a, float b, bool fp32) {
-  if (fp32) {
-    *reinterpret_cast<float2*>(reinterpret_cast<float*>(out) + idx) = make_float2(a, b);
-  } else {
-    float x;
-    *reinterpret_cast<uint32_t*>(reinterpret_cast<uint16_t*>(out) + idx) =
-        (uint32_t)Mma<T>::round(a, &x) | ((uint32_t)Mma<T>::round(b, &x) << 16);
-  }
-}
-
 
 __device__ __forceinline__ f32x4 load_agent_f4(const float* p) {
   const float2 a = load_agent_f2(p), b = load_agent_f2(p + 2);
@@ -732,7 +561,9 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
         for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mb + rv_b[i]);
         sc[m] = qk_scores<T, true>(k[m], qop);
       }
-      softmax_pv<T, true, 2>(st, sc, v, cb * kPage, ccur.len, a.scale_log2, g);
+      u32x2 vop[2][8];
+      v_operands<true, 2>(v, vop);
+      softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, false, a.scale_log2, g);
       cb += 2;
     } else {
       u32x4 k[4], v[1][4];
@@ -740,8 +571,12 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       for (int q = 0; q < 4; ++q) k[q] = *reinterpret_cast<const u32x4*>(sb + rk_t[q]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[0][i] = *reinterpret_cast<const u32x4*>(sb + rv_t[i]);
-      f32x4 sc[1] = {qk_scores<T, false>(k, qop)};
-      softmax_pv<T, false, 1>(st, sc, v, cb * kPage, ccur.len, a.scale_log2, g);
+      const f32x4 sc[1] = {qk_scores<T, false>(k, qop)};
+      const bool tail = cb * kPage + kPage > ccur.len;
+      zero_tail_v<1>(v, cb * kPage, ccur.len, g);
+      u32x2 vop[1][8];
+      v_operands<false, 1>(v, vop);
+      softmax_pv<T, 1>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
       cb += 1;
     }
     cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;

@@ -68,6 +68,7 @@ struct PrefillArgs {
   const int32_t* bounds;
   void* out;                 // [total][Hq][128]
   int32_t batch, num_kv_heads, num_q_heads, max_blocks, max_q_len, out_fp32;
+  int32_t num_blocks;        // pool size: table entries are clamped into it
   float scale_log2;
 };
 
