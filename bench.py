@@ -1,29 +1,39 @@
 #!/usr/bin/env python3
 """Benchmark of the mixed-fidelity paged-attention hot path on one MI355X.
 
-Workload (Llama-3-8B-shaped decode layer): 64 sequences, 32 query / 8 KV
+Decode workload (Llama-3-8B-shaped layer): 64 sequences, 32 query / 8 KV
 heads, head dim 128, 16-token pages, context lengths uniform in
 [2048, 8192] (seed 1), bf16 K/V ~ N(0,1) with 10 outlier (head, channel)
-positions per plane scaled x10, BASE fraction swept over {0, 0.25, 0.5, 1}
-with BASE pairs chosen at random (irregular -> general elastic path;
-f = 0 -> native path).  One pool per BASE fraction, each made by demoting
-the chosen pairs with the library itself.
+positions per plane scaled x10.  BASE fraction swept over {0, 0.25, 0.5,
+1}: BASE pairs chosen at random (f = 0 -> native path; 0.25, 0.5 ->
+general elastic path; 1 -> every complete pair BASE, structured path).  One
+pool per BASE fraction, each made by demoting the chosen pairs with the
+library itself.
 
-One step = for each BASE fraction: append the newest token of every
-sequence as TARGET (rewriting the same values), lower the tags to dispatch
-metadata on the host, and run decode attention; then one transition round
-on the f=0.5 pool: demote 16 TARGET pairs (the paper's minimum demotion
-batch) and refine them back.
+Prefill workload (same layer shape): 16 sequences, each a 2048-token
+prefix with half of its pairs BASE plus a 512-token causal chunk.
 
-Output: one JSON line.  ``value`` = algorithmic HBM bytes of the whole step
-/ step time (GB/s); ``tokens_per_s_per_layer`` = decoded query tokens /
-step time.  ``roofline`` prices the decode-attention launches, timed with
-HIP events on the launch stream.  ``cpu_baseline`` times the float64 CPU
-oracle on a bounded sample (all 64 sequences at every BASE fraction),
-whose outputs also serve as a sampled parity check of the GPU outputs.
+One step = one pass over every hot-path operation:
+  for each decode BASE fraction: append the newest token of every sequence
+  as TARGET (rewriting the same values), lower the tags on the host, run
+  decode attention;  append the prefill chunk's K/V and run prefill;  one
+  transition round on the f=0.5 decode pool: demote 16 TARGET pairs (the
+  paper's minimum demotion batch) and refine them back.
+
+Output: one JSON line.  ``value`` = algorithmic HBM bytes of the step's
+decode-attention launches / their time (GB/s, HIP events on the launch
+stream); ``ms_per_step`` is the wall time of the whole step and
+``step_GB_per_s`` its algorithmic bytes over that time;
+``tokens_per_s_per_layer`` = decoded query tokens / decode-attention time.
+``roofline`` prices the elastic decode kernel (the launches at BASE
+fraction 0.25, 0.5 and 1); ``prefill`` reports its own TFLOP/s against the
+dense bf16 matrix peak.  ``cpu_baseline`` times the float64 CPU oracle on a
+bounded sample (every decode sequence at every BASE fraction, plus 2
+prefill sequences), whose outputs also serve as a parity check of the GPU outputs of the same step.
 """
 
 import argparse
+import hashlib
 import json
 import math
 import os
@@ -36,12 +46,16 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+MFMA_BF16_PEAK_TFLOPS = 2500.0
 WORKLOAD = "llama3-8b-decode"
 B, HQ, HKV, D, PAGE = 64, 32, 8, 128, 16
 FRACTIONS = (0.0, 0.25, 0.5, 1.0)
+ELASTIC = (1, 2, 3)          # indices of the fractions decoded by the elastic kernel
 SEED = 1
 TRANSITION_PAIRS = 16
-SAMPLE_SEQS = 64
+PF_SEQS, PF_PREFIX, PF_CHUNK, PF_SEED = 16, 2048, 512, 3
+PF_SAMPLE = 2
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic.json")
 
 
 def parse():
@@ -52,28 +66,108 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device copy (for scaling PMC byte counters)")
+    ap.add_argument("--reduce-pmc", metavar="DIR",
+                    help="fold the rocprofv3 counter CSVs under DIR (pmc_dec_*, pmc_copy_* runs) "
+                         "into the decode traffic summary; no GPU use")
+    ap.add_argument("--decode-only", action="store_true",
+                    help="only the elastic decode launches (for PMC byte counters of that kernel)")
     return ap.parse_args()
 
 
-def decode_bytes(seq_lens, tags_rows, hq, hkv, mode):
-    """Algorithmic HBM bytes of one decode call: every visible K/V element
-    once (2 B TARGET, 1 B BASE), Q and the bf16 output, 4 B of block table
-    per block, plus 1 B of tag per block on the general path."""
-    kv = 0
-    blocks = 0
+def kv_bytes(seq_lens, tags_rows, hkv):
+    """Algorithmic K/V bytes: every visible element once, 2 B TARGET / 1 B BASE."""
+    total = 0
     for s, length in enumerate(seq_lens):
-        nblk = -(-int(length) // PAGE)
-        blocks += nblk
-        full = int(length) // PAGE
-        t = tags_rows[s, :nblk].astype(np.int64)
-        per_tok = 2 * hkv * D
-        tok_bytes = np.where(t == 1, 1, 2) * per_tok
-        kv += int((tok_bytes[:full] * PAGE).sum())
+        length = int(length)
+        nblk = -(-length // PAGE)
+        full = length // PAGE
+        per_tok = np.where(tags_rows[s, :nblk] == 1, 1, 2).astype(np.int64) * (2 * hkv * D)
+        total += int((per_tok[:full] * PAGE).sum())
         if nblk > full:
-            kv += int(tok_bytes[full]) * (int(length) - full * PAGE)
+            total += int(per_tok[full]) * (length - full * PAGE)
+    return total
+
+
+def decode_bytes(seq_lens, tags_rows, hq, hkv, mode):
+    """One decode call: K/V + Q + bf16 output + 4 B of block table per block
+    (+ 1 B of tag per block on the general path)."""
+    blocks = sum(-(-int(l) // PAGE) for l in seq_lens)
     qo = 2 * len(seq_lens) * hq * D * 2
     meta = blocks * 4 + (blocks if mode == 2 else 0) + len(seq_lens) * 4
-    return kv + qo + meta
+    return kv_bytes(seq_lens, tags_rows, hkv) + qo + meta
+
+
+def prefill_flops(prefix, chunk, nseq, hq):
+    return 4 * hq * D * nseq * sum(prefix + i + 1 for i in range(chunk))
+
+
+def source_digest():
+    h = hashlib.sha256()
+    for name in ("attn_device.h", "common.h", "decode.hip"):
+        with open(os.path.join(ROOT, "paper_2609_33536_amd", "csrc", name), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+def measured_traffic():
+    """HBM bytes per f=0.5 decode launch from the committed PMC summary, if it
+    was taken from the current decode source."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            t = json.load(f)
+    except (OSError, ValueError):
+        return None
+    return t if t.get("source_digest") == source_digest() else None
+
+
+def reduce_pmc(directory):
+    """Scale the decode launches' FETCH_SIZE / WRITE_SIZE (KiB per dispatch)
+    by what the same counters read for a 1 GiB device copy, and write the
+    per-launch HBM bytes next to the algorithmic bytes of the same launches."""
+    import csv
+
+    def per_kernel(run, counter):
+        path = os.path.join(directory, f"{run}_{counter}", "run_counter_collection.csv")
+        vals = {}
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
+        return vals
+
+    def log_json(run, key):
+        with open(os.path.join(directory, f"{run}.log")) as f:
+            for line in f:
+                if line.startswith("{") and key in line:
+                    return json.loads(line)
+        raise ValueError(f"no {key} line in {run}.log")
+
+    copy = log_json("pmc_copy_FETCH_SIZE", "copy_calibration_bytes")
+    dec = log_json("pmc_dec_FETCH_SIZE", "decode_only_rounds")
+    scale, per_launch = {}, {}
+    for counter in ("FETCH_SIZE", "WRITE_SIZE"):
+        c = [v for k, vs in per_kernel("pmc_copy", counter).items() if "copyBuffer" in k for v in vs]
+        scale[counter] = copy["copy_calibration_bytes"] / (sum(c) / len(c))
+        d = [v for k, vs in per_kernel("pmc_dec", counter).items() if "decode_kernel" in k for v in vs]
+        nf = len(dec["base_fractions"])
+        rounds = len(d) // nf
+        assert rounds * nf == len(d), (counter, len(d), nf)
+        # launches rotate over the fractions; skip the first round (cold)
+        per_launch[counter] = [float(np.mean(d[nf + i::nf])) * scale[counter] for i in range(nf)]
+    hbm = [f + w for f, w in zip(per_launch["FETCH_SIZE"], per_launch["WRITE_SIZE"])]
+    out = {"source_digest": source_digest(),
+           "kernel": "decode_kernel<Bf16, 4, true, 4>",
+           "base_fractions": dec["base_fractions"],
+           "fetch_scale": round(scale["FETCH_SIZE"], 5), "write_scale": round(scale["WRITE_SIZE"], 5),
+           "fetch_bytes": [round(v) for v in per_launch["FETCH_SIZE"]],
+           "write_bytes": [round(v) for v in per_launch["WRITE_SIZE"]],
+           "algorithmic_bytes": dec["bytes_per_launch"],
+           "hbm_bytes_per_launch": round(float(np.mean(hbm))),
+           "algorithmic_bytes_per_launch": round(float(np.mean(dec["bytes_per_launch"])))}
+    out["hbm_over_algorithmic"] = round(out["hbm_bytes_per_launch"] / out["algorithmic_bytes_per_launch"], 4)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(out, f, indent=1)
+        f.write("\n")
+    print(json.dumps(out))
 
 
 def copy_calibration():
@@ -87,12 +181,67 @@ def copy_calibration():
     print(json.dumps({"copy_calibration_bytes": n, "launches": 5}))
 
 
+def build_decode(torch, kvpool, workloads, steps, warmup):
+    rng = np.random.default_rng(SEED)
+    seq_lens = workloads.seq_lens_uniform(rng, B, 2048, 8192)
+    spare = TRANSITION_PAIRS * (steps + warmup + 2) + 64
+    base = workloads.make_decode_case_torch(seq_lens, HQ, HKV, seed=SEED, outlier_channels=10,
+                                            spare_blocks=spare)
+    host = workloads.extract_sequences(base["pool"], base["block_table"], seq_lens, list(range(B)))
+    host_q = base["q"].view(torch.int16).cpu().numpy().view(np.uint16)
+    pools, pairs_by_f, modes = [], [], []
+    for k, f in enumerate(FRACTIONS):
+        pairs = workloads.choose_pairs(np.random.default_rng(SEED * 1000 + k), seq_lens, f, "random")
+        kv = kvpool.PagedKV(base["pool"].clone(), base["block_table"], seq_lens, base["free"], HKV)
+        if len(pairs):
+            kv.demote(pairs, emit_lo=False)
+            kv.commit()
+        modes.append(kv.relower())
+        pools.append(kv)
+        pairs_by_f.append(pairs)
+    # the newest token of each sequence, to be rewritten with its own values
+    appends = []
+    for kv in pools:
+        sl = np.array([int(kv.mirror.bt[s, (int(l) - 1) // PAGE]) * PAGE + (int(l) - 1) % PAGE
+                       for s, l in enumerate(seq_lens)], dtype=np.int32)
+        view = kv.kv.view(-1, 2, HKV, PAGE, D)
+        blk = torch.from_numpy(sl // PAGE).long().cuda()
+        off = torch.from_numpy(sl % PAGE).long().cuda()
+        appends.append((torch.from_numpy(sl).cuda(), view[blk, 0, :, off, :].contiguous(),
+                        view[blk, 1, :, off, :].contiguous()))
+    return dict(seq_lens=seq_lens, q=base["q"], pools=pools, pairs=pairs_by_f, modes=modes,
+                appends=appends, host=host, host_q=host_q)
+
+
+def build_prefill(torch, kvpool, workloads):
+    c = workloads.make_prefill_case([PF_PREFIX] * PF_SEQS, [PF_CHUNK] * PF_SEQS, HQ, HKV, seed=PF_SEED,
+                                    base_fraction=0.5, spare_blocks=2)
+    kv = kvpool.PagedKV(c["pool"], c["block_table"], c["seq_lens"], c["free"], HKV)
+
+    def to_bf16(w):
+        return torch.from_numpy(np.ascontiguousarray(w).view(np.int16)).cuda().view(torch.bfloat16)
+
+    slots = torch.from_numpy(c["slots"]).cuda()
+    k_new, v_new = to_bf16(c["k_new"]), to_bf16(c["v_new"])
+    kv.append(slots, k_new, v_new)
+    if len(c["pairs"]):
+        kv.demote(c["pairs"], emit_lo=False)
+        kv.commit()
+    kv.relower()
+    return dict(case=c, kv=kv, slots=slots, k_new=k_new, v_new=v_new, q=to_bf16(c["q"]),
+                cu=torch.from_numpy(c["cu_q"]).cuda(),
+                out=torch.empty((PF_SEQS * PF_CHUNK, HQ, D), dtype=torch.bfloat16, device="cuda"))
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported in this build "
               "(sharding across GPUs is described in DESIGN.md but not built)", file=sys.stderr)
         return 2
+    if args.reduce_pmc:
+        reduce_pmc(args.reduce_pmc)
+        return 0
     import torch
     if args.copy_calibration:
         copy_calibration()
@@ -102,93 +251,77 @@ def main():
     _ensure_built()
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
-
-    rng = np.random.default_rng(SEED)
-    seq_lens = workloads.seq_lens_uniform(rng, B, 2048, 8192)
-    spare = TRANSITION_PAIRS * (args.steps + args.warmup + 2) + 64
-    print(f"[bench] generating {WORKLOAD}: B={B} Hq={HQ} Hkv={HKV} sum(L)={int(seq_lens.sum())}",
-          file=sys.stderr, flush=True)
-    base = workloads.make_decode_case_torch(seq_lens, HQ, HKV, seed=SEED, outlier_channels=10,
-                                            spare_blocks=spare)
-    q = base["q"]
     scale = 1.0 / math.sqrt(D)
 
-    # oracle inputs for the bounded sample: TARGET data straight from the generator
-    sample_ids = list(range(SAMPLE_SEQS))
-    host_pool, host_bt, host_lens = workloads.extract_sequences(base["pool"], base["block_table"],
-                                                                seq_lens, sample_ids)
-    host_q = q[:SAMPLE_SEQS].view(torch.int16).cpu().numpy().view(np.uint16)
-
-    pools, pairs_by_f, modes = [], [], []
-    for k, f in enumerate(FRACTIONS):
-        prng = np.random.default_rng(SEED * 1000 + k)
-        pairs = workloads.choose_pairs(prng, seq_lens, f, "random")
-        kv = kvpool.PagedKV(base["pool"].clone(), base["block_table"], seq_lens, base["free"], HKV)
-        if len(pairs):
-            kv.demote(pairs, emit_lo=False)
-            kv.commit()
-        modes.append(kv.relower())
-        pools.append(kv)
-        pairs_by_f.append(pairs)
-    del base
-    torch.cuda.synchronize()
-
-    # append: the newest token of each sequence, rewritten with its own values
-    last_slots = np.array([int(pools[0].mirror.bt[s, (int(l) - 1) // PAGE]) * PAGE + (int(l) - 1) % PAGE
-                           for s, l in enumerate(seq_lens)], dtype=np.int32)
-    slots_by_f, knew_by_f, vnew_by_f = [], [], []
-    for kv in pools:
-        sl = np.array([int(kv.mirror.bt[s, (int(l) - 1) // PAGE]) * PAGE + (int(l) - 1) % PAGE
-                       for s, l in enumerate(seq_lens)], dtype=np.int32)
-        blk = torch.from_numpy(sl // PAGE).long().cuda()
-        off = torch.from_numpy(sl % PAGE).long().cuda()
-        view = kv.kv.view(-1, 2, HKV, PAGE, D)
-        knew_by_f.append(view[blk, 0, :, off, :].contiguous())     # [B][Hkv][D]
-        vnew_by_f.append(view[blk, 1, :, off, :].contiguous())
-        slots_by_f.append(torch.from_numpy(sl).cuda())
-    del last_slots
-
+    print(f"[bench] building {WORKLOAD}: B={B} Hq={HQ} Hkv={HKV}", file=sys.stderr, flush=True)
+    dec = build_decode(torch, kvpool, workloads, args.steps, args.warmup)
+    seq_lens, q, pools = dec["seq_lens"], dec["q"], dec["pools"]
     outs = [torch.empty((B, HQ, D), dtype=torch.bfloat16, device="cuda") for _ in FRACTIONS]
     batches = [kv.batch(HQ) for kv in pools]
-    ws_bytes = max(ekv.decode_workspace_bytes(kv.pool, bt) for kv, bt in zip(pools, batches))
-    ws = torch.zeros(ws_bytes, dtype=torch.uint8, device="cuda")
+    ws = torch.zeros(max(ekv.decode_workspace_bytes(kv.pool, bt) for kv, bt in zip(pools, batches)),
+                     dtype=torch.uint8, device="cuda")
 
-    # transition candidates: TARGET pairs of the f=0.5 pool (a round trip keeps them TARGET)
-    tk = FRACTIONS.index(0.5)
-    tpool = pools[tk]
+    if args.decode_only:
+        for _ in range(args.warmup + args.steps):
+            for k in ELASTIC:
+                ekv.attn_decode(pools[k].pool, batches[k], q, outs[k], scale, ws)
+        torch.cuda.synchronize()
+        print(json.dumps({"decode_only_rounds": args.warmup + args.steps,
+                          "base_fractions": [FRACTIONS[k] for k in ELASTIC],
+                          "bytes_per_launch": [decode_bytes(seq_lens, pools[k].mirror.tags, HQ, HKV,
+                                                            dec["modes"][k]) for k in ELASTIC]}))
+        return 0
+
+    print("[bench] building the prefill workload", file=sys.stderr, flush=True)
+    pf = build_prefill(torch, kvpool, workloads)
+    pf_batch = pf["kv"].batch(HQ)
+
+    # transition candidates: TARGET pairs of the f=0.5 pool, newest block excluded
+    tpool = pools[FRACTIONS.index(0.5)]
     trng = np.random.default_rng(SEED * 7 + 3)
-    target_pairs = []
+    cand = []
     for s, l in enumerate(seq_lens):
         nblk = -(-int(l) // PAGE)
         for j in range(int(l) // (2 * PAGE)):
-            if 2 * j + 1 < nblk - 1 and tpool.mirror.tags[s, 2 * j] == 0:   # newest block stays put
-                target_pairs.append((s, j))
-    target_pairs = np.array(target_pairs, dtype=np.int32)
+            if 2 * j + 1 < nblk - 1 and tpool.mirror.tags[s, 2 * j] == 0:
+                cand.append((s, j))
+    cand = np.array(cand, dtype=np.int32)
 
-    step_bytes = {"decode": 0, "append": 0, "transition": 0}
-    decode_bytes_f = [decode_bytes(seq_lens, kv.mirror.tags, HQ, HKV, m) for kv, m in zip(pools, modes)]
-    append_bytes = B * 2 * HKV * D * 2 * 2 + B * 4
     block_bytes = 2 * HKV * PAGE * D * 2
-    transition_bytes = TRANSITION_PAIRS * 4 * block_bytes * 2      # demote + refine, 4 blocks per pair each
-    step_bytes["decode"] = sum(decode_bytes_f)
-    step_bytes["append"] = append_bytes * len(FRACTIONS)
-    step_bytes["transition"] = transition_bytes
+    decode_bytes_f = [decode_bytes(seq_lens, kv.mirror.tags, HQ, HKV, m) for kv, m in zip(pools, dec["modes"])]
+    pfc = pf["case"]
+    pf_bytes = (kv_bytes(pfc["seq_lens"], pf["kv"].mirror.tags, HKV)
+                + 2 * PF_SEQS * PF_CHUNK * HQ * D * 2 + PF_SEQS * (PF_PREFIX + PF_CHUNK) // PAGE * 4)
+    step_bytes = {
+        "decode": sum(decode_bytes_f),
+        "append": len(FRACTIONS) * (B * 2 * HKV * D * 2 * 2 + B * 4)
+                  + PF_SEQS * PF_CHUNK * (2 * HKV * D * 2 * 2 + 4),
+        "prefill": pf_bytes,
+        "transition": TRANSITION_PAIRS * 4 * block_bytes * 2,
+    }
     total_step_bytes = sum(step_bytes.values())
+    pf_flops = prefill_flops(PF_PREFIX, PF_CHUNK, PF_SEQS, HQ)
 
     events = []
 
-    def step(i, timed):
+    def step(timed):
         rec = []
         for k, kv in enumerate(pools):
-            kv.append(slots_by_f[k], knew_by_f[k], vnew_by_f[k])
+            slots, kn, vn = dec["appends"][k]
+            kv.append(slots, kn, vn)
             kv.relower()
-            e0 = torch.cuda.Event(enable_timing=True)
-            e1 = torch.cuda.Event(enable_timing=True)
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             ekv.attn_decode(kv.pool, batches[k], q, outs[k], scale, ws)
             e1.record(stream)
             rec.append((e0, e1))
-        sel = target_pairs[trng.choice(len(target_pairs), TRANSITION_PAIRS, replace=False)]
+        pf["kv"].append(pf["slots"], pf["k_new"], pf["v_new"])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ekv.attn_prefill(pf["kv"].pool, pf_batch, pf["q"], pf["cu"], PF_CHUNK, pf["out"], scale)
+        e1.record(stream)
+        rec.append((e0, e1))
+        sel = cand[trng.choice(len(cand), TRANSITION_PAIRS, replace=False)]
         sel = sel[np.lexsort((sel[:, 1], sel[:, 0]))]
         tpool.commit(wait=False)
         _, lo, _ = tpool.demote(sel)
@@ -197,28 +330,26 @@ def main():
             events.append(rec)
 
     print(f"[bench] warmup {args.warmup} steps", file=sys.stderr, flush=True)
-    for i in range(args.warmup):
-        step(i, False)
+    for _ in range(args.warmup):
+        step(False)
     torch.cuda.synchronize()
     print(f"[bench] timing {args.steps} steps", file=sys.stderr, flush=True)
     t0 = time.perf_counter()
-    for i in range(args.steps):
-        step(i, True)
+    for _ in range(args.steps):
+        step(True)
     torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    ms_per_step = (t1 - t0) * 1e3 / args.steps
+    ms_per_step = (time.perf_counter() - t0) * 1e3 / args.steps
 
-    per_f_ms = [float(np.mean([rec[k][0].elapsed_time(rec[k][1]) for rec in events]))
-                for k in range(len(FRACTIONS))]
-    decode_gbs = [decode_bytes_f[k] / (per_f_ms[k] * 1e-3) / 1e9 for k in range(len(FRACTIONS))]
-    dec_total_ms = sum(per_f_ms)
-    achieved = step_bytes["decode"] / (dec_total_ms * 1e-3) / 1e9
-    value = total_step_bytes / (ms_per_step * 1e-3) / 1e9
-    tok_s = B * len(FRACTIONS) / (ms_per_step * 1e-3)
-
+    nf = len(FRACTIONS)
+    per_ms = [float(np.mean([rec[k][0].elapsed_time(rec[k][1]) for rec in events])) for k in range(nf + 1)]
+    dec_ms, pf_ms = per_ms[:nf], per_ms[nf]
+    dec_gbs = step_bytes["decode"] / (sum(dec_ms) * 1e-3) / 1e9
+    el_ms = [dec_ms[k] for k in ELASTIC]
+    achieved = sum(decode_bytes_f[k] for k in ELASTIC) / (sum(el_ms) * 1e-3) / 1e9
+    traffic = measured_traffic()
     result = {
         "metric": "mixed-fidelity decode attention: achieved HBM GB/s + tokens/s per layer",
-        "value": round(value, 1),
+        "value": round(dec_gbs, 1),
         "unit": "GB/s",
         "n_gpus": 1,
         "steps": args.steps,
@@ -232,63 +363,90 @@ def main():
         "config": {"workload": WORKLOAD, "batch": B, "num_q_heads": HQ, "num_kv_heads": HKV,
                    "head_dim": D, "page_size": PAGE, "context": "uniform[2048,8192] seed 1",
                    "sum_context_tokens": int(seq_lens.sum()), "base_fractions": list(FRACTIONS),
+                   "prefill": f"{PF_SEQS} x ({PF_PREFIX} prefix, 50% BASE pairs, + {PF_CHUNK} chunk)",
                    "transition_pairs_per_step": TRANSITION_PAIRS, "parallelism": "single-gpu"},
-        "tokens_per_s_per_layer": round(tok_s, 1),
+        "tokens_per_s_per_layer": round(B * nf / (sum(dec_ms) * 1e-3), 1),
+        "step_GB_per_s": round(total_step_bytes / (ms_per_step * 1e-3) / 1e9, 1),
         "step_bytes": step_bytes,
-        "decode": [{"base_fraction": f, "mode": ["native", "structured", "general"][modes[k]],
-                    "ms": round(per_f_ms[k], 5), "GB_per_s": round(decode_gbs[k], 1),
-                    "tokens_per_s": round(B / (per_f_ms[k] * 1e-3), 1),
+        "decode": [{"base_fraction": f, "mode": ["native", "structured", "general"][dec["modes"][k]],
+                    "ms": round(dec_ms[k], 5),
+                    "GB_per_s": round(decode_bytes_f[k] / (dec_ms[k] * 1e-3) / 1e9, 1),
+                    "tokens_per_s": round(B / (dec_ms[k] * 1e-3), 1),
                     "realized_base_block_fraction": round(
                         float(sum(pools[k].mirror.tags[s, :-(-int(l) // PAGE)].sum()
-                                  for s, l in enumerate(seq_lens)) /
-                              sum(-(-int(l) // PAGE) for l in seq_lens)), 4)}
+                                  for s, l in enumerate(seq_lens))
+                              / sum(-(-int(l) // PAGE) for l in seq_lens)), 4)}
                    for k, f in enumerate(FRACTIONS)],
-        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
-                     "kernel": "ekv_attn_decode (split-KV decode + combine), all four BASE fractions",
-                     "avg_launch_ms": round(dec_total_ms / len(FRACTIONS), 5)},
+        "prefill": {"ms": round(pf_ms, 5), "TFLOP_per_s": round(pf_flops / (pf_ms * 1e-3) / 1e12, 1),
+                    "mfma_peak_frac": round(pf_flops / (pf_ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+                    "new_tokens_per_s": round(PF_SEQS * PF_CHUNK / (pf_ms * 1e-3), 1)},
+        "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                     "frac": round(achieved / HBM_PEAK_GBS, 4),
+                     "traffic": (traffic["hbm_bytes_per_launch"] if traffic else None),
+                     "kernel": "decode_kernel<Bf16, 4, true, 4> (ekv_attn_decode, elastic path)",
+                     "algorithmic_bytes_per_launch": round(sum(decode_bytes_f[k] for k in ELASTIC) / len(ELASTIC)),
+                     "avg_launch_ms": round(sum(el_ms) / len(el_ms), 5)},
     }
-
+    if traffic:
+        result["roofline"]["traffic_note"] = (
+            "mean over the f=0.25/0.5/1 launches of PMC FETCH_SIZE and WRITE_SIZE, each scaled by "
+            "what it reads for a 1 GiB device copy")
     if not args.no_cpu_baseline:
         print("[bench] cpu_baseline: float64 oracle on the sample", file=sys.stderr, flush=True)
-        result["cpu_baseline"], result["parity"] = cpu_baseline(
-            host_pool, host_bt, host_lens, host_q, pairs_by_f, outs, sample_ids)
+        result["cpu_baseline"], result["parity"] = cpu_baseline(dec, outs, pf)
     print(json.dumps(result), flush=True)
     return 0
 
 
-def cpu_baseline(host_pool, host_bt, host_lens, host_q, pairs_by_f, outs, sample_ids):
+def cpu_baseline(dec, outs, pf):
     from threadpoolctl import threadpool_limits
 
     from oracle import attention as oatt
     from oracle import transitions as otr
+    host_pool, host_bt, host_lens = dec["host"]
     tags0 = np.zeros(host_bt.shape, dtype=np.uint8)
-    remap = {s: r for r, s in enumerate(sample_ids)}
-    total_s = 0.0
-    total_bytes = 0
-    worst = 0.0
+    seconds, nbytes, worst = 0.0, 0, 0.0
+
+    def excess(got, ref):
+        return float((np.abs(got - ref) - (2e-3 + 1e-2 * np.abs(ref))).max())
+
     with threadpool_limits(limits=1):
         for k, f in enumerate(FRACTIONS):
-            pairs = np.array([(remap[s], j) for s, j in pairs_by_f[k] if s in remap],
-                             dtype=np.int32).reshape(-1, 2)
+            pairs = dec["pairs"][k]
             t0 = time.perf_counter()
             pool, bt, tg = host_pool, host_bt, tags0
             if len(pairs):
                 pool, bt, tg, _, _ = otr.demote(pool, bt, tg, pairs, host_lens)
-            ref = oatt.decode(host_q, pool, bt, tg, host_lens)
-            total_s += time.perf_counter() - t0
-            total_bytes += decode_bytes(host_lens, tg, HQ, HKV, 2 if len(pairs) else 0)
-            got = outs[k][:len(sample_ids)].float().cpu().numpy()
-            err = np.abs(got - ref) - (2e-3 + 1e-2 * np.abs(ref))
-            worst = max(worst, float(err.max()))
-            maxabs = float(np.abs(got - ref).max())
-            print(f"[bench] parity f={f}: max|gpu-oracle| = {maxabs:.3e}", file=sys.stderr, flush=True)
-    cb = {"value": round(total_bytes / total_s / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
-          "sample": f"{len(sample_ids)} of {B} sequences at each BASE fraction "
-                    f"{list(FRACTIONS)} (oracle demote + decode, float64, 1 BLAS thread)",
-          "seconds": round(total_s, 2)}
+            ref = oatt.decode(dec["host_q"], pool, bt, tg, host_lens)
+            seconds += time.perf_counter() - t0
+            nbytes += decode_bytes(host_lens, tg, HQ, HKV, 2 if len(pairs) else 0)
+            got = outs[k].float().cpu().numpy()
+            worst = max(worst, excess(got, ref))
+            print(f"[bench] parity decode f={f}: max|gpu-oracle| = {np.abs(got - ref).max():.3e}",
+                  file=sys.stderr, flush=True)
+        c = pf["case"]
+        rows = PF_SAMPLE * PF_CHUNK
+        sub_pairs = c["pairs"][c["pairs"][:, 0] < PF_SAMPLE]
+        t0 = time.perf_counter()
+        pool = otr.append(c["pool"], c["slots"][:rows], c["k_new"][:rows], c["v_new"][:rows])
+        bt, tg = c["block_table"], c["tags"]
+        if len(sub_pairs):
+            pool, bt, tg, _, _ = otr.demote(pool, bt, tg, sub_pairs, c["seq_lens"])
+        ref = oatt.prefill(c["q"][:rows], c["cu_q"][:PF_SAMPLE + 1], pool, bt[:PF_SAMPLE], tg[:PF_SAMPLE],
+                           c["seq_lens"][:PF_SAMPLE])
+        seconds += time.perf_counter() - t0
+        nbytes += kv_bytes(c["seq_lens"][:PF_SAMPLE], tg[:PF_SAMPLE], HKV) + 2 * rows * HQ * D * 2
+        got = pf["out"][:rows].float().cpu().numpy()
+        worst = max(worst, excess(got, ref))
+        print(f"[bench] parity prefill: max|gpu-oracle| = {np.abs(got - ref).max():.3e}", file=sys.stderr,
+              flush=True)
+    cb = {"value": round(nbytes / seconds / 1e9, 4), "unit": "GB/s", "cores": 1, "kind": "oracle",
+          "sample": f"decode: all {B} sequences at each BASE fraction {list(FRACTIONS)}; prefill: "
+                    f"{PF_SAMPLE} of {PF_SEQS} sequences (oracle append/demote/attention, float64, "
+                    f"1 BLAS thread)",
+          "seconds": round(seconds, 2)}
     parity = {"ok": worst <= 0.0, "tolerance": "abs 2e-3 + 1e-2*|ref| (bf16 output)",
-              "sampled_sequences": len(sample_ids)}
+              "checked": f"all decode outputs; prefill outputs of {PF_SAMPLE} sequences"}
     return cb, parity
 
 
