@@ -53,3 +53,41 @@ def host_safety_check(case, kv_pool_words_shape):
 
 def default_scale():
     return 1.0 / math.sqrt(128)
+
+
+def oracle_transition_on_touched(kind, host_pool, bt, tags, seq_lens, pairs, new_blocks=None, lo=None):
+    """Run the oracle's demote/refine on just the blocks the list touches
+    (renumbered densely), so that a multi-GB pool is never copied whole.
+
+    Returns (bt, tags, freed, lo, touched blocks) and writes the transformed
+    blocks back into ``host_pool`` (the oracle's own copy).  Equivalent to the
+    oracle on the whole pool because a transition reads and writes only the
+    blocks of its listed pairs (checked on the CPU against the whole-pool
+    oracle)."""
+    from oracle import transitions as otr
+    pairs = np.asarray(pairs, dtype=np.int64).reshape(-1, 2)
+    s, j = pairs[:, 0], pairs[:, 1]
+    if kind == "demote":
+        touched = np.concatenate([bt[s, 2 * j], bt[s, 2 * j + 1]])
+    else:
+        touched = np.concatenate([bt[s, 2 * j], np.asarray(new_blocks, dtype=np.int64)])
+    blocks, inv = np.unique(touched, return_inverse=True)
+    local = host_pool[blocks]
+    lbt = np.full_like(bt, -1)
+    n = len(pairs)
+    if kind == "demote":
+        lbt[s, 2 * j] = inv[:n]
+        lbt[s, 2 * j + 1] = inv[n:]
+        lpool, lbt2, tg2, lfreed, lo_out = otr.demote(local, lbt, tags, pairs, seq_lens)
+        freed = blocks[lfreed].astype(np.int32)
+    else:
+        lbt[s, 2 * j] = inv[:n]
+        lbt[s, 2 * j + 1] = inv[:n]
+        lpool, lbt2, tg2 = otr.refine(local, lbt, tags, pairs, inv[n:], lo, seq_lens)
+        freed, lo_out = None, None
+    untouched = lbt2 == -1
+    assert np.array_equal(untouched, lbt == -1)
+    bt2 = bt.copy()
+    bt2[~untouched] = blocks[lbt2[~untouched]]
+    host_pool[blocks] = lpool
+    return bt2, tg2, freed, lo_out, blocks

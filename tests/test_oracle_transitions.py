@@ -131,3 +131,30 @@ def test_invalid_refine_lists_rejected():
     with pytest.raises(transitions.InvalidTransition):     # TARGET pair in a refine list
         transitions.refine(c["pool"], c["block_table"], c["tags"], c["pairs"][:1],
                            np.array([0]), np.zeros((1, 2, 2, 2, 4, 16), np.uint8), c["seq_lens"])
+
+
+def test_touched_block_harness_equals_whole_pool_oracle():
+    """The GPU tests run the oracle's transitions on only the blocks a list
+    touches; that must give exactly what the oracle gives on the whole pool."""
+    from tests.gpu_util import oracle_transition_on_touched
+    c = workloads.make_decode_case([64, 130, 96, 200], 4, 2, seed=9, spare_blocks=12)
+    rng = np.random.default_rng(9)
+    lens, bt0 = c["seq_lens"], c["block_table"]
+    tg0 = np.zeros(bt0.shape, dtype=np.uint8)
+    pairs = np.array([(s, j) for s in range(4) for j in range(int(lens[s]) // 32)], dtype=np.int32)
+    dp = pairs[rng.permutation(len(pairs))[:6]]
+    whole = transitions.demote(c["pool"], bt0, tg0, dp, lens)
+    host = c["pool"].copy()
+    bt, tg, freed, lo, touched = oracle_transition_on_touched("demote", host, bt0, tg0, lens, dp)
+    assert np.array_equal(host, whole[0]) and np.array_equal(bt, whole[1]) and np.array_equal(tg, whole[2])
+    assert np.array_equal(freed, whole[3]) and np.array_equal(lo, whole[4])
+    assert len(touched) == 2 * len(dp)
+    fifo = transitions.FreeFifo(c["free"])
+    fifo.commit_freed(freed)
+    rp = dp[[4, 0, 2]]
+    new = fifo.acquire(len(rp))
+    rlo = lo[[4, 0, 2]]
+    whole_r = transitions.refine(whole[0], whole[1], whole[2], rp, new, rlo, lens)
+    bt2, tg2, _, _, _ = oracle_transition_on_touched("refine", host, bt, tg, lens, rp, new, rlo)
+    assert np.array_equal(host, whole_r[0]) and np.array_equal(bt2, whole_r[1])
+    assert np.array_equal(tg2, whole_r[2])
