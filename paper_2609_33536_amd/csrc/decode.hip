@@ -166,6 +166,7 @@ __device__ void merge_head_serial(const DecodeArgs& a, size_t head, int nsplit, 
 // (n rounded down to a multiple of 8 -- waiting longer is always safe).
 template <int COMMON>
 __device__ __forceinline__ void wait_vm(int n) {
+  n = __builtin_amdgcn_readfirstlane(n);   // wave-uniform: scalar branches below
   if (n >= 63) return;
   const int k = n >> 3;
   if (k == COMMON) {
@@ -434,6 +435,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   int ib = icur.b0;
   int islot = 0;
   bool issue_done = false;
+  int n_issued = 0, n_consumed = 0;   // ring slots
 
   auto issue_slot = [&]() {
     if (ib >= icur.b1) {   // enter the next window (its metadata was requested one window ago)
@@ -466,6 +468,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     ops += 8;
     ib += base ? 2 : 1;
     islot = islot + 1 == NSLOT ? 0 : islot + 1;
+    ++n_issued;
     issue_done = ib >= icur.b1 && !i_has_next;
   };
 
@@ -540,7 +543,10 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     if (!issue_done) issue_slot();
 
   while (true) {
-    if (!issue_done) issue_slot();
+    // keep the ring full: NSLOT slots issued and not yet consumed
+#pragma unroll
+    for (int u = 0; u < 2; ++u)
+      if (!issue_done && n_issued - n_consumed < NSLOT) issue_slot();
     c_ops += 8;
     wait_vm<NSLOT - 1>(ops - c_ops);
     const char* sb = sm.ring[cslot];
@@ -565,6 +571,35 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       v_operands<true, 2>(v, vop);
       softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, false, a.scale_log2, g);
       cb += 2;
+      ++n_consumed;
+      cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
+    } else if (NSLOT >= 4 && cb + 1 < ccur.b1) {
+      // two TARGET blocks (the two members of a pair, in consecutive slots):
+      // one softmax step over 32 tokens, two independent QK chains
+      const int cslot2 = cslot + 1 == NSLOT ? 0 : cslot + 1;
+      c_ops += 8;
+      wait_vm<NSLOT - 2>(ops - c_ops);
+      const char* sb2 = sm.ring[cslot2];
+      u32x4 k[2][4], v[2][4];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) {
+        k[0][q] = *reinterpret_cast<const u32x4*>(sb + rk_t[q]);
+        k[1][q] = *reinterpret_cast<const u32x4*>(sb2 + rk_t[q]);
+      }
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        v[0][i] = *reinterpret_cast<const u32x4*>(sb + rv_t[i]);
+        v[1][i] = *reinterpret_cast<const u32x4*>(sb2 + rv_t[i]);
+      }
+      const f32x4 sc[2] = {qk_scores<T, false>(k[0], qop), qk_scores<T, false>(k[1], qop)};
+      const bool tail = cb * kPage + 2 * kPage > ccur.len;
+      zero_tail_v<2>(v, cb * kPage, ccur.len, g);
+      u32x2 vop[2][8];
+      v_operands<false, 2>(v, vop);
+      softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
+      cb += 2;
+      n_consumed += 2;
+      cslot = cslot2 + 1 == NSLOT ? 0 : cslot2 + 1;
     } else {
       u32x4 k[4], v[1][4];
 #pragma unroll
@@ -578,8 +613,9 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       v_operands<false, 1>(v, vop);
       softmax_pv<T, 1>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
       cb += 1;
+      ++n_consumed;
+      cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
     }
-    cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
     if (cb < ccur.b1) continue;
     // window finished
     if (ccur.piece_end) finalize_piece();
