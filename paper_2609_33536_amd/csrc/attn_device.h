@@ -174,6 +174,81 @@ __device__ __forceinline__ void softmax_pv(SplitState& st, const f32x4 (&s)[NG],
   }
 }
 
+// Column-stacked variant for query groups of at most 8 heads: query column
+// n < G and column n + G both hold head n (their scores, max and sum agree),
+// and one 16x16x32 MFMA per head-dim row set covers 32 tokens (NG = 2: the
+// lane's 4 tokens of each of two 16-token groups; NG = 1: one group, the
+// other half zero).  Columns n < G accumulate V^T times the 16-bit head of P,
+// columns G <= n < 2G the 16-bit remainder; stacked_sum() adds the two
+// column sets at the end.  So P still carries ~16 significant bits, and V
+// is neither duplicated nor multiplied twice.
+template <typename T, int NG, int G>
+__device__ __forceinline__ void softmax_pv_stacked(SplitState& st, const f32x4 (&s)[NG], const u32x2 (&vop)[NG][8],
+                                                   int tok0, int lim, bool mask, float scale_log2, int g, int n) {
+  static_assert(2 * G <= 16, "two column sets must fit the 16 MFMA columns");
+  float sc[NG][4];
+#pragma unroll
+  for (int q = 0; q < NG; ++q)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) sc[q][i] = s[q][i] * scale_log2;
+  if (mask) {
+#pragma unroll
+    for (int q = 0; q < NG; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        if (tok0 + q * kPage + 4 * g + i >= lim) sc[q][i] = -__builtin_inff();
+  }
+  float mx = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
+#pragma unroll
+  for (int q = 1; q < NG; ++q) mx = fmaxf(mx, fmaxf(fmaxf(sc[q][0], sc[q][1]), fmaxf(sc[q][2], sc[q][3])));
+  mx = head_max(mx);
+  if (__builtin_amdgcn_ballot_w64(mx > st.m + 8.0f)) {
+    const float m_new = fmaxf(st.m, mx);
+    const float alpha = fast_exp2(st.m - m_new);
+    st.l *= alpha;
+#pragma unroll
+    for (int j = 0; j < 8; ++j) st.o[j] *= alpha;
+    st.m = m_new;
+  }
+  const bool lo_cols = n >= G;
+  uint32_t pw[2][2] = {{0u, 0u}, {0u, 0u}};
+#pragma unroll
+  for (int q = 0; q < NG; ++q) {
+    float p[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sc[q][i] - st.m);
+    st.l += (p[0] + p[1]) + (p[2] + p[3]);
+    uint16_t w[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      float back;
+      const uint16_t hi = Mma<T>::round(p[i], &back);
+      float dummy;
+      const uint16_t lo = Mma<T>::round(p[i] - back, &dummy);
+      w[i] = lo_cols ? lo : hi;
+    }
+    pw[q][0] = (uint32_t)w[0] | ((uint32_t)w[1] << 16);
+    pw[q][1] = (uint32_t)w[2] | ((uint32_t)w[3] << 16);
+  }
+  const u32x4 pb = {pw[0][0], pw[0][1], pw[1][0], pw[1][1]};
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const u32x2 a0 = vop[0][j];
+    const u32x2 a1 = NG == 2 ? vop[NG - 1][j] : u32x2{0u, 0u};
+    st.o[j] = Mma<T>::qk(u32x4{a0.x, a0.y, a1.x, a1.y}, pb, st.o[j]);
+  }
+}
+
+// After column-stacked accumulation: column n (< G) gets its remainder
+// column n + G added (lanes n and n + G of each 16-lane row).
+template <int G>
+__device__ __forceinline__ void stacked_sum(SplitState& st) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j)
+#pragma unroll
+    for (int r = 0; r < 4; ++r) st.o[j][r] += __shfl_xor(st.o[j][r], G);
+}
+
 template <typename T>
 __device__ __forceinline__ void store_row8(void* out, size_t idx, f32x4 a, f32x4 b, bool fp32) {
   if (fp32) {

@@ -241,6 +241,10 @@ struct alignas(16) DecodeSmem {
 template <typename T, int G, bool ELASTIC, int NSLOT>
 __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   __shared__ DecodeSmem<G, ELASTIC, NSLOT> sm;
+  // query groups of at most 8 heads hold each head in two MFMA columns
+  // (n and n + G): P's 16-bit head and remainder accumulate side by side
+  constexpr bool kStack = 2 * G <= 16;
+  constexpr int kQCols = kStack ? 2 * G : G;
   const int lane = threadIdx.x;
   const int n = lane & 15;
   const int g = lane >> 4;
@@ -483,8 +487,8 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   auto load_q = [&](const char* wb) {
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-      qop[k] = (n < G) ? *reinterpret_cast<const u32x4*>(wb + kWinQ + n * 2 * kHeadDim + 16 * (4 * g + k))
-                       : u32x4{0u, 0u, 0u, 0u};
+      qop[k] = (n < kQCols) ? *reinterpret_cast<const u32x4*>(wb + kWinQ + (n % G) * 2 * kHeadDim + 16 * (4 * g + k))
+                            : u32x4{0u, 0u, 0u, 0u};
   };
   load_q(sm.win[0]);
   int cb = ccur.b0;
@@ -506,6 +510,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   int pend_counter[2] = {0, 0}, pend_pieces[2] = {0, 0};
 
   auto finalize_piece = [&]() {
+    if constexpr (kStack) stacked_sum<G>(st);
     const float l = head_sum(st.l);
     const size_t head0 = (size_t)ccur.s * a.num_q_heads + (size_t)ccur.kvh * G;
     const int first = ccur.seq_base + ccur.kvh * ccur.np;
@@ -569,7 +574,8 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       }
       u32x2 vop[2][8];
       v_operands<true, 2>(v, vop);
-      softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, false, a.scale_log2, g);
+      if constexpr (kStack) softmax_pv_stacked<T, 2, G>(st, sc, vop, cb * kPage, ccur.len, false, a.scale_log2, g, n);
+      else softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, false, a.scale_log2, g);
       cb += 2;
       ++n_consumed;
       cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
@@ -596,7 +602,8 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       zero_tail_v<2>(v, cb * kPage, ccur.len, g);
       u32x2 vop[2][8];
       v_operands<false, 2>(v, vop);
-      softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
+      if constexpr (kStack) softmax_pv_stacked<T, 2, G>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g, n);
+      else softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
       cb += 2;
       n_consumed += 2;
       cslot = cslot2 + 1 == NSLOT ? 0 : cslot2 + 1;
@@ -611,7 +618,8 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       zero_tail_v<1>(v, cb * kPage, ccur.len, g);
       u32x2 vop[1][8];
       v_operands<false, 1>(v, vop);
-      softmax_pv<T, 1>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
+      if constexpr (kStack) softmax_pv_stacked<T, 1, G>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g, n);
+      else softmax_pv<T, 1>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
       cb += 1;
       ++n_consumed;
       cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
