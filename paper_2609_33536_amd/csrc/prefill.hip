@@ -4,26 +4,86 @@
 // itself).
 //
 // A workgroup of 4 waves serves one (sequence, KV head, tile of query
-// tokens).  Its query "columns" are (token, head-in-group) pairs, 16 per
-// MFMA column group; each wave owns NCG groups, so one K/V block brought
-// into LDS feeds 4 * 16 * NCG query columns.  K/V blocks stream through an
-// LDS ring shared by the four waves (each wave issues a quarter of every
-// slot's direct-to-LDS loads, then the waves meet at a barrier); a slot is
-// one TARGET block or one packed BASE pair, exactly as in decode, and the
-// per-slot math (QK^T on 16x16x32 MFMA, online softmax, PV with P split into
-// a 16-bit head and remainder) is the decode's.  Column c of group q sees
-// kv tokens p < lim(c) = prefix + (its chunk index) + 1.
+// tokens).  Each wave owns 32 query "columns" -- (token, head-in-group)
+// pairs -- and the waves share the K/V blocks, which stream through an LDS
+// ring by direct-to-LDS loads (each wave loads a quarter of every K and V
+// tile; the waves meet at a barrier before a tile is read).
 //
-// Block-table entries and tags are fetched per window of 64 blocks; the
-// ring drains at window boundaries.
+// Work unit: 32 keys (two TARGET blocks, or one packed BASE pair, or the
+// lone last block).  On 32x32x16 matrix cores:
+//   S^T (32 keys x 32 columns) = K (32 x 128) . Q^T, 8 products;
+//     lane l holds column l % 32 and keys 8(r/4) + 4(l/32) + r%4, r < 16.
+//   online softmax over those 16 scores (+ the partner lane l ^ 32);
+//   O^T (128 dims x 32 columns) += V^T . P^T, for P's 16-bit head and its
+//     16-bit remainder (P keeps ~16 significant bits), 4 dim tiles x 2
+//     key steps x 2.  The P operand of key step k is the lane's own scores
+//     r = 8k .. 8k+7, so key index 8(l/32) + i of step k stands for key
+//     16k + 8(i/4) + 4(l/32) + i%4; the V^T operand follows the same order.
+// V^T operands come straight from LDS with transposing reads: 16-bit
+// elements (TARGET) by two ds_read_b64_tr_b16, bytes (BASE) by one
+// ds_read_b64_tr_b8 followed by the byte -> high-byte expansion.  Within
+// each 16-lane group such a read hands lane j element j of the rows the
+// group's lanes point at (row 4a + j/4, element j%4 for 16-bit; row
+// 2a + j/8, byte j%8 for 8-bit), so pointing lane 4a + b at key a, dims
+// d + 4b .. (resp. lane 2a + b at key a, dims d + 8b ..) gives lane j
+// keys a = 0..3 (0..7) of dim d + j.
+//
+// Column c sees keys p < lim(c) = prefix + (its chunk index) + 1.
+// Block-table entries and tags are staged in LDS per window of 256 blocks.
+#include <type_traits>
+
 #include "attn_device.h"
 
 namespace ekv {
 namespace {
 
-constexpr int kPrefillWaves = 4;
-constexpr int kPrefillSlots = 3;
-constexpr int kPrefillWindow = 64;
+constexpr int kPfWaves = 4;
+constexpr int kPfRing = 4;        // 8 KiB slots
+constexpr int kPfCols = 32;       // query columns per wave
+constexpr int kPfWindow = 256;    // blocks per metadata window
+
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef short i16x4v __attribute__((ext_vector_type(4)));
+typedef int i32x2v __attribute__((ext_vector_type(2)));
+typedef __attribute__((address_space(3))) i16x4v* lds_i16x4;
+typedef __attribute__((address_space(3))) i32x2v* lds_i32x2;
+
+template <typename T> struct Mma32;
+template <> struct Mma32<Bf16> {
+  static __device__ __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(__builtin_bit_cast(bf16x8, a), __builtin_bit_cast(bf16x8, b),
+                                                   c, 0, 0, 0);
+  }
+};
+template <> struct Mma32<Fp16> {
+  static __device__ __forceinline__ f32x16 mma(u32x4 a, u32x4 b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_f16(__builtin_bit_cast(f16x8, a), __builtin_bit_cast(f16x8, b),
+                                                  c, 0, 0, 0);
+  }
+};
+
+// Two probabilities -> packed 16-bit heads and packed 16-bit remainders
+// (head + remainder = p to ~16 significant bits).  bf16: the head is the
+// upper half of the fp32 word (truncation), one byte permute for the pair.
+template <typename T>
+__device__ __forceinline__ void split_p(float p0, float p1, uint32_t& hi, uint32_t& lo);
+template <>
+__device__ __forceinline__ void split_p<Bf16>(float p0, float p1, uint32_t& hi, uint32_t& lo) {
+  const uint32_t x0 = __float_as_uint(p0), x1 = __float_as_uint(p1);
+  hi = perm(x1, x0, 0x07060302u);   // upper halves: x0 -> low word, x1 -> high word
+  float dummy;
+  const uint16_t e0 = Mma<Bf16>::round(p0 - __uint_as_float(x0 & 0xffff0000u), &dummy);
+  const uint16_t e1 = Mma<Bf16>::round(p1 - __uint_as_float(x1 & 0xffff0000u), &dummy);
+  lo = (uint32_t)e0 | ((uint32_t)e1 << 16);
+}
+template <>
+__device__ __forceinline__ void split_p<Fp16>(float p0, float p1, uint32_t& hi, uint32_t& lo) {
+  float b0, b1, dummy;
+  const uint16_t h0 = Mma<Fp16>::round(p0, &b0), h1 = Mma<Fp16>::round(p1, &b1);
+  const uint16_t e0 = Mma<Fp16>::round(p0 - b0, &dummy), e1 = Mma<Fp16>::round(p1 - b1, &dummy);
+  hi = (uint32_t)h0 | ((uint32_t)h1 << 16);
+  lo = (uint32_t)e0 | ((uint32_t)e1 << 16);
+}
 
 __device__ __forceinline__ void barrier() {
   asm volatile("" ::: "memory");
@@ -31,19 +91,36 @@ __device__ __forceinline__ void barrier() {
   asm volatile("" ::: "memory");
 }
 
-template <typename T, int G, bool ELASTIC, int NCG>
-__global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
-  __shared__ __attribute__((aligned(16))) char ring[kPrefillSlots][kSlotBytes];
-  constexpr int kTokPerGroup = 16 / G;
-  constexpr int kTileTok = kPrefillWaves * NCG * kTokPerGroup;
+// Wait until at most 2n of this wave's vector memory instructions are in
+// flight (each ring slot costs a wave two loads); n is rounded down.
+__device__ __forceinline__ void wait_slots(int n) {
+  n = __builtin_amdgcn_readfirstlane(n);
+  switch (n < 0 ? 0 : (n > 7 ? 7 : n)) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(14)" ::: "memory"); break;
+  }
+}
+
+template <typename T, int G, bool ELASTIC>
+__global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
+  __shared__ __attribute__((aligned(16))) char ring[kPfRing][kSlotBytes];
+  __shared__ int win_bt[kPfWindow];
+  __shared__ int win_tag[kPfWindow];
+  constexpr int kTileTok = kPfWaves * kPfCols / G;
   const int s = blockIdx.z;
   const int kvh = blockIdx.y;
   const int tile = blockIdx.x;
   const int tid = threadIdx.x;
   const int wave = tid >> 6;
   const int lane = tid & 63;
-  const int n = lane & 15;
-  const int g = lane >> 4;
+  const int n = lane & 31;     // MFMA column
+  const int h = lane >> 5;     // half of the key / head-dim index space
   const int q0 = a.cu_q[s];
   const int nq = a.cu_q[s + 1] - q0;
   const int t_begin = tile * kTileTok;
@@ -51,22 +128,26 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
   const int len = max(0, min(a.seq_lens[s], a.max_blocks * kPage));
   const int prefix = len - nq;
 
-  // this wave's query columns
-  u32x4 qop[NCG][4];
-  int lim[NCG], lim_min[NCG], tq[NCG];
+  // this lane's query column and its Q^T operands (dims 16k + 8h .. + 7)
+  const int col = wave * kPfCols + n;
+  const int tq = t_begin + col / G;
+  const int head = col % G;
+  const bool col_ok = tq < nq;
+  const int lim = col_ok ? min(len, prefix + tq + 1) : len;
+  // The softmax uses exp2(s * c - m) with c = |scale| log2(e) >= 0; a
+  // negative scale is applied by negating Q (exact) instead.
+  const float c_scale = fabsf(a.scale_log2);
+  const uint32_t q_sign = a.scale_log2 < 0.f ? 0x80008000u : 0u;
+  u32x4 qop[8];
+  {
+    const uint16_t* qrow =
+        a.q + ((size_t)(q0 + (col_ok ? tq : 0)) * a.num_q_heads + (size_t)kvh * G + head) * kHeadDim;
 #pragma unroll
-  for (int cg = 0; cg < NCG; ++cg) {
-    const int t_first = t_begin + (wave * NCG + cg) * kTokPerGroup;
-    tq[cg] = t_first + n / G;
-    const int h = n % G;
-    const bool ok = tq[cg] < nq;
-    lim[cg] = ok ? min(len, prefix + tq[cg] + 1) : len;
-    lim_min[cg] = min(len, prefix + t_first + 1);
-    const uint16_t* qrow = a.q + ((size_t)(q0 + (ok ? tq[cg] : 0)) * a.num_q_heads + (size_t)kvh * G + h) * kHeadDim;
-#pragma unroll
-    for (int k = 0; k < 4; ++k)
-      qop[cg][k] = ok ? *reinterpret_cast<const u32x4*>(qrow + 8 * (4 * g + k)) : u32x4{0u, 0u, 0u, 0u};
+    for (int k = 0; k < 8; ++k)
+      qop[k] = col_ok ? (*reinterpret_cast<const u32x4*>(qrow + 16 * k + 8 * h) ^ q_sign) : u32x4{0u, 0u, 0u, 0u};
   }
+  // keys every column of this wave sees (below that no mask is needed)
+  const int lim_wave = min(len, prefix + t_begin + wave * kPfCols / G + 1);
   const int t_last = min(nq, t_begin + kTileTok) - 1;
   const int kv_end = max(1, min(len, prefix + t_last + 1));
   const int nblk = (kv_end + kPage - 1) / kPage;
@@ -88,136 +169,213 @@ __global__ __launch_bounds__(256) void prefill_kernel(PrefillArgs a) {
     }
   }
 
-  uint32_t rk_t[4], rv_t[4], rk_b[2], rv_b[4];
-#pragma unroll
-  for (int k = 0; k < 4; ++k) rk_t[k] = n * (2 * kHeadDim) + 16 * ((4 * g + k) ^ n);
-#pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int t = 4 * g + i;
-    rv_t[i] = kTileBytes + t * (2 * kHeadDim) + 16 * (n ^ t);
-    rv_b[i] = kTileBytes + t * kHeadDim + 16 * ((n >> 1) ^ tau(t)) + 8 * (n & 1);
-  }
-#pragma unroll
-  for (int h = 0; h < 2; ++h) rk_b[h] = n * kHeadDim + 16 * ((2 * g + h) ^ tau(n));
-  // each wave loads quarter `wave` of every 4 KiB plane tile of a slot
-  const DmaOffsets dma = dma_offsets(lane + 64 * wave);   // row `wave` of the per-lane offsets
+  // each wave loads quarter `wave` of every K and V tile of a slot
+  const DmaOffsets dma = dma_offsets(lane + 64 * wave);
   const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTileBytes;
   const char* pool = reinterpret_cast<const char*>(a.pool) + (size_t)kvh * kTileBytes;
   const size_t v_off = (size_t)a.num_kv_heads * kTileBytes;
   const int32_t* btrow = a.bt + (size_t)s * a.max_blocks;
+  const uint8_t* tagrow = a.tags ? a.tags + (size_t)s * a.max_blocks : nullptr;
 
-  SplitState st[NCG];
+  // LDS reads.  K (A operand of S^T): key row m = lane % 32.  V^T: the
+  // 16-lane group g16 covers dims 16 (g16 & 1) .. + 15 of each 32-dim tile;
+  // within it, position i16 supplies the row address of the transposing read.
+  const int t_row = n & 15;
+  const int g16 = lane >> 4;
+  const int i16 = lane & 15;
+  const int dq = 16 * (g16 & 1);
+  const int tr_a = i16 >> 2, tr_b = i16 & 3;   // 16-bit: key a, dims + 4b
+  const int b8_a = i16 >> 1, b8_b = i16 & 1;   // 8-bit: key a, dims + 8b
+  // byte offsets inside a slot: K rows (per 16-dim step k), V^T rows (per
+  // 32-dim tile t and, for 16-bit elements, per half of the key step)
+  uint32_t off_kt[8], off_kb[8], off_vt[4][2], off_vb[4];
 #pragma unroll
-  for (int cg = 0; cg < NCG; ++cg) {
+  for (int k = 0; k < 8; ++k) {
+    off_kt[k] = t_row * (2 * kHeadDim) + 16 * ((2 * k + h) ^ t_row);
+    off_kb[k] = (n >> 4) * (kTileBytes / 2) + t_row * kHeadDim + 16 * (k ^ tau(t_row)) + 8 * h;
+  }
 #pragma unroll
-    for (int j = 0; j < 8; ++j) st[cg].o[j] = f32x4{0.f, 0.f, 0.f, 0.f};
-    st[cg].m = -__builtin_inff();
-    st[cg].l = 0.f;
+  for (int t = 0; t < 4; ++t) {
+    const int dd = 32 * t + dq + 4 * tr_b;
+#pragma unroll
+    for (int half = 0; half < 2; ++half) {
+      const int key = 8 * half + 4 * h + tr_a;
+      off_vt[t][half] = kTileBytes + key * (2 * kHeadDim) + 16 * ((dd >> 3) ^ key) + 2 * (dd & 7);
+    }
+    const int keyb = 8 * (b8_a >> 2) + 4 * h + (b8_a & 3);
+    off_vb[t] = kTileBytes + keyb * kHeadDim + 16 * (((32 * t + dq) >> 4) ^ tau(keyb)) + 8 * b8_b;
   }
 
-  for (int w0 = 0; w0 < nblk; w0 += kPrefillWindow) {
-    const int w1 = min(nblk, w0 + kPrefillWindow);
-    const int nw = w1 - w0;
-    int bt_lane = lane < nw ? btrow[w0 + lane] : 0;
-    bt_lane = (unsigned)bt_lane < (unsigned)a.num_blocks ? bt_lane : 0;   // never leave the pool
-    const int tag_lane = (use_tags && lane < nw) ? a.tags[(size_t)s * a.max_blocks + w0 + lane] : 0;
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  f32x16 o[4];
+#pragma unroll
+  for (int t = 0; t < 4; ++t) o[t] = f32x16{};
+  float m_run = -__builtin_inff();   // reference max, log2 units (same in lanes l and l ^ 32)
+  float l_run = 0.f;                 // running sum over this lane's keys
+
+  for (int w0 = 0; w0 < nblk; w0 += kPfWindow) {
+    const int w1 = min(nblk, w0 + kPfWindow);
+    barrier();   // the ring and the window buffers are free
+    for (int i = tid; i < w1 - w0; i += 64 * kPfWaves) {
+      const int bt = btrow[w0 + i];
+      win_bt[i] = (unsigned)bt < (unsigned)a.num_blocks ? bt : 0;   // never leave the pool
+      win_tag[i] = (ELASTIC && use_tags) ? (int)tagrow[w0 + i] : 0;
+    }
+    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
+    barrier();
+
     auto is_base = [&](int blk) -> bool {
       if constexpr (!ELASTIC) return false;
-      else return use_tags ? (__builtin_amdgcn_readlane(tag_lane, blk - w0) != 0)
-                           : (blk >= base_lo && blk < base_hi);
+      else return use_tags ? (win_tag[blk - w0] != 0) : (blk >= base_lo && blk < base_hi);
     };
-    int ib = w0, cb = w0, issued = 0, consumed = 0, islot = 0, cslot = 0;
+    int ib = w0, issued = 0, consumed = 0;
     auto issue = [&]() {
       const bool base = is_base(ib);
-      const char* src = pool + (size_t)__builtin_amdgcn_readlane(bt_lane, ib - w0) * block_bytes;
-      char* dst = ring[islot];
+      const char* src = pool + (size_t)win_bt[ib - w0] * block_bytes;
+      char* dst = ring[issued % kPfRing];
       const uint32_t off = base ? dma.base[0] : dma.tgt[0];
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off), (lds_ptr)(dst + 1024 * wave), 16, 0, 0);
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + v_off + off),
                                        (lds_ptr)(dst + kTileBytes + 1024 * wave), 16, 0, 0);
       ib += base ? 2 : 1;
       ++issued;
-      islot = islot + 1 == kPrefillSlots ? 0 : islot + 1;
     };
 #pragma unroll
-    for (int k = 0; k < kPrefillSlots - 1; ++k)
+    for (int k = 0; k < kPfRing - 1; ++k)
       if (ib < w1) issue();
-    while (cb < w1) {
-      const int ahead = issued - consumed - 1;
-      if (ahead >= 2) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
-      else if (ahead == 1) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
-      else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      barrier();   // every wave's quarter of this slot has landed; the slot reused next is free
-      if (ib < w1) issue();
-      const char* sb = ring[cslot];
-      const int tok0 = cb * kPage;
-      if (is_base(cb)) {
-        u32x4 k[2][4], v[2][4];
+
+    for (int cb = w0; cb < w1;) {
+      // the unit: a BASE pair (one slot), two TARGET blocks, or a lone block
+      const bool base = is_base(cb);
+      const bool two = !base && cb + 1 < w1;
+      const int nslots = two ? 2 : 1;
+      while (issued < consumed + nslots) issue();   // (the ring normally runs ahead)
+      wait_slots(issued - consumed - nslots);
+      barrier();   // every wave's quarters have landed; the slots of the last unit are free
+      while (ib < w1 && issued - consumed < kPfRing) issue();
+
+      const char* sa = ring[consumed % kPfRing];
+      const char* sbk = ring[(consumed + (two ? 1 : 0)) % kPfRing];
+      const int key0 = cb * kPage;
+      const int nkeys = base || two ? 32 : 16;
+
+      auto unit = [&](auto masked) {
+        constexpr bool kMasked = decltype(masked)::value;
+        // ---- S^T = K Q^T ----
+        f32x16 sc = f32x16{};
 #pragma unroll
-        for (int m = 0; m < 2; ++m) {
-          const char* mb = sb + m * (kTileBytes / 2);
-          const u32x4 k0 = *reinterpret_cast<const u32x4*>(mb + rk_b[0]);
-          const u32x4 k1 = *reinterpret_cast<const u32x4*>(mb + rk_b[1]);
-          k[m][0].xy = k0.xy;
-          k[m][1].xy = k0.zw;
-          k[m][2].xy = k1.xy;
-          k[m][3].xy = k1.zw;
-#pragma unroll
-          for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mb + rv_b[i]);
+        for (int k = 0; k < 8; ++k) {
+          u32x4 kop;
+          if (base) kop = expand_base8(*reinterpret_cast<const u32x2*>(sa + off_kb[k]));
+          else kop = *reinterpret_cast<const u32x4*>((n < 16 ? sa : sbk) + off_kt[k]);
+          sc = Mma32<T>::mma(kop, qop[k], sc);
         }
-        u32x2 vop[2][8];
-        v_operands<true, 2>(v, vop);
+
+        // ---- online softmax over this lane's 16 keys (+ lane ^ 32) ----
+        if constexpr (kMasked) {
 #pragma unroll
-        for (int cg = 0; cg < NCG; ++cg) {
-          const f32x4 sc[2] = {qk_scores<T, true>(k[0], qop[cg]), qk_scores<T, true>(k[1], qop[cg])};
-          softmax_pv<T, 2>(st[cg], sc, vop, tok0, lim[cg], tok0 + 2 * kPage > lim_min[cg], a.scale_log2, g);
+          for (int r = 0; r < 16; ++r) {
+            const int key = 8 * (r >> 2) + 4 * h + (r & 3);
+            if (key >= nkeys || key0 + key >= lim) sc[r] = -__builtin_inff();
+          }
         }
-        cb += 2;
-      } else {
-        u32x4 k[4], v[1][4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) k[q] = *reinterpret_cast<const u32x4*>(sb + rk_t[q]);
-#pragma unroll
-        for (int i = 0; i < 4; ++i) v[0][i] = *reinterpret_cast<const u32x4*>(sb + rv_t[i]);
-        zero_tail_v<1>(v, tok0, len, g);
-        u32x2 vop[1][8];
-        v_operands<false, 1>(v, vop);
-#pragma unroll
-        for (int cg = 0; cg < NCG; ++cg) {
-          const f32x4 sc[1] = {qk_scores<T, false>(k, qop[cg])};
-          softmax_pv<T, 1>(st[cg], sc, vop, tok0, lim[cg], tok0 + kPage > lim_min[cg], a.scale_log2, g);
+        float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])), fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
+        mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sc[8], sc[9]), fmaxf(sc[10], sc[11])),
+                             fmaxf(fmaxf(sc[12], sc[13]), fmaxf(sc[14], sc[15]))));
+        {
+          const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
+          mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c_scale;
         }
-        cb += 1;
-      }
-      ++consumed;
-      cslot = cslot + 1 == kPrefillSlots ? 0 : cslot + 1;
+        if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.0f)) {
+          const float m_new = fmaxf(m_run, mx);
+          const float alpha = fast_exp2(m_run - m_new);
+          l_run *= alpha;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) o[t] *= alpha;
+          m_run = m_new;
+        }
+        // P = exp2(s c - m); its 16-bit head by truncation, the remainder
+        // p - head rounded to 16 bits
+        u32x4 phi[2], plo[2];
+        float lsum[2];
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          float p[8];
+#pragma unroll
+          for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(sc[8 * ks + i], c_scale, -m_run));
+          lsum[ks] = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
+          uint32_t wh[4], wl[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) split_p<T>(p[2 * u], p[2 * u + 1], wh[u], wl[u]);
+          phi[ks] = u32x4{wh[0], wh[1], wh[2], wh[3]};
+          plo[ks] = u32x4{wl[0], wl[1], wl[2], wl[3]};
+        }
+        l_run += lsum[0] + lsum[1];
+
+        // ---- O^T += V^T P^T (16-bit head and remainder of P) ----
+#pragma unroll
+        for (int ks = 0; ks < 2; ++ks) {
+          if (kMasked && ks == 1 && nkeys < 32) break;
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            u32x4 vop;
+            if (base) {
+              const i32x2v raw =
+                  __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2)(sa + ks * (kTileBytes / 2) + off_vb[t]));
+              vop = expand_base8(u32x2{(uint32_t)raw[0], (uint32_t)raw[1]});
+            } else {
+              const char* sl = ks == 0 ? sa : sbk;
+              uint32_t w[4];
+#pragma unroll
+              for (int half = 0; half < 2; ++half) {
+                const u32x2 pr = __builtin_bit_cast(
+                    u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4)(sl + off_vt[t][half])));
+                w[2 * half] = pr.x;
+                w[2 * half + 1] = pr.y;
+              }
+              if (kMasked) {   // keys at or past the sequence end: zero V (their slots hold anything)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                  const int key = 16 * ks + 8 * (e >> 2) + 4 * h + (e & 3);
+                  if (key0 + key >= len) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+                }
+              }
+              vop = u32x4{w[0], w[1], w[2], w[3]};
+            }
+            o[t] = Mma32<T>::mma(vop, phi[ks], o[t]);
+            o[t] = Mma32<T>::mma(vop, plo[ks], o[t]);
+          }
+        }
+      };
+      if (key0 + nkeys > lim_wave || nkeys < 32) unit(std::true_type{});
+      else unit(std::false_type{});
+      consumed += nslots;
+      cb += base || two ? 2 : 1;
     }
-    barrier();   // the ring is reused by the next window
   }
 
+  // ---- output: this lane holds dims 32t + 8u + 4h .. + 3 of its column ----
+  const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(l_run), __float_as_uint(l_run), false, false);
+  const float l_tot = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
+  if (col_ok) {
+    const float inv = 1.0f / l_tot;
+    const size_t row = ((size_t)(q0 + tq) * a.num_q_heads + (size_t)kvh * G + head) * kHeadDim;
 #pragma unroll
-  for (int cg = 0; cg < NCG; ++cg) {
-    const float l = head_sum(st[cg].l);
-    if (tq[cg] < nq) {
-      const float inv = 1.0f / l;
-      const size_t row = ((size_t)(q0 + tq[cg]) * a.num_q_heads + (size_t)kvh * G + n % G) * kHeadDim;
+    for (int t = 0; t < 4; ++t)
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        store_row8<T>(a.out, row + 32 * g + 8 * r,
-                      f32x4{st[cg].o[0][r], st[cg].o[1][r], st[cg].o[2][r], st[cg].o[3][r]} * inv,
-                      f32x4{st[cg].o[4][r], st[cg].o[5][r], st[cg].o[6][r], st[cg].o[7][r]} * inv, a.out_fp32);
-    }
+      for (int u = 0; u < 4; ++u) {
+        const size_t idx = row + 32 * t + 8 * u + 4 * h;
+        store_pair<T>(a.out, idx, o[t][4 * u] * inv, o[t][4 * u + 1] * inv, a.out_fp32);
+        store_pair<T>(a.out, idx + 2, o[t][4 * u + 2] * inv, o[t][4 * u + 3] * inv, a.out_fp32);
+      }
   }
 }
 
 template <typename T, int G>
 hipError_t launch_typed(const PrefillArgs& a, bool elastic, hipStream_t st) {
-  constexpr int kNcg = 2;
-  constexpr int kTileTok = kPrefillWaves * kNcg * (16 / G);
+  constexpr int kTileTok = kPfWaves * kPfCols / G;
   dim3 grid((a.max_q_len + kTileTok - 1) / kTileTok, a.num_kv_heads, a.batch);
-  if (elastic) hipLaunchKernelGGL((prefill_kernel<T, G, true, kNcg>), grid, dim3(256), 0, st, a);
-  else hipLaunchKernelGGL((prefill_kernel<T, G, false, kNcg>), grid, dim3(256), 0, st, a);
+  if (elastic) hipLaunchKernelGGL((prefill_kernel<T, G, true>), grid, dim3(64 * kPfWaves), 0, st, a);
+  else hipLaunchKernelGGL((prefill_kernel<T, G, false>), grid, dim3(64 * kPfWaves), 0, st, a);
   return hipGetLastError();
 }
 
