@@ -77,26 +77,21 @@ __device__ __forceinline__ float wave_sum(float x) {
 
 // Merge the nsplit (<= 64) partials of the G heads of one (sequence, KV
 // head): out = sum_k w_k o_k / sum_k w_k l_k with w_k = exp2(m_k - max m).
-// Lane k holds split k's weight; for the numerators lane (c, par) =
+// Lane k holds split k's (max, sum); for the numerators lane (c, par) =
 // (lane & 31, lane >> 5) owns head-dim columns 4c..4c+3 of the splits with
-// parity par, and keeps up to 16 coherent loads in flight at a time.
+// parity par.  The (max, sum) loads and the first 16 row loads are issued
+// together, so a merge of up to 2 * kB splits costs one memory round trip.
 template <typename T, int G>
 __device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int lane) {
   constexpr int kB = G >= 16 ? 1 : 16 / G;     // split pairs per batch
-  float wk[G], inv_den[G];
-  f32x4 num[G];
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    const float* ml = a.ws_ml + 2 * (head0 + h) * a.max_splits;
-    const float2 mlk = lane < nsplit ? load_agent_f2(ml + 2 * lane) : make_float2(-__builtin_inff(), 0.f);
-    const float mmax = wave_max(mlk.x);
-    wk[h] = lane < nsplit ? fast_exp2(mlk.x - mmax) : 0.f;
-    inv_den[h] = 1.0f / wave_sum(wk[h] * mlk.y);
-    num[h] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
   const int c = lane & 31, par = lane >> 5;
-  for (int k0 = 0; k0 < nsplit; k0 += 2 * kB) {
-    f32x4 v[G][kB];
+  float2 mlk[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h)
+    mlk[h] = lane < nsplit ? load_agent_f2(a.ws_ml + 2 * ((head0 + h) * a.max_splits + lane))
+                           : make_float2(-__builtin_inff(), 0.f);
+  f32x4 v[G][kB];
+  auto load_batch = [&](int k0) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
       const float* o = a.ws_o + (head0 + h) * a.max_splits * kHeadDim + 4 * c;
@@ -106,6 +101,18 @@ __device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int 
         v[h][b] = k < nsplit ? load_agent_f4(o + (size_t)k * kHeadDim) : f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
+  };
+  load_batch(0);
+  float wk[G], inv_den[G];
+  f32x4 num[G];
+#pragma unroll
+  for (int h = 0; h < G; ++h) {
+    const float mmax = wave_max(mlk[h].x);
+    wk[h] = lane < nsplit ? fast_exp2(mlk[h].x - mmax) : 0.f;
+    inv_den[h] = 1.0f / wave_sum(wk[h] * mlk[h].y);
+    num[h] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+  for (int k0 = 0;;) {
 #pragma unroll
     for (int h = 0; h < G; ++h)
 #pragma unroll
@@ -115,6 +122,9 @@ __device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int 
         const float w1 = k + 1 < 64 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[h]), k + 1)) : 0.f;
         num[h] += (par ? w1 : w0) * v[h][b];
       }
+    k0 += 2 * kB;
+    if (k0 >= nsplit) break;
+    load_batch(k0);
   }
 #pragma unroll
   for (int h = 0; h < G; ++h) {
@@ -252,13 +262,14 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   const int B = a.batch;
 
   // ---- the range of this workgroup -------------------------------------
+  const int len0 = lane < B ? clamp_len(a.seq_lens[lane], a.len_cap) : 0;   // kept: sequences 0..63
   int total_pairs = 0;
   for (int c0 = 0; c0 < B; c0 += 512) {
     int np8[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int idx = c0 + 64 * u + lane;
-      np8[u] = idx < B ? pairs_of(clamp_len(a.seq_lens[idx], a.len_cap)) : 0;
+      np8[u] = pairs_of(idx < 64 ? len0 : (idx < B ? clamp_len(a.seq_lens[idx], a.len_cap) : 0));
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) total_pairs += __builtin_amdgcn_readfirstlane(wave_sum_int(np8[u]));
@@ -286,7 +297,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     int cum = 0;
     for (int c0 = 0;; c0 += 64) {
       const int idx = c0 + lane;
-      const int len = idx < B ? clamp_len(a.seq_lens[idx], a.len_cap) : 0;
+      const int len = c0 == 0 ? len0 : (idx < B ? clamp_len(a.seq_lens[idx], a.len_cap) : 0);
       const int np = pairs_of(len);
       const int incl = wave_incl_scan(np, lane);
       const uint64_t hit = __builtin_amdgcn_ballot_w64(hkv * (cum + incl) > start);
@@ -645,12 +656,16 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   // ---- merges ----------------------------------------------------------
   if (pend_n == 0) return;
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // partials have landed before they are counted
+  // both counters are bumped before either result is awaited
+  uint32_t prev0 = 0u, prev1 = 0u;
+  if (lane == 0) {
+    prev0 = __hip_atomic_fetch_add(a.counters + pend_counter[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (pend_n > 1)
+      prev1 = __hip_atomic_fetch_add(a.counters + pend_counter[1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
   for (int k = 0; k < pend_n; ++k) {
     uint32_t* counter = a.counters + pend_counter[k];
-    uint32_t prev = 0;
-    if (lane == 0) prev = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    prev = __builtin_amdgcn_readfirstlane(prev);
-    if (prev != (uint32_t)(pend_pieces[k] - 1)) continue;
+    if (__builtin_amdgcn_readfirstlane(k == 0 ? prev0 : prev1) != (uint32_t)(pend_pieces[k] - 1)) continue;
     asm volatile("" ::: "memory");
     if (lane == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     if (pend_pieces[k] <= 64) merge_splits<T, G>(a, pend_head0[k], pend_pieces[k], lane);
