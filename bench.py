@@ -54,7 +54,7 @@ ELASTIC = (1, 2, 3)          # indices of the fractions decoded by the elastic k
 SEED = 1
 TRANSITION_PAIRS = 16
 PF_SEQS, PF_PREFIX, PF_CHUNK, PF_SEED = 16, 2048, 512, 3
-PF_SAMPLE = 2
+PF_SAMPLE = 8
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic.json")
 
 

@@ -1,18 +1,26 @@
 // Dual-mode split-KV decode attention for gfx950 (paper §3.2; App. B.3).
 //
-// One wave (64 lanes) owns one (sequence, KV head, split) work item and
-// streams that split's 16-token KV blocks through the block table.  For
-// each block it forms S^T = K Q^T for the whole query group with one
-// 16x16x32 MFMA chain (tokens x heads, head dim reduced in 4 steps), runs
-// an online softmax, and accumulates O^T += V^T P^T with 16x16x16 MFMAs.
+// One wave (64 lanes) per workgroup.  The work -- every pair of 16-token
+// KV blocks of every (sequence, KV head) -- is flattened and cut into equal
+// contiguous ranges, one per workgroup of a persistent grid; a wave streams
+// its range's blocks through the block table, crossing (sequence, KV head)
+// boundaries.  For each block it forms S^T = K Q^T for the whole query
+// group with one 16x16x32 MFMA chain (tokens x heads, head dim reduced in 4
+// steps), runs an online softmax over 32-token steps, and accumulates
+// O^T += V^T P^T with 16x16x16 MFMAs.
 //
 // Lane (n, g) = (lane & 15, lane >> 4):
 //   QK   A operand: token n of the block, head-dim chunk 4*g + step (8 elems)
-//        B operand: query head n of the group, same chunk (zero if n >= G)
-//        result:    scores of head n for tokens 4g .. 4g+3
+//        B operand: query head n % G of the group, same chunk (zero for
+//        unused columns)
+//        result:    scores of column n for tokens 4g .. 4g+3
 //   PV   A operand: V[4g+i][8n + j] for i = 0..3 (MFMA j = 0..7)
 //        B operand: the lane's own 4 probabilities (no shuffle needed)
-//        result:    O[head n][d], d = 32g + 8r + j, r = 0..3
+//        result:    O[column n][d], d = 32g + 8r + j, r = 0..3
+// For G <= 8 column n < G carries P's 16-bit head and column n + G its
+// 16-bit remainder for the same head, so one product per 16 tokens covers
+// both; the two columns are added when a piece ends.
+//
 // K/V move HBM -> LDS with direct-to-LDS loads (global_load_lds_dwordx4),
 // each instruction one coalesced 1 KiB, into a per-wave ring of NSLOT 8 KiB
 // slots.  A slot holds the (K, V) 4 KiB tiles of one physical block for this
@@ -36,10 +44,10 @@
 // P is split into a 16-bit head and a 16-bit remainder and both are
 // multiplied with V, so the PV product carries ~16 significant bits of P.
 //
-// Splits of one (sequence, KV head) write fp32 partials (o, max, sum); the
-// wave that finishes last -- found with a per-(sequence, KV head) counter in
-// the workspace -- merges them and writes the output, then resets the
-// counter to zero for the next call.
+// Pieces of a (sequence, KV head) cut by range ends write fp32 partials
+// (o, max, sum); the wave that finishes last -- found with a per-(sequence,
+// KV head) counter in the workspace -- merges them and writes the output,
+// then resets the counter to zero for the next call.
 #include "attn_device.h"
 #include "common.h"
 #include "launch.h"
