@@ -59,3 +59,44 @@ def test_dropped_low_byte_in_refine_is_caught(monkeypatch):
                         lambda hi, lo: (np.asarray(hi, np.uint16) << np.uint16(8)).astype(np.uint16))
     with pytest.raises(AssertionError):
         tt.test_round_trip_restores_every_byte()
+
+
+# ---- controller (Alg. 1) ---------------------------------------------------
+
+from oracle import control as ocontrol
+from tests import test_oracle_control as tc
+
+
+@pytest.mark.parametrize("name,bad", [
+    ("shortage", lambda demand, free: max(0, int(free) - int(demand))),           # sign
+    ("demotion_count", lambda eligible, trigger, min_batch: min(eligible, trigger)),  # B_min dropped
+    ("surplus", lambda demoted, delta: int(demoted)),                             # shortage not subtracted
+    ("next_reserve", lambda reserve, decay, e: int(reserve) + int(e)),           # no decay
+    ("promotion_budget", lambda free_post, reserve: int(free_post)),             # reserve ignored
+])
+def test_controller_formula_mistakes_are_caught(monkeypatch, name, bad):
+    monkeypatch.setattr(ocontrol, name, bad)
+    with pytest.raises(AssertionError):
+        tc.test_hand_worked_trace()
+
+
+def test_controller_rank_order_mistakes_are_caught(monkeypatch):
+    orig = ocontrol.eligible_target_pairs
+    monkeypatch.setattr(ocontrol, "eligible_target_pairs", lambda *a, **k: orig(*a, **k)[::-1])
+    with pytest.raises(AssertionError):
+        tc.test_hand_worked_trace()
+    monkeypatch.undo()
+    orig_b = ocontrol.eligible_base_pairs
+    monkeypatch.setattr(ocontrol, "eligible_base_pairs", lambda *a, **k: orig_b(*a, **k)[::-1])
+    with pytest.raises(AssertionError):
+        tc.test_slack_limits_promotions()
+
+
+def test_controller_ignoring_protected_pairs_is_caught(monkeypatch):
+    def no_protection(tags, seq_lens, cfg, backed=None, page=16):
+        plain = ocontrol.Config(min_batch=cfg.min_batch, decay=cfg.decay)
+        return orig(tags, seq_lens, plain, backed, page)
+    orig = ocontrol.eligible_target_pairs
+    monkeypatch.setattr(ocontrol, "eligible_target_pairs", no_protection)
+    with pytest.raises(AssertionError):
+        tc.test_min_batch_capped_by_eligible_pairs()
