@@ -231,6 +231,81 @@ ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,
                                 int32_t page_size, int32_t num_blocks,
                                 const int32_t* h_new_blocks);
 
+/*
+ * Pressure-aware fidelity control (§3.3, Alg. 1; defaults from App. B.1;
+ * the watermark / eager-promotion / no-promotion switches of the ablations
+ * in App. C.7), host only.  One scheduling step is two calls around the
+ * serving scheduler; the caller applies the returned lists with
+ * ekv_demote / ekv_refine (and its block allocator) and keeps the state.
+ *
+ * Eligible TARGET pair (s, j): both tags TARGET, both blocks full
+ * (32 (j+1) <= len), sink_pairs <= j < len/32 - recent_pairs, and, when
+ * h_backed (uint8 [batch][max_blocks], entry of member 0) is given, backed.
+ * Demotion takes eligible pairs oldest first: ascending (j, s).  Promotion
+ * takes BASE pairs (both blocks holding tokens) newest first: descending
+ * j, then ascending s.  (The paper ranks by unspecified runtime signals;
+ * these orders keep every sequence's BASE pairs one run next to its sink,
+ * which the structured attention path serves.)
+ */
+#define EKV_CTRL_SHORTAGE 0          /* demote on a positive shortage (Alg. 1) */
+#define EKV_CTRL_WATERMARK 1         /* demote while free blocks < watermark (ablation) */
+#define EKV_CTRL_EAGER_PROMOTION 1   /* flag: promotion budget ignores the reserve (ablation) */
+#define EKV_CTRL_NO_PROMOTION 2      /* flag: never promote (ablation) */
+
+typedef struct {
+  int32_t min_batch;     /* B_min: fewest pairs a triggered demotion takes (paper: 16) */
+  int32_t decay;         /* lambda: reserve decay per step, in blocks (paper: 2) */
+  int32_t a_max;         /* A_max: no demand probe while free blocks > a_max; < 0: always probe */
+  int32_t sink_pairs;    /* pairs at the start of every sequence never demoted */
+  int32_t recent_pairs;  /* last complete pairs of every sequence never demoted */
+  int32_t policy;        /* EKV_CTRL_SHORTAGE or EKV_CTRL_WATERMARK */
+  int32_t watermark;     /* W of EKV_CTRL_WATERMARK, in blocks */
+  int32_t flags;         /* EKV_CTRL_EAGER_PROMOTION | EKV_CTRL_NO_PROMOTION */
+} ekv_ctrl_config;
+
+typedef struct {
+  int32_t reserve;       /* R: decaying demotion reserve in blocks; start at 0 */
+  int32_t surplus;       /* E_t of the current step (set by ekv_ctrl_demotion) */
+  int32_t shortage;      /* Delta_t of the current step (set by ekv_ctrl_demotion) */
+  int32_t budget;        /* P_t of the current step (set by ekv_ctrl_promotion) */
+} ekv_ctrl_state;
+
+/*
+ * First half of a step, before scheduling.  demand = D_t, the blocks the
+ * step needs (the paper's side-effect-free scheduler dry run, done by the
+ * caller); free_blocks = F_t.  Delta_t = max(0, D_t - F_t), taken as 0
+ * while F_t > a_max.  If the trigger (Delta_t, or max(0, W - F_t) under
+ * EKV_CTRL_WATERMARK) is positive, writes
+ * n_d = min(|eligible|, max(trigger, min_batch)) pairs (s, j) to
+ * h_pairs_out [max_pairs][2] and *n_out = n_d; sets st->shortage = Delta_t
+ * and st->surplus = E_t = max(0, n_d - Delta_t).  Each demoted pair frees
+ * one block once the demotion completes.
+ * h_tags [batch][max_blocks] and h_seq_lens [batch] are host mirrors.
+ * Errors: EKV_ERR_INVALID (NULL pointers, negative sizes, a length beyond
+ * max_blocks*page_size, unknown policy or flags, more than max_pairs
+ * pairs chosen; the state is then unchanged).
+ */
+ekv_status ekv_ctrl_demotion(const ekv_ctrl_config* cfg, ekv_ctrl_state* st, int32_t demand,
+                             int32_t free_blocks, const uint8_t* h_tags, const int32_t* h_seq_lens,
+                             const uint8_t* h_backed, int32_t batch, int32_t max_blocks,
+                             int32_t page_size, int32_t* h_pairs_out, int32_t max_pairs, int32_t* n_out);
+
+/*
+ * Second half, after the step's required scheduling and allocation, with
+ * free_post = F_post free blocks.  Updates st->reserve to
+ * R_t = max(0, R_{t-1} - decay) + E_t and st->budget to
+ * P_t = max(0, F_post - R_t) (F_post under EKV_CTRL_EAGER_PROMOTION); then
+ * writes up to min(P_t, slack) BASE pairs to h_pairs_out [max_pairs][2]
+ * (none under EKV_CTRL_NO_PROMOTION).  slack = the pairs the transfer path
+ * can take this step.  Each promoted pair needs one free block (the new
+ * block of ekv_refine).
+ * Errors: as ekv_ctrl_demotion.
+ */
+ekv_status ekv_ctrl_promotion(const ekv_ctrl_config* cfg, ekv_ctrl_state* st, int32_t free_post, int32_t slack,
+                              const uint8_t* h_tags, const int32_t* h_seq_lens, int32_t batch,
+                              int32_t max_blocks, int32_t page_size, int32_t* h_pairs_out, int32_t max_pairs,
+                              int32_t* n_out);
+
 #ifdef __cplusplus
 }
 #endif

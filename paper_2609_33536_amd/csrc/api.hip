@@ -11,13 +11,17 @@
 
 #include "ekv.h"
 #include "common.h"
+#include "host_status.h"
 #include "launch.h"
 
 namespace {
 
 thread_local std::string g_last_error;
 
-ekv_status fail(ekv_status s, const char* fmt, ...) __attribute__((format(printf, 2, 3)));
+}  // namespace
+
+namespace ekv {
+
 ekv_status fail(ekv_status s, const char* fmt, ...) {
   char buf[512];
   va_list ap;
@@ -27,6 +31,12 @@ ekv_status fail(ekv_status s, const char* fmt, ...) {
   g_last_error = buf;
   return s;
 }
+
+}  // namespace ekv
+
+namespace {
+
+using ekv::fail;
 
 ekv_status hip_status(hipError_t e, const char* what) {
   if (e == hipSuccess) return EKV_OK;

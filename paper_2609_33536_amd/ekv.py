@@ -41,6 +41,21 @@ class Batch(ctypes.Structure):
                 ("boundaries", ctypes.c_void_p)]
 
 
+class CtrlConfig(ctypes.Structure):
+    _fields_ = [("min_batch", ctypes.c_int32), ("decay", ctypes.c_int32), ("a_max", ctypes.c_int32),
+                ("sink_pairs", ctypes.c_int32), ("recent_pairs", ctypes.c_int32), ("policy", ctypes.c_int32),
+                ("watermark", ctypes.c_int32), ("flags", ctypes.c_int32)]
+
+
+class CtrlState(ctypes.Structure):
+    _fields_ = [("reserve", ctypes.c_int32), ("surplus", ctypes.c_int32), ("shortage", ctypes.c_int32),
+                ("budget", ctypes.c_int32)]
+
+
+CTRL_SHORTAGE, CTRL_WATERMARK = 0, 1
+CTRL_EAGER_PROMOTION, CTRL_NO_PROMOTION = 1, 2
+
+
 # name -> (restype, argtypes), in the order of include/ekv.h
 _P, _I, _U, _F, _S = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t, ctypes.c_float, ctypes.c_void_p
 SIGNATURES = {
@@ -56,6 +71,10 @@ SIGNATURES = {
     "ekv_demote": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _I, _I, _P, _P, _S]),
     "ekv_refine": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_check_transition": (_I, [_I, _P, _I, _P, _P, _P, _I, _I, _I, _I, _P]),
+    "ekv_ctrl_demotion": (_I, [ctypes.POINTER(CtrlConfig), ctypes.POINTER(CtrlState), _I, _I, _P, _P, _P,
+                               _I, _I, _I, _P, _I, _P]),
+    "ekv_ctrl_promotion": (_I, [ctypes.POINTER(CtrlConfig), ctypes.POINTER(CtrlState), _I, _I, _P, _P, _I,
+                                _I, _I, _P, _I, _P]),
 }
 
 _lib = None
@@ -188,3 +207,41 @@ def check_transition(kind, pairs, block_table, tags, seq_lens, num_blocks, new_b
     status = lib().ekv_check_transition(kind, pp, pairs.shape[0], bp, tgp, sp, bt.shape[0],
                                         bt.shape[1], page, num_blocks, nbp)
     return status == OK, (lib().ekv_last_error().decode() if status != OK else "")
+
+
+def ctrl_config(min_batch=16, decay=2, a_max=-1, sink_pairs=0, recent_pairs=0, policy=CTRL_SHORTAGE,
+                watermark=0, eager=False, no_promotion=False):
+    """Controller parameters (defaults: App. B.1's B_min = 16, lambda = 2)."""
+    flags = (CTRL_EAGER_PROMOTION if eager else 0) | (CTRL_NO_PROMOTION if no_promotion else 0)
+    return CtrlConfig(min_batch, decay, a_max, sink_pairs, recent_pairs, policy, watermark, flags)
+
+
+def ctrl_demotion(cfg, state, demand, free, tags, seq_lens, backed=None, page=PAGE):
+    """First half of a control step: returns the pairs to demote (int32 [n][2])."""
+    tags, tp = _host(tags, np.uint8)
+    seq_lens, sp = _host(seq_lens, np.int32)
+    bkp = None
+    if backed is not None:
+        backed, bkp = _host(backed, np.uint8)
+    bsz, max_blocks = tags.shape
+    cap = bsz * (max_blocks // 2)
+    out = np.zeros((max(cap, 1), 2), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check(lib().ekv_ctrl_demotion(ctypes.byref(cfg), ctypes.byref(state), int(demand), int(free), tp, sp, bkp,
+                                   bsz, max_blocks, page, out.ctypes.data_as(ctypes.c_void_p), cap,
+                                   ctypes.byref(n)))
+    return out[:n.value].copy()
+
+
+def ctrl_promotion(cfg, state, free_post, slack, tags, seq_lens, page=PAGE):
+    """Second half, after scheduling: returns the pairs to promote (int32 [n][2])."""
+    tags, tp = _host(tags, np.uint8)
+    seq_lens, sp = _host(seq_lens, np.int32)
+    bsz, max_blocks = tags.shape
+    cap = bsz * (max_blocks // 2)
+    out = np.zeros((max(cap, 1), 2), dtype=np.int32)
+    n = ctypes.c_int32(0)
+    _check(lib().ekv_ctrl_promotion(ctypes.byref(cfg), ctypes.byref(state), int(free_post), int(slack), tp, sp,
+                                    bsz, max_blocks, page, out.ctypes.data_as(ctypes.c_void_p), cap,
+                                    ctypes.byref(n)))
+    return out[:n.value].copy()
