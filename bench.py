@@ -391,11 +391,39 @@ def main():
         result["roofline"]["traffic_note"] = (
             "mean over the f=0.25/0.5/1 launches of PMC FETCH_SIZE and WRITE_SIZE, each scaled by "
             "what it reads for a 1 GiB device copy")
+    result["controller"] = controller_cost(ekv, tpool.mirror)
     if not args.no_cpu_baseline:
         print("[bench] cpu_baseline: float64 oracle on the sample", file=sys.stderr, flush=True)
         result["cpu_baseline"], result["parity"] = cpu_baseline(dec, outs, pf)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def controller_cost(ekv, mirror, reps=200):
+    """Host time of one control step (ekv_ctrl_demotion + ekv_ctrl_promotion,
+    Alg. 1) over the 8B workload's host mirror at f=0.5: a shortage of 2
+    blocks (so B_min = 16 pairs are demoted) and a promotion budget of 16.
+    Arrays are marshalled once; the figure is the library's own work."""
+    import ctypes
+    cfg = ekv.ctrl_config(min_batch=16, decay=2, sink_pairs=1, recent_pairs=2)
+    tags = np.ascontiguousarray(mirror.tags, dtype=np.uint8)
+    lens = np.ascontiguousarray(mirror.seq_lens, dtype=np.int32)
+    bsz, max_blocks = tags.shape
+    cap = bsz * (max_blocks // 2)
+    out = np.zeros((cap, 2), dtype=np.int32)
+    tp, lp, op = (x.ctypes.data_as(ctypes.c_void_p) for x in (tags, lens, out))
+    n_d, n_p = ctypes.c_int32(0), ctypes.c_int32(0)
+    lib = ekv.lib()
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        st = ekv.CtrlState()
+        lib.ekv_ctrl_demotion(ctypes.byref(cfg), ctypes.byref(st), 10, 8, tp, lp, None, bsz, max_blocks, PAGE,
+                              op, cap, ctypes.byref(n_d))
+        lib.ekv_ctrl_promotion(ctypes.byref(cfg), ctypes.byref(st), st.surplus + 16, 64, tp, lp, bsz,
+                               max_blocks, PAGE, op, cap, ctypes.byref(n_p))
+    us = (time.perf_counter() - t0) * 1e6 / reps
+    return {"host_us_per_step": round(us, 1), "demoted_pairs": n_d.value, "promoted_pairs": n_p.value,
+            "sequences": int(bsz), "note": "shortage 2 blocks, B_min 16, lambda 2, budget 16"}
 
 
 def cpu_baseline(dec, outs, pf):
