@@ -54,7 +54,7 @@ ELASTIC = (1, 2, 3)          # indices of the fractions decoded by the elastic k
 SEED = 1
 TRANSITION_PAIRS = 16
 PF_SEQS, PF_PREFIX, PF_CHUNK, PF_SEED = 16, 2048, 512, 3
-PF_SAMPLE = 8
+PF_SAMPLE = 16
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "decode_traffic.json")
 
 
@@ -392,11 +392,55 @@ def main():
             "mean over the f=0.25/0.5/1 launches of PMC FETCH_SIZE and WRITE_SIZE, each scaled by "
             "what it reads for a 1 GiB device copy")
     result["controller"] = controller_cost(ekv, tpool.mirror)
+    print("[bench] multi-layer transitions", file=sys.stderr, flush=True)
+    result["transitions_all_layers"] = transitions_all_layers(torch, ekv, stream)
     if not args.no_cpu_baseline:
         print("[bench] cpu_baseline: float64 oracle on the sample", file=sys.stderr, flush=True)
         result["cpu_baseline"], result["parity"] = cpu_baseline(dec, outs, pf)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def transitions_all_layers(torch, ekv, stream, layers=32, pairs=TRANSITION_PAIRS, reps=20):
+    """One demotion batch of the paper's size (16 pairs, App. B.1) across all
+    32 layers of the 8B model in one launch, then its refinement: 32 pools of
+    1024 blocks (2 GiB in all, so successive batches miss the caches), pairs
+    drawn at random from 16 sequences x 64 blocks.  Per pair and layer both
+    directions move 4 block-equivalents (256 KiB at 8 KV heads)."""
+    nb, nseq = 1024, 16
+    block_bytes = 2 * HKV * PAGE * D * 2
+    pools = [torch.empty(nb * block_bytes // 2, dtype=torch.int16, device="cuda") for _ in range(layers)]
+    layer_kv = torch.tensor([p.data_ptr() for p in pools], dtype=torch.int64, device="cuda")
+    pool = ekv.make_pool(pools[0], HKV, "bf16")
+    bt_h = np.arange(nb, dtype=np.int32).reshape(nseq, nb // nseq)
+    bt = torch.from_numpy(bt_h.copy()).cuda()
+    tags = torch.zeros(bt_h.shape, dtype=torch.uint8, device="cuda")
+    freed = torch.empty(pairs, dtype=torch.int32, device="cuda")
+    lo = torch.empty((pairs, layers, block_bytes), dtype=torch.uint8, device="cuda")
+    rng = np.random.default_rng(SEED * 11)
+    all_pairs = np.array([(s, j) for s in range(nseq) for j in range(nb // nseq // 2)], dtype=np.int32)
+    times = []
+    for r in range(reps + 2):
+        sel = all_pairs[np.sort(rng.choice(len(all_pairs), pairs, replace=False))]
+        pairs_d = torch.from_numpy(sel).cuda()
+        member1 = torch.from_numpy(bt_h[sel[:, 0], 2 * sel[:, 1] + 1].copy()).cuda()
+        ev = [torch.cuda.Event(enable_timing=True) for _ in range(3)]
+        ev[0].record(stream)
+        ekv.demote_layers(pool, layer_kv, pairs_d, bt, tags, freed, lo)
+        ev[1].record(stream)
+        ekv.refine_layers(pool, layer_kv, pairs_d, member1, bt, tags, lo)
+        ev[2].record(stream)
+        torch.cuda.synchronize()
+        if r >= 2:
+            times.append((ev[0].elapsed_time(ev[1]), ev[1].elapsed_time(ev[2])))
+    assert np.array_equal(bt.cpu().numpy(), bt_h) and int(tags.sum()) == 0
+    d_ms, r_ms = (float(np.median([t[k] for t in times])) for k in range(2))
+    moved = 4 * block_bytes * pairs * layers
+    del pools, lo
+    return {"layers": layers, "pairs": pairs, "bytes_each_way": moved,
+            "demote_ms": round(d_ms, 4), "demote_GB_per_s": round(moved / (d_ms * 1e-3) / 1e9, 1),
+            "refine_ms": round(r_ms, 4), "refine_GB_per_s": round(moved / (r_ms * 1e-3) / 1e9, 1),
+            "paper_sync_demotion_ms": 25.44}
 
 
 def controller_cost(ekv, mirror, reps=200):

@@ -218,6 +218,32 @@ ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
                       int32_t batch, int32_t max_blocks, const uint8_t* lo_in, hipStream_t stream);
 
 /*
+ * Multi-layer transitions: the same pairs demoted (or refined) in every
+ * layer's pool of a model in one launch.  In paged serving every layer has
+ * its own pool and all layers share one block table, so a pair is one
+ * decision for all layers; the paper's synchronous demotion of one such
+ * batch costs 25.44 ms per invocation (App. C.6), while its traffic is
+ * 4 block-equivalents per pair per layer.  Per layer l the data change is
+ * exactly that of ekv_demote / ekv_refine on pool layer_kv[l]; the block
+ * table, tags and freed list are updated once, after every layer's data.
+ *   pool      shape and dtype shared by every layer (pool->kv must be non-NULL
+ *             -- e.g. layer 0's pool -- but is not read)
+ *   layer_kv  device uint64 [num_layers]: the address of each layer's pool
+ *   lo_out / lo_in  device (or mapped pinned host) uint8
+ *             [n][num_layers][one block's bytes]: a pair's refinement bytes of
+ *             all layers are contiguous
+ * 1 <= num_layers <= 65535.  Other arguments and errors as ekv_demote /
+ * ekv_refine.
+ */
+ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
+                             const int32_t* pairs, int32_t* block_table, uint8_t* tags, int32_t batch,
+                             int32_t max_blocks, int32_t* freed_out, uint8_t* lo_out, hipStream_t stream);
+ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
+                             const int32_t* pairs, const int32_t* new_blocks, int32_t* block_table,
+                             uint8_t* tags, int32_t batch, int32_t max_blocks, const uint8_t* lo_in,
+                             hipStream_t stream);
+
+/*
  * Host-side validation of a transition list against host mirrors (App. B.1:
  * only demotable TARGET pairs and promotable BASE pairs are offered).
  * kind 0 = demotion (pairs must be TARGET), 1 = refinement (pairs must be

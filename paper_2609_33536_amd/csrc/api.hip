@@ -305,9 +305,23 @@ ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int
   if (st != EKV_OK) return st;
   if (n == 0) return EKV_OK;
   if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
-  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), pairs, nullptr, block_table, tags,
-                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks};
+  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
+                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, 1};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
+}
+
+ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
+                             const int32_t* pairs, int32_t* block_table, uint8_t* tags, int32_t batch,
+                             int32_t max_blocks, int32_t* freed_out, uint8_t* lo_out, hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (!layer_kv || num_layers < 1 || num_layers > 65535)
+    return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
+  if (n == 0) return EKV_OK;
+  if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
+  ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
+                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, num_layers};
+  return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
 }
 
 ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
@@ -317,9 +331,24 @@ ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
   if (st != EKV_OK) return st;
   if (n == 0) return EKV_OK;
   if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
-  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks};
+  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
+                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, 1};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
+}
+
+ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
+                             const int32_t* pairs, const int32_t* new_blocks, int32_t* block_table,
+                             uint8_t* tags, int32_t batch, int32_t max_blocks, const uint8_t* lo_in,
+                             hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (!layer_kv || num_layers < 1 || num_layers > 65535)
+    return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
+  if (n == 0) return EKV_OK;
+  if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
+  ekv::TransitionArgs a{nullptr, layer_kv, pairs, new_blocks, block_table, tags,
+                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, num_layers};
+  return hip_status(ekv::launch_refine(a, stream), "ekv_refine_layers launch");
 }
 
 ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,

@@ -35,14 +35,16 @@ hipError_t launch_decode(const DecodeArgs& a, int dtype, int group, bool elastic
 hipError_t launch_zero_u32(uint32_t* p, size_t n, hipStream_t st);
 
 struct TransitionArgs {
-  uint16_t* pool;
+  uint16_t* pool;            // the pool of a single-layer call
+  const uint64_t* layers;    // device [num_layers] pool addresses, or null (single layer: pool)
   const int32_t* pairs;      // [n][2] = (s, j)
   const int32_t* new_blocks; // refine: [n]
   int32_t* bt;               // [B][max_blocks]
   uint8_t* tags;             // [B][max_blocks]
   int32_t* freed;            // demote: [n]
-  uint8_t* lo;               // demote: lo_out (nullable); refine: lo_in
+  uint8_t* lo;               // demote: lo_out (nullable); refine: lo_in; [n][num_layers][one block]
   int32_t n, num_kv_heads, max_blocks;
+  int32_t num_layers;        // 1 for a single-layer call
 };
 
 hipError_t launch_demote(const TransitionArgs& a, hipStream_t st);

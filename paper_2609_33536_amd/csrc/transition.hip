@@ -13,6 +13,11 @@
 // Block-table and tag updates run in a second, tiny kernel after the data
 // kernel on the same stream, so no data wave can observe a half-updated
 // table.
+//
+// A multi-layer call transforms the same pairs in every layer's pool in one
+// launch (grid z = layer): the layers share one block table, as the layers
+// of a paged serving runtime do, so the table is read by every layer's
+// waves and committed once.
 #include "common.h"
 #include "launch.h"
 
@@ -29,6 +34,14 @@ __device__ __forceinline__ u32x2 join_words(uint32_t hi, uint32_t lo) {
 
 __device__ __forceinline__ void wait_all_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
+// The pool of this workgroup's layer (grid z) and its refinement bytes of pair i.
+__device__ __forceinline__ uint16_t* layer_pool(const TransitionArgs& a) {
+  return a.layers ? reinterpret_cast<uint16_t*>(a.layers[blockIdx.z]) : a.pool;
+}
+__device__ __forceinline__ size_t lo_offset(const TransitionArgs& a, int i, size_t block_words) {
+  return ((size_t)i * a.num_layers + blockIdx.z) * (2 * block_words);
+}
+
 __global__ __launch_bounds__(64) void demote_kernel(TransitionArgs a) {
   const int tile = blockIdx.x;   // plane * Hkv + head
   const int i = blockIdx.y;
@@ -36,8 +49,9 @@ __global__ __launch_bounds__(64) void demote_kernel(TransitionArgs a) {
   const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
   const int32_t* row = a.bt + (size_t)s * a.max_blocks;
   const size_t block_words = (size_t)2 * a.num_kv_heads * kTileWords;
-  uint16_t* t0 = a.pool + (size_t)row[2 * j] * block_words + (size_t)tile * kTileWords;
-  const uint16_t* t1 = a.pool + (size_t)row[2 * j + 1] * block_words + (size_t)tile * kTileWords;
+  uint16_t* pool = layer_pool(a);
+  uint16_t* t0 = pool + (size_t)row[2 * j] * block_words + (size_t)tile * kTileWords;
+  const uint16_t* t1 = pool + (size_t)row[2 * j + 1] * block_words + (size_t)tile * kTileWords;
 
   u32x4 w0[4], w1[4];
 #pragma unroll
@@ -54,7 +68,7 @@ __global__ __launch_bounds__(64) void demote_kernel(TransitionArgs a) {
     *reinterpret_cast<u32x2*>(packed + kTileBytes / 2 + off) = u32x2{hi_bytes(w1[r].xy), hi_bytes(w1[r].zw)};
   }
   if (a.lo) {
-    uint8_t* lo = a.lo + (size_t)i * (2 * block_words) + (size_t)tile * kTileBytes;
+    uint8_t* lo = a.lo + lo_offset(a, i, block_words) + (size_t)tile * kTileBytes;
 #pragma unroll
     for (int r = 0; r < 4; ++r) {
       const int off = 8 * lane + 512 * r;
@@ -83,10 +97,11 @@ __global__ __launch_bounds__(64) void refine_kernel(TransitionArgs a) {
   const int lane = threadIdx.x;
   const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
   const size_t block_words = (size_t)2 * a.num_kv_heads * kTileWords;
-  uint16_t* tp = a.pool + (size_t)a.bt[(size_t)s * a.max_blocks + 2 * j] * block_words + (size_t)tile * kTileWords;
-  uint16_t* tq = a.pool + (size_t)a.new_blocks[i] * block_words + (size_t)tile * kTileWords;
+  uint16_t* pool = layer_pool(a);
+  uint16_t* tp = pool + (size_t)a.bt[(size_t)s * a.max_blocks + 2 * j] * block_words + (size_t)tile * kTileWords;
+  uint16_t* tq = pool + (size_t)a.new_blocks[i] * block_words + (size_t)tile * kTileWords;
   const uint8_t* packed = reinterpret_cast<const uint8_t*>(tp);
-  const uint8_t* lo = a.lo + (size_t)i * (2 * block_words) + (size_t)tile * kTileBytes;
+  const uint8_t* lo = a.lo + lo_offset(a, i, block_words) + (size_t)tile * kTileBytes;
 
   u32x2 h0[4], h1[4], l0[4], l1[4];
 #pragma unroll
@@ -139,7 +154,7 @@ __global__ __launch_bounds__(64) void append_kernel(AppendArgs a) {
 
 hipError_t launch_demote(const TransitionArgs& a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  hipLaunchKernelGGL(demote_kernel, dim3(2 * a.num_kv_heads, a.n), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(demote_kernel, dim3(2 * a.num_kv_heads, a.n, a.num_layers), dim3(64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(demote_commit_kernel, dim3((a.n + 255) / 256), dim3(256), 0, st, a);
@@ -148,7 +163,7 @@ hipError_t launch_demote(const TransitionArgs& a, hipStream_t st) {
 
 hipError_t launch_refine(const TransitionArgs& a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  hipLaunchKernelGGL(refine_kernel, dim3(2 * a.num_kv_heads, a.n), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(refine_kernel, dim3(2 * a.num_kv_heads, a.n, a.num_layers), dim3(64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(refine_commit_kernel, dim3((a.n + 255) / 256), dim3(256), 0, st, a);

@@ -70,6 +70,8 @@ SIGNATURES = {
     "ekv_append_kv": (_I, [ctypes.POINTER(Pool), _P, _P, _P, _I, _S]),
     "ekv_demote": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _I, _I, _P, _P, _S]),
     "ekv_refine": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _P, _S]),
+    "ekv_demote_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _I, _I, _P, _P, _S]),
+    "ekv_refine_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_check_transition": (_I, [_I, _P, _I, _P, _P, _P, _I, _I, _I, _I, _P]),
     "ekv_ctrl_demotion": (_I, [ctypes.POINTER(CtrlConfig), ctypes.POINTER(CtrlState), _I, _I, _P, _P, _P,
                                _I, _I, _I, _P, _I, _P]),
@@ -192,6 +194,21 @@ def refine(pool, pairs, new_blocks, block_table, tags, lo_in, stream=None):
     bsz, max_blocks = block_table.shape
     _check(lib().ekv_refine(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(new_blocks),
                             _ptr(block_table), _ptr(tags), bsz, max_blocks, _ptr(lo_in), _stream(stream)))
+
+
+def demote_layers(pool, layer_kv, pairs, block_table, tags, freed_out, lo_out=None, stream=None):
+    """layer_kv: device int64 tensor [L] of the layers' pool addresses."""
+    bsz, max_blocks = block_table.shape
+    _check(lib().ekv_demote_layers(ctypes.byref(pool), _ptr(layer_kv), layer_kv.shape[0], pairs.shape[0],
+                                   _ptr(pairs), _ptr(block_table), _ptr(tags), bsz, max_blocks, _ptr(freed_out),
+                                   _ptr(lo_out), _stream(stream)))
+
+
+def refine_layers(pool, layer_kv, pairs, new_blocks, block_table, tags, lo_in, stream=None):
+    bsz, max_blocks = block_table.shape
+    _check(lib().ekv_refine_layers(ctypes.byref(pool), _ptr(layer_kv), layer_kv.shape[0], pairs.shape[0],
+                                   _ptr(pairs), _ptr(new_blocks), _ptr(block_table), _ptr(tags), bsz, max_blocks,
+                                   _ptr(lo_in), _stream(stream)))
 
 
 def check_transition(kind, pairs, block_table, tags, seq_lens, num_blocks, new_blocks=None, page=PAGE):
