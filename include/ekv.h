@@ -218,6 +218,24 @@ ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
                       int32_t batch, int32_t max_blocks, const uint8_t* lo_in, hipStream_t stream);
 
 /*
+ * Refinement from staged bytes, the last step of asynchronous promotion
+ * (App. B.2: reserve the extra block, restore from the CPU backing while the
+ * BASE mapping stays executable, publish after TARGET is materialised).
+ * The caller has copied pair i's refinement bytes (one block's worth, the
+ * lo layout of ekv_demote) into its reserved block Q = new_blocks[i] --
+ * typically a host-to-device copy from pinned memory on a copy stream --
+ * and orders this call after that copy.  Then, as ekv_refine: member 0 is
+ * rebuilt in place in P = block_table[s][2j], member 1 in place in Q over
+ * the staged bytes, block_table[s][2j+1] = Q and both tags = TARGET.
+ * Until this call the pair is BASE and its mapping untouched, so attention
+ * may run on it while the copy is in flight.
+ * Errors: EKV_ERR_INVALID, EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.
+ */
+ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pairs, const int32_t* new_blocks,
+                             int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,
+                             hipStream_t stream);
+
+/*
  * Multi-layer transitions: the same pairs demoted (or refined) in every
  * layer's pool of a model in one launch.  In paged serving every layer has
  * its own pool and all layers share one block table, so a pair is one

@@ -306,7 +306,7 @@ ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int
   if (n == 0) return EKV_OK;
   if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
-                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, 1};
+                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, 1, 0};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
 }
 
@@ -320,7 +320,7 @@ ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
   if (n == 0) return EKV_OK;
   if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
-                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, num_layers};
+                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, num_layers, 0};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
 }
 
@@ -332,8 +332,20 @@ ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
   if (n == 0) return EKV_OK;
   if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, 1};
+                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, 1, 0};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
+}
+
+ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pairs, const int32_t* new_blocks,
+                             int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,
+                             hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (n == 0) return EKV_OK;
+  if (!new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
+  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
+                        nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1};
+  return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
 }
 
 ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
@@ -347,7 +359,7 @@ ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
   if (n == 0) return EKV_OK;
   if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, num_layers};
+                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, num_layers, 0};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_layers launch");
 }
 

@@ -45,6 +45,7 @@ struct TransitionArgs {
   uint8_t* lo;               // demote: lo_out (nullable); refine: lo_in; [n][num_layers][one block]
   int32_t n, num_kv_heads, max_blocks;
   int32_t num_layers;        // 1 for a single-layer call
+  int32_t staged;            // refine: pair i's refinement bytes are in block new_blocks[i] (lo unused)
 };
 
 hipError_t launch_demote(const TransitionArgs& a, hipStream_t st);

@@ -14,6 +14,11 @@
 // kernel on the same stream, so no data wave can observe a half-updated
 // table.
 //
+// A staged refinement finds a pair's refinement bytes in its new block Q,
+// where an asynchronous host-to-device copy put them while the pair stayed
+// BASE (App. B.2): every wave reads its whole P and Q tiles before writing
+// either, so rebuilding Q over its own staged bytes is still tile-local.
+//
 // A multi-layer call transforms the same pairs in every layer's pool in one
 // launch (grid z = layer): the layers share one block table, as the layers
 // of a paged serving runtime do, so the table is read by every layer's
@@ -101,7 +106,10 @@ __global__ __launch_bounds__(64) void refine_kernel(TransitionArgs a) {
   uint16_t* tp = pool + (size_t)a.bt[(size_t)s * a.max_blocks + 2 * j] * block_words + (size_t)tile * kTileWords;
   uint16_t* tq = pool + (size_t)a.new_blocks[i] * block_words + (size_t)tile * kTileWords;
   const uint8_t* packed = reinterpret_cast<const uint8_t*>(tp);
-  const uint8_t* lo = a.lo + lo_offset(a, i, block_words) + (size_t)tile * kTileBytes;
+  // staged: the refinement bytes were copied into Q itself; its (plane, head)
+  // tile holds exactly the bytes this wave rebuilds that tile from
+  const uint8_t* lo = a.staged ? reinterpret_cast<const uint8_t*>(tq)
+                               : a.lo + lo_offset(a, i, block_words) + (size_t)tile * kTileBytes;
 
   u32x2 h0[4], h1[4], l0[4], l1[4];
 #pragma unroll

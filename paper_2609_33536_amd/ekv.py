@@ -70,6 +70,7 @@ SIGNATURES = {
     "ekv_append_kv": (_I, [ctypes.POINTER(Pool), _P, _P, _P, _I, _S]),
     "ekv_demote": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _I, _I, _P, _P, _S]),
     "ekv_refine": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _P, _S]),
+    "ekv_refine_staged": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _S]),
     "ekv_demote_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _I, _I, _P, _P, _S]),
     "ekv_refine_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_check_transition": (_I, [_I, _P, _I, _P, _P, _P, _I, _I, _I, _I, _P]),
@@ -194,6 +195,13 @@ def refine(pool, pairs, new_blocks, block_table, tags, lo_in, stream=None):
     bsz, max_blocks = block_table.shape
     _check(lib().ekv_refine(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(new_blocks),
                             _ptr(block_table), _ptr(tags), bsz, max_blocks, _ptr(lo_in), _stream(stream)))
+
+
+def refine_staged(pool, pairs, new_blocks, block_table, tags, stream=None):
+    """Refinement whose bytes were copied into each pair's new block beforehand."""
+    bsz, max_blocks = block_table.shape
+    _check(lib().ekv_refine_staged(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(new_blocks),
+                                   _ptr(block_table), _ptr(tags), bsz, max_blocks, _stream(stream)))
 
 
 def demote_layers(pool, layer_kv, pairs, block_table, tags, freed_out, lo_out=None, stream=None):

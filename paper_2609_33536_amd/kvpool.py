@@ -31,6 +31,7 @@ class HostMirror:
         self.num_blocks = int(num_blocks)
         self.page = page
         self.free = deque(int(b) for b in sorted(free_ids))
+        self.reserved = set()   # pairs whose promotion is in flight
 
     def _validate(self, kind, pairs, new_blocks=None):
         ok, msg = ekv.check_transition(kind, pairs, self.bt, self.tags, self.seq_lens,
@@ -54,9 +55,10 @@ class HostMirror:
         """Return demoted pairs' released blocks once the GPU has finished."""
         self.free.extend(int(b) for b in freed)
 
-    def plan_refine(self, pairs):
-        """Validate a refinement list, take one block per pair from the free
-        pool and apply the table update; returns the new blocks."""
+    def reserve_refine(self, pairs):
+        """Validate a refinement list and take one block per pair from the
+        free pool, leaving the table as it is (the pairs stay BASE until
+        :meth:`publish_refine`); returns the new blocks."""
         pairs = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
         n = len(pairs)
         if n > len(self.free):
@@ -64,12 +66,27 @@ class HostMirror:
         new = np.array([self.free.popleft() for _ in range(n)], dtype=np.int32)
         try:
             self._validate(1, pairs, new)
+            for s, j in pairs:
+                if (int(s), int(j)) in self.reserved:
+                    raise ekv.EkvError(ekv.ERR_INVALID, f"pair ({s},{j}) is already being promoted")
         except ekv.EkvError:
             self.free.extendleft(reversed(new.tolist()))
             raise
-        for i, (s, j) in enumerate(pairs):
+        self.reserved.update((int(s), int(j)) for s, j in pairs)
+        return new
+
+    def publish_refine(self, pairs, new):
+        """Apply the table update of a refinement (after its device work)."""
+        for i, (s, j) in enumerate(np.asarray(pairs, dtype=np.int32).reshape(-1, 2)):
             self.bt[s, 2 * j + 1] = new[i]
             self.tags[s, 2 * j] = self.tags[s, 2 * j + 1] = 0
+            self.reserved.discard((int(s), int(j)))
+
+    def plan_refine(self, pairs):
+        """Validate a refinement list, take one block per pair from the free
+        pool and apply the table update; returns the new blocks."""
+        new = self.reserve_refine(pairs)
+        self.publish_refine(pairs, new)
         return new
 
     def lower(self):
@@ -161,3 +178,89 @@ class PagedKV:
 
     def append(self, slots, k, v, stream=None):
         ekv.append_kv(self.pool, slots, k, v, stream)
+
+
+class AsyncPromotion:
+    """CPU backing and asynchronous promotion (App. B.2).
+
+    Demotion runs on the compute stream and emits the pair's refinement
+    bytes; a copy stream moves them into pinned host memory (the CPU
+    backing).  Promotion reserves one free block Q per pair and copies the
+    backing into Q on the copy stream; the pair stays BASE and executable
+    meanwhile.  :meth:`publish` orders the compute stream after a finished
+    copy and runs the staged refinement, which rebuilds the pair and
+    publishes the mapping.  Both streams have the default priority.
+    """
+
+    def __init__(self, kv, copy_stream=None):
+        import torch
+        self.kv = kv
+        self.copy = copy_stream if copy_stream is not None else torch.cuda.Stream()
+        self.backing = {}     # (s, j) -> (pinned uint8 [block bytes], event: backing complete)
+        self.inflight = []    # (copy-done event, pairs, new blocks, pinned sources)
+
+    def demote(self, pairs, stream=None):
+        """Demote on ``stream`` and back the refinement bytes up to the host.
+        Returns (freed ids on device, host freed ids)."""
+        import torch
+        stream = stream if stream is not None else torch.cuda.current_stream()
+        pairs = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
+        freed, lo, host_freed = self.kv.demote(pairs, emit_lo=True, stream=stream)
+        if len(pairs) == 0:
+            return freed, host_freed
+        ready = torch.cuda.Event()
+        ready.record(stream)
+        host = torch.empty(lo.shape, dtype=torch.uint8, pin_memory=True)
+        with torch.cuda.stream(self.copy):
+            self.copy.wait_event(ready)
+            host.copy_(lo, non_blocking=True)
+            lo.record_stream(self.copy)
+        done = torch.cuda.Event()
+        done.record(self.copy)
+        for i, (s, j) in enumerate(pairs):
+            self.backing[(int(s), int(j))] = (host[i], done)
+        return freed, host_freed
+
+    def promote(self, pairs):
+        """Reserve a block per pair and start restoring it from the backing;
+        returns the reserved blocks.  The pairs stay BASE until published."""
+        import torch
+        pairs = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
+        missing = [(int(s), int(j)) for s, j in pairs if (int(s), int(j)) not in self.backing]
+        if missing:
+            raise ekv.EkvError(ekv.ERR_INVALID, f"no CPU backing for pairs {missing[:4]}")
+        new = self.kv.mirror.reserve_refine(pairs)
+        nbytes = self.kv.block_bytes
+        flat = self.kv.kv.view(-1).view(torch.uint8)
+        sources = []
+        with torch.cuda.stream(self.copy):
+            for i, (s, j) in enumerate(pairs):
+                host, done = self.backing.pop((int(s), int(j)))
+                self.copy.wait_event(done)
+                q = int(new[i])
+                flat[q * nbytes:(q + 1) * nbytes].copy_(host, non_blocking=True)
+                sources.append(host)
+        ev = torch.cuda.Event()
+        ev.record(self.copy)
+        self.inflight.append((ev, pairs, new, sources))
+        return new
+
+    def publish(self, wait=False, stream=None):
+        """Publish every promotion whose copy has finished (all, with
+        ``wait``); returns the number of pairs published."""
+        import torch
+        stream = stream if stream is not None else torch.cuda.current_stream()
+        keep, count = [], 0
+        for ev, pairs, new, sources in self.inflight:
+            if not (wait or ev.query()):
+                keep.append((ev, pairs, new, sources))
+                continue
+            stream.wait_event(ev)
+            with torch.cuda.stream(stream):
+                pairs_d = self.kv._upload(pairs)
+                new_d = self.kv._upload(new)
+            ekv.refine_staged(self.kv.pool, pairs_d, new_d, self.kv.bt, self.kv.tags, stream)
+            self.kv.mirror.publish_refine(pairs, new)
+            count += len(pairs)
+        self.inflight = keep
+        return count
