@@ -392,6 +392,8 @@ def main():
             "mean over the f=0.25/0.5/1 launches of PMC FETCH_SIZE and WRITE_SIZE, each scaled by "
             "what it reads for a 1 GiB device copy")
     result["controller"] = controller_cost(ekv, tpool.mirror)
+    print("[bench] asynchronous promotion", file=sys.stderr, flush=True)
+    result["async_promotion"] = async_promotion_cost(torch, kvpool, tpool, cand, stream)
     print("[bench] multi-layer transitions", file=sys.stderr, flush=True)
     result["transitions_all_layers"] = transitions_all_layers(torch, ekv, stream)
     if not args.no_cpu_baseline:
@@ -399,6 +401,41 @@ def main():
         result["cpu_baseline"], result["parity"] = cpu_baseline(dec, outs, pf)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def async_promotion_cost(torch, kvpool, kv, cand, stream, pairs=256):
+    """Asynchronous promotion (App. B.2) of 256 pairs of the f=0.5 8B pool:
+    their refinement bytes (one 64 KiB block each, 16 MiB in all) are backed
+    up to pinned host memory at demotion; promotion then reserves the new
+    blocks and copies the backing into them on the copy stream, and the
+    staged refinement publishes them.  Reported: host time to issue the
+    promotion, the copy's duration on the copy stream, and the host time of
+    the publication after the copy."""
+    eng = kvpool.AsyncPromotion(kv)
+    rng = np.random.default_rng(SEED * 13)
+    kv.commit(wait=True)
+    sel = cand[np.sort(rng.choice(len(cand), pairs, replace=False))]
+    sel = sel[np.lexsort((sel[:, 1], sel[:, 0]))]
+    eng.demote(sel, stream)
+    torch.cuda.synchronize()
+    kv.commit(wait=True)
+    c0, c1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    c0.record(eng.copy)
+    t0 = time.perf_counter()
+    eng.promote(sel)
+    t1 = time.perf_counter()
+    c1.record(eng.copy)
+    c1.synchronize()
+    t2 = time.perf_counter()
+    eng.publish(wait=True, stream=stream)
+    torch.cuda.synchronize()
+    t3 = time.perf_counter()
+    assert int(kv.mirror.tags[sel[:, 0], 2 * sel[:, 1]].sum()) == 0
+    copy_ms = c0.elapsed_time(c1)
+    nbytes = pairs * kv.block_bytes
+    return {"pairs": pairs, "bytes": nbytes, "issue_ms": round((t1 - t0) * 1e3, 3),
+            "copy_ms": round(copy_ms, 3), "copy_GB_per_s": round(nbytes / (copy_ms * 1e-3) / 1e9, 1),
+            "publish_ms": round((t3 - t2) * 1e3, 3)}
 
 
 def transitions_all_layers(torch, ekv, stream, layers=32, pairs=TRANSITION_PAIRS, reps=20):
