@@ -67,14 +67,16 @@ template <> struct Mma32<Fp16> {
 // upper half of the fp32 word (truncation), one byte permute for the pair.
 template <typename T>
 __device__ __forceinline__ void split_p(float p0, float p1, uint32_t& hi, uint32_t& lo);
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+
 template <>
 __device__ __forceinline__ void split_p<Bf16>(float p0, float p1, uint32_t& hi, uint32_t& lo) {
   const uint32_t x0 = __float_as_uint(p0), x1 = __float_as_uint(p1);
   hi = perm(x1, x0, 0x07060302u);   // upper halves: x0 -> low word, x1 -> high word
-  float dummy;
-  const uint16_t e0 = Mma<Bf16>::round(p0 - __uint_as_float(x0 & 0xffff0000u), &dummy);
-  const uint16_t e1 = Mma<Bf16>::round(p1 - __uint_as_float(x1 & 0xffff0000u), &dummy);
-  lo = (uint32_t)e0 | ((uint32_t)e1 << 16);
+  // both remainders rounded to nearest-even in one packed conversion
+  const f32x2v rem = {p0 - __uint_as_float(x0 & 0xffff0000u), p1 - __uint_as_float(x1 & 0xffff0000u)};
+  lo = __builtin_bit_cast(uint32_t, __builtin_convertvector(rem, bf16x2v));
 }
 template <>
 __device__ __forceinline__ void split_p<Fp16>(float p0, float p1, uint32_t& hi, uint32_t& lo) {
@@ -83,6 +85,13 @@ __device__ __forceinline__ void split_p<Fp16>(float p0, float p1, uint32_t& hi, 
   const uint16_t e0 = Mma<Fp16>::round(p0 - b0, &dummy), e1 = Mma<Fp16>::round(p1 - b1, &dummy);
   hi = (uint32_t)h0 | ((uint32_t)h1 << 16);
   lo = (uint32_t)e0 | ((uint32_t)e1 << 16);
+}
+
+// max of three floats in one instruction (finite or -inf inputs)
+__device__ __forceinline__ float max3(float a, float b, float c) {
+  float r;
+  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+  return r;
 }
 
 __device__ __forceinline__ void barrier() {
@@ -278,12 +287,13 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
             if (key >= nkeys || key0 + key >= lim) sc[r] = -__builtin_inff();
           }
         }
-        float mx = fmaxf(fmaxf(fmaxf(sc[0], sc[1]), fmaxf(sc[2], sc[3])), fmaxf(fmaxf(sc[4], sc[5]), fmaxf(sc[6], sc[7])));
-        mx = fmaxf(mx, fmaxf(fmaxf(fmaxf(sc[8], sc[9]), fmaxf(sc[10], sc[11])),
-                             fmaxf(fmaxf(sc[12], sc[13]), fmaxf(sc[14], sc[15]))));
+        const float m0 = max3(sc[0], sc[1], sc[2]), m1 = max3(sc[3], sc[4], sc[5]);
+        const float m2 = max3(sc[6], sc[7], sc[8]), m3 = max3(sc[9], sc[10], sc[11]);
+        const float m4 = max3(sc[12], sc[13], sc[14]);
+        float mx = max3(max3(m0, m1, m2), max3(m3, m4, sc[15]), m0);
         {
           const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-          mx = fmaxf(__uint_as_float(sw[0]), __uint_as_float(sw[1])) * c_scale;
+          mx = max3(__uint_as_float(sw[0]), __uint_as_float(sw[1]), __uint_as_float(sw[1])) * c_scale;
         }
         if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.0f)) {
           const float m_new = fmaxf(m_run, mx);
