@@ -100,3 +100,33 @@ def test_controller_ignoring_protected_pairs_is_caught(monkeypatch):
     monkeypatch.setattr(ocontrol, "eligible_target_pairs", no_protection)
     with pytest.raises(AssertionError):
         tc.test_min_batch_capped_by_eligible_pairs()
+
+
+# ---- 8-bit TARGET / 4-bit BASE ---------------------------------------------
+
+from oracle import fp8 as ofp8
+from tests import test_oracle_fp8 as tf
+
+
+def test_fp8_swapped_nibble_order_is_caught(monkeypatch):
+    monkeypatch.setattr(ofp8, "pack_nibbles",
+                        lambda n: (np.asarray(n, np.uint8)[..., 1::2] | (np.asarray(n, np.uint8)[..., 0::2] << 4)
+                                   ).astype(np.uint8))
+    with pytest.raises(AssertionError):
+        tf.test_nibble_packing_by_hand()
+
+
+def test_fp8_low_nibble_as_base_is_caught(monkeypatch):
+    monkeypatch.setattr(ofp8, "hi_nibble", lambda b: (np.asarray(b, np.uint8) & 0x0F).astype(np.uint8))
+    with pytest.raises(AssertionError):
+        tf.test_base_values_closed_form_and_exact_refinement()
+
+
+def test_fp8_wrong_member_is_caught(monkeypatch):
+    orig = ofp8.block_bytes
+
+    def member0(pool, bt_row, tag_row, i):
+        return orig(pool, bt_row, tag_row, i - (i % 2) if int(tag_row[i]) else i)
+    monkeypatch.setattr(ofp8, "block_bytes", member0)
+    with pytest.raises(AssertionError):
+        tf.test_gather_matches_dense_copy_and_base_reads_packed_member()
