@@ -68,7 +68,24 @@ enum {
   EKV_ERR_HIP = 3           /* a HIP runtime call failed */
 };
 
-enum { EKV_DTYPE_BF16 = 0, EKV_DTYPE_FP16 = 1, EKV_DTYPE_FP32 = 2 };
+enum { EKV_DTYPE_BF16 = 0, EKV_DTYPE_FP16 = 1, EKV_DTYPE_FP32 = 2, EKV_DTYPE_E5M2 = 3 };
+
+/*
+ * 8-bit TARGET / 4-bit BASE pools (the paper notes the contract carries
+ * over to an 8-bit TARGET with a 4-bit executable state, App. C.5):
+ * dtype EKV_DTYPE_E5M2 stores TARGET as FP8 E5M2 bytes -- the high byte of
+ * an FP16 word, executed as that FP16 word with a zero low byte -- in
+ *   pool  uint8 [num_blocks][2][num_kv_heads][page_size][head_dim].
+ * BASE is the byte's high nibble (sign and top three exponent bits),
+ * executed with a zero low nibble; the low nibble refines it exactly.  A
+ * BASE pair packs both members' nibbles into member 0's block: per
+ * (plane, head), the 2 KiB of a TARGET tile hold [member 0 | member 1],
+ * each uint8 [page_size][head_dim / 2] with element e of a row in byte
+ * e / 2, low nibble for even e.  Refinement nibbles ("lo") of a pair use the
+ * same layout and fill exactly one 8-bit block.  Queries are FP16 and
+ * outputs FP16 or FP32.  Supported: decode, append, demote, refine (also
+ * multi-layer and staged); prefill returns EKV_ERR_UNSUPPORTED.
+ */
 
 /* Batch execution mode (§3.2; App. B.3): NATIVE for TARGET-only batches;
  * STRUCTURED when every sequence is TARGET* BASE* TARGET* (described by its
@@ -83,7 +100,7 @@ typedef struct {
   int32_t num_kv_heads;
   int32_t page_size;      /* 16 */
   int32_t head_dim;       /* 128 */
-  int32_t dtype;          /* EKV_DTYPE_BF16 or EKV_DTYPE_FP16 */
+  int32_t dtype;          /* EKV_DTYPE_BF16, EKV_DTYPE_FP16 or EKV_DTYPE_E5M2 */
 } ekv_pool;
 
 typedef struct {

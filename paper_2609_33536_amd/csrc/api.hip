@@ -52,8 +52,8 @@ ekv_status check_pool(const ekv_pool* p) {
     return fail(EKV_ERR_INVALID, "pool sizes must be positive");
   if (p->head_dim != ekv::kHeadDim || p->page_size != ekv::kPage)
     return fail(EKV_ERR_UNSUPPORTED, "only head_dim 128 and page_size 16 are supported");
-  if (p->dtype != EKV_DTYPE_BF16 && p->dtype != EKV_DTYPE_FP16)
-    return fail(EKV_ERR_UNSUPPORTED, "pool dtype must be bf16 or fp16");
+  if (p->dtype != EKV_DTYPE_BF16 && p->dtype != EKV_DTYPE_FP16 && p->dtype != EKV_DTYPE_E5M2)
+    return fail(EKV_ERR_UNSUPPORTED, "pool dtype must be bf16, fp16 or e5m2");
   if (p->num_kv_heads > 64) return fail(EKV_ERR_UNSUPPORTED, "at most 64 KV heads");
   return EKV_OK;
 }
@@ -201,8 +201,9 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
   if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
   if (batch->batch == 0) return EKV_OK;
   if (!q || !out) return fail(EKV_ERR_INVALID, "q and out are required");
-  if (out_dtype != pool->dtype && out_dtype != EKV_DTYPE_FP32)
-    return fail(EKV_ERR_INVALID, "out_dtype must be the pool dtype or fp32");
+  const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
+  if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
+    return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
   if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
   const DecodePlan plan = plan_decode(pool, batch);
   if (!ws || ws_bytes < plan.total)
@@ -249,6 +250,7 @@ ekv_status ekv_attn_prefill(const ekv_pool* pool, const ekv_batch* batch, const 
   if (total_q < 0 || max_q_len < 0) return fail(EKV_ERR_INVALID, "negative sizes");
   if (batch->batch == 0 || total_q == 0) return EKV_OK;
   if (!q || !out || !cu_q) return fail(EKV_ERR_INVALID, "q, cu_q and out are required");
+  if (pool->dtype == EKV_DTYPE_E5M2) return fail(EKV_ERR_UNSUPPORTED, "prefill over 8-bit pools is not built");
   if (out_dtype != pool->dtype && out_dtype != EKV_DTYPE_FP32)
     return fail(EKV_ERR_INVALID, "out_dtype must be the pool dtype or fp32");
   if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
@@ -282,7 +284,7 @@ ekv_status ekv_append_kv(const ekv_pool* pool, const int32_t* slots, const void*
   if (n == 0) return EKV_OK;
   if (!slots || !k || !v) return fail(EKV_ERR_INVALID, "slots, k and v are required");
   ekv::AppendArgs a{static_cast<uint16_t*>(pool->kv), slots, static_cast<const uint16_t*>(k),
-                    static_cast<const uint16_t*>(v), n, pool->num_kv_heads};
+                    static_cast<const uint16_t*>(v), n, pool->num_kv_heads, pool->dtype == EKV_DTYPE_E5M2};
   return hip_status(ekv::launch_append(a, stream), "ekv_append_kv launch");
 }
 
@@ -306,7 +308,7 @@ ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int
   if (n == 0) return EKV_OK;
   if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
-                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, 1, 0};
+                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
 }
 
@@ -320,7 +322,7 @@ ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
   if (n == 0) return EKV_OK;
   if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
-                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, num_layers, 0};
+                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
 }
 
@@ -332,7 +334,7 @@ ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
   if (n == 0) return EKV_OK;
   if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, 1, 0};
+                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
 }
 
@@ -344,7 +346,7 @@ ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pai
   if (n == 0) return EKV_OK;
   if (!new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1};
+                        nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1, pool->dtype == EKV_DTYPE_E5M2};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
 }
 
@@ -359,7 +361,7 @@ ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
   if (n == 0) return EKV_OK;
   if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, num_layers, 0};
+                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_layers launch");
 }
 

@@ -203,6 +203,97 @@ __device__ __forceinline__ void wait_vm(int n) {
   }
 }
 
+// As wait_vm, in steps of 4 (slots of the 8-bit format cost 4 or 8 loads).
+__device__ __forceinline__ void wait_vm4(int n) {
+  n = __builtin_amdgcn_readfirstlane(n);   // wave-uniform: scalar branches below
+  if (n >= 63) return;
+  switch (n >> 2) {
+    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
+    case 1: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
+    case 2: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
+    case 3: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
+    case 4: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
+    case 5: asm volatile("s_waitcnt vmcnt(20)" ::: "memory"); break;
+    case 6: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
+    case 7: asm volatile("s_waitcnt vmcnt(28)" ::: "memory"); break;
+    case 8: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
+    case 9: asm volatile("s_waitcnt vmcnt(36)" ::: "memory"); break;
+    case 10: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
+    case 11: asm volatile("s_waitcnt vmcnt(44)" ::: "memory"); break;
+    case 12: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
+    case 13: asm volatile("s_waitcnt vmcnt(52)" ::: "memory"); break;
+    case 14: asm volatile("s_waitcnt vmcnt(56)" ::: "memory"); break;
+    default: asm volatile("s_waitcnt vmcnt(60)" ::: "memory"); break;
+  }
+}
+
+// ---- 8-bit TARGET / 4-bit BASE slots -------------------------------------
+// A slot holds the K and V tiles of 32 tokens laid out exactly as a 16-bit
+// packed BASE pair ([member 0 | member 1] rows of 128 bytes, swizzled as in
+// dma_offsets), so the byte path reads both formats alike.  A TARGET pair
+// arrives so directly, member m from its own block; a BASE pair arrives as
+// its packed nibbles (2 KiB per tile) in the upper half of the slot and is
+// expanded in place before use.
+
+// Linear copy of a 2 KiB tile: lane L's 16 bytes of load r land at dst + 1024 r + 16 L.
+__device__ __forceinline__ void dma_linear2(const char* src, char* dst, int lane) {
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + 1024 * r + 16 * lane),
+                                     (lds_ptr)(dst + 1024 * r), 16, 0, 0);
+}
+
+// A TARGET pair's tile: loads 0, 1 (member 0) from tile0, 2, 3 (member 1) from tile1.
+__device__ __forceinline__ void dma_pair_bytes(const char* tile0, const char* tile1, const uint32_t (&off)[4],
+                                               char* dst) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r) {
+    const char* src = r < 2 ? tile0 + off[r] : tile1 + (off[r] - kTileBytes / 2);
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src), (lds_ptr)(dst + 1024 * r), 16, 0, 0);
+  }
+}
+
+// The lone last block of a sequence: member 0's rows only.
+__device__ __forceinline__ void dma_member0_bytes(const char* tile0, const uint32_t (&off)[4], char* dst) {
+#pragma unroll
+  for (int r = 0; r < 2; ++r)
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile0 + off[r]), (lds_ptr)(dst + 1024 * r), 16, 0,
+                                     0);
+}
+
+// 8 bytes of nibbles (element 2k low, 2k+1 high in byte k) -> 16 element
+// bytes, each nibble in the high half with a zero low half.
+__device__ __forceinline__ u32x4 expand_nibbles(u32x2 w) {
+  u32x4 r;
+#pragma unroll
+  for (int h = 0; h < 2; ++h) {
+    const uint32_t even = (w[h] << 4) & 0xF0F0F0F0u, odd = w[h] & 0xF0F0F0F0u;
+    r[2 * h] = perm(odd, even, 0x05010400u);
+    r[2 * h + 1] = perm(odd, even, 0x07030602u);
+  }
+  return r;
+}
+
+// Expand a BASE pair's nibbles (K at +4 KiB, V at +6 KiB) into the byte
+// layout over the whole slot.  Lane L takes member L / 32, row (L / 2) % 16,
+// half L % 2 of both planes; the wave reads all it needs before it writes.
+__device__ __forceinline__ void expand_nibbles_in_slot(char* sb, int lane) {
+  const int m = lane >> 5, t = (lane >> 1) & 15, hh = lane & 1;
+  const char* nk = sb + kTileBytes + m * (kTileBytes / 4) + t * (kHeadDim / 2) + 32 * hh;
+  const u32x4 k0 = *reinterpret_cast<const u32x4*>(nk), k1 = *reinterpret_cast<const u32x4*>(nk + 16);
+  const u32x4 v0 = *reinterpret_cast<const u32x4*>(nk + kTileBytes / 2);
+  const u32x4 v1 = *reinterpret_cast<const u32x4*>(nk + kTileBytes / 2 + 16);
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
+  const u32x2 kw[4] = {k0.xy, k0.zw, k1.xy, k1.zw}, vw[4] = {v0.xy, v0.zw, v1.xy, v1.zw};
+  char* row = sb + m * (kTileBytes / 2) + t * kHeadDim;
+#pragma unroll
+  for (int c = 0; c < 4; ++c) {
+    const int pos = 16 * ((4 * hh + c) ^ tau(t));
+    *reinterpret_cast<u32x4*>(row + pos) = expand_nibbles(kw[c]);
+    *reinterpret_cast<u32x4*>(row + kTileBytes + pos) = expand_nibbles(vw[c]);
+  }
+}
+
 __device__ __forceinline__ int wave_sum_int(int x) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
@@ -256,7 +347,7 @@ struct alignas(16) DecodeSmem {
 // written out directly; one cut by range ends leaves one partial per piece,
 // and the last piece to arrive merges them (after its stream has ended).
 // ---------------------------------------------------------------------------
-template <typename T, int G, bool ELASTIC, int NSLOT>
+template <typename T, int G, bool ELASTIC, int NSLOT, bool F8>
 __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   __shared__ DecodeSmem<G, ELASTIC, NSLOT> sm;
   // query groups of at most 8 heads hold each head in two MFMA columns
@@ -433,8 +524,10 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   for (int h = 0; h < 2; ++h) rk_b[h] = n * kHeadDim + 16 * ((2 * g + h) ^ tau(n));
   const DmaOffsets dma = dma_offsets(lane);
 
-  const size_t block_bytes = (size_t)2 * hkv * kTileBytes;
-  const size_t v_off = (size_t)hkv * kTileBytes;
+  // a (plane, head) tile: 4 KiB of 16-bit words, or 2 KiB of bytes (F8)
+  constexpr int kTile = F8 ? kTileBytes / 2 : kTileBytes;
+  const size_t block_bytes = (size_t)2 * hkv * kTile;
+  const size_t v_off = (size_t)hkv * kTile;
 
   // ---- issue side ------------------------------------------------------
   Walker iwk = w0;
@@ -479,17 +572,44 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     const bool base = block_is_base(imode, itag, icur.b0, ib);
     int phys = __builtin_amdgcn_readlane(bt_lane, ib - icur.b0);
     phys = (unsigned)phys < (unsigned)a.num_blocks ? phys : 0;   // never leave the pool
-    const char* src = reinterpret_cast<const char*>(a.pool) + (size_t)phys * block_bytes + (size_t)icur.kvh * kTileBytes;
+    const char* src = reinterpret_cast<const char*>(a.pool) + (size_t)phys * block_bytes + (size_t)icur.kvh * kTile;
     char* dst = sm.ring[islot];
-    if (base) {
-      dma_tile(src, dma.base, dst);
-      dma_tile(src + v_off, dma.base, dst + kTileBytes);
+    if constexpr (F8) {
+      if (base) {
+        // packed nibbles, as stored, into the upper half of the slot (expanded on use)
+        dma_linear2(src, dst + kTileBytes, lane);
+        dma_linear2(src + v_off, dst + kTileBytes + kTileBytes / 2, lane);
+        ops += 4;
+        ib += 2;
+      } else if (ib + 1 < icur.b1) {
+        // a whole TARGET pair: member m's rows from its own block, in the
+        // layout of a 16-bit packed BASE pair (bytes, member-major)
+        int phys1 = __builtin_amdgcn_readlane(bt_lane, ib + 1 - icur.b0);
+        phys1 = (unsigned)phys1 < (unsigned)a.num_blocks ? phys1 : 0;
+        const char* src1 = reinterpret_cast<const char*>(a.pool) + (size_t)phys1 * block_bytes +
+                           (size_t)icur.kvh * kTile;
+        dma_pair_bytes(src, src1, dma.base, dst);
+        dma_pair_bytes(src + v_off, src1 + v_off, dma.base, dst + kTileBytes);
+        ops += 8;
+        ib += 2;
+      } else {
+        // the sequence's last block, alone: member 0 only
+        dma_member0_bytes(src, dma.base, dst);
+        dma_member0_bytes(src + v_off, dma.base, dst + kTileBytes);
+        ops += 4;
+        ib += 1;
+      }
     } else {
-      dma_tile(src, dma.tgt, dst);
-      dma_tile(src + v_off, dma.tgt, dst + kTileBytes);
+      if (base) {
+        dma_tile(src, dma.base, dst);
+        dma_tile(src + v_off, dma.base, dst + kTileBytes);
+      } else {
+        dma_tile(src, dma.tgt, dst);
+        dma_tile(src + v_off, dma.tgt, dst + kTileBytes);
+      }
+      ops += 8;
+      ib += base ? 2 : 1;
     }
-    ops += 8;
-    ib += base ? 2 : 1;
     islot = islot + 1 == NSLOT ? 0 : islot + 1;
     ++n_issued;
     issue_done = ib >= icur.b1 && !i_has_next;
@@ -571,6 +691,39 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
 #pragma unroll
     for (int u = 0; u < 2; ++u)
       if (!issue_done && n_issued - n_consumed < NSLOT) issue_slot();
+    if constexpr (F8) {
+      // one slot: a BASE pair (nibbles), a TARGET pair, or the lone last block
+      const bool base = block_is_base(cmode, ctag, ccur.b0, cb);
+      const bool lone = !base && cb + 1 >= ccur.b1;
+      c_ops += (base || lone) ? 4 : 8;
+      wait_vm4(ops - c_ops);
+      char* sb = sm.ring[cslot];
+      if (base) expand_nibbles_in_slot(sb, lane);
+      u32x4 k[2][4], v[2][4];
+      f32x4 sc[2];
+#pragma unroll
+      for (int m = 0; m < 2; ++m) {
+        const char* mb = sb + m * (kTileBytes / 2);
+        const u32x4 k0 = *reinterpret_cast<const u32x4*>(mb + rk_b[0]);
+        const u32x4 k1 = *reinterpret_cast<const u32x4*>(mb + rk_b[1]);
+        k[m][0].xy = k0.xy;
+        k[m][1].xy = k0.zw;
+        k[m][2].xy = k1.xy;
+        k[m][3].xy = k1.zw;
+#pragma unroll
+        for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mb + rv_b[i]);
+        sc[m] = qk_scores<T, true>(k[m], qop);
+      }
+      const bool tail = cb * kPage + 2 * kPage > ccur.len;
+      zero_tail_v<2>(v, cb * kPage, ccur.len, g);
+      u32x2 vop[2][8];
+      v_operands<true, 2>(v, vop);
+      if constexpr (kStack) softmax_pv_stacked<T, 2, G>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g, n);
+      else softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
+      cb += lone ? 1 : 2;
+      ++n_consumed;
+      cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
+    } else {
     c_ops += 8;
     wait_vm<NSLOT - 1>(ops - c_ops);
     const char* sb = sm.ring[cslot];
@@ -643,6 +796,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       ++n_consumed;
       cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
     }
+    }   // 16-bit TARGET
     if (cb < ccur.b1) continue;
     // window finished
     if (ccur.piece_end) finalize_piece();
@@ -692,9 +846,9 @@ int resident_groups(K kernel) {
   return cus * per_cu;
 }
 
-template <typename T, int G, int NSLOT>
+template <typename T, int G, int NSLOT, bool F8>
 hipError_t launch_slots(const DecodeArgs& args, bool elastic, hipStream_t st) {
-  auto kernel = elastic ? decode_kernel<T, G, true, NSLOT> : decode_kernel<T, G, false, NSLOT>;
+  auto kernel = elastic ? decode_kernel<T, G, true, NSLOT, F8> : decode_kernel<T, G, false, NSLOT, F8>;
   DecodeArgs a = args;
   const int resident = resident_groups(kernel);
   if (resident <= 0) return hipErrorInvalidDeviceFunction;
@@ -704,23 +858,23 @@ hipError_t launch_slots(const DecodeArgs& args, bool elastic, hipStream_t st) {
   return hipGetLastError();
 }
 
-template <typename T, int G>
+template <typename T, int G, bool F8>
 hipError_t launch_typed(const DecodeArgs& a, bool elastic, hipStream_t st) {
   switch (a.slots) {
-    case 2: return launch_slots<T, G, 2>(a, elastic, st);
-    case 4: return launch_slots<T, G, 4>(a, elastic, st);
-    default: return launch_slots<T, G, 3>(a, elastic, st);
+    case 2: return launch_slots<T, G, 2, F8>(a, elastic, st);
+    case 4: return launch_slots<T, G, 4, F8>(a, elastic, st);
+    default: return launch_slots<T, G, 3, F8>(a, elastic, st);
   }
 }
 
-template <typename T>
+template <typename T, bool F8>
 hipError_t launch_group(const DecodeArgs& a, int group, bool elastic, hipStream_t st) {
   switch (group) {
-    case 1: return launch_typed<T, 1>(a, elastic, st);
-    case 2: return launch_typed<T, 2>(a, elastic, st);
-    case 4: return launch_typed<T, 4>(a, elastic, st);
-    case 8: return launch_typed<T, 8>(a, elastic, st);
-    case 16: return launch_typed<T, 16>(a, elastic, st);
+    case 1: return launch_typed<T, 1, F8>(a, elastic, st);
+    case 2: return launch_typed<T, 2, F8>(a, elastic, st);
+    case 4: return launch_typed<T, 4, F8>(a, elastic, st);
+    case 8: return launch_typed<T, 8, F8>(a, elastic, st);
+    case 16: return launch_typed<T, 16, F8>(a, elastic, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -734,7 +888,12 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 
 hipError_t launch_decode(const DecodeArgs& a, int dtype, int group, bool elastic, hipStream_t st) {
   if (a.batch == 0) return hipSuccess;
-  return dtype == 0 ? launch_group<Bf16>(a, group, elastic, st) : launch_group<Fp16>(a, group, elastic, st);
+  switch (dtype) {
+    case 0: return launch_group<Bf16, false>(a, group, elastic, st);
+    case 1: return launch_group<Fp16, false>(a, group, elastic, st);
+    case 3: return launch_group<Fp16, true>(a, group, elastic, st);   // E5M2 bytes, FP16 queries
+    default: return hipErrorInvalidValue;
+  }
 }
 
 hipError_t launch_zero_u32(uint32_t* p, size_t n, hipStream_t st) {

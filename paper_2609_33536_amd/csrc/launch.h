@@ -46,6 +46,7 @@ struct TransitionArgs {
   int32_t n, num_kv_heads, max_blocks;
   int32_t num_layers;        // 1 for a single-layer call
   int32_t staged;            // refine: pair i's refinement bytes are in block new_blocks[i] (lo unused)
+  int32_t elem8;             // 8-bit TARGET / 4-bit BASE pool (else 16-bit / 8-bit)
 };
 
 hipError_t launch_demote(const TransitionArgs& a, hipStream_t st);
@@ -57,6 +58,7 @@ struct AppendArgs {
   const uint16_t* k;
   const uint16_t* v;
   int32_t n, num_kv_heads;
+  int32_t elem8;             // 1-byte elements
 };
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t st);

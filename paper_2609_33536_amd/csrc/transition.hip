@@ -131,6 +131,96 @@ __global__ __launch_bounds__(64) void refine_kernel(TransitionArgs a) {
   }
 }
 
+// ---- 8-bit TARGET / 4-bit BASE ---------------------------------------------
+// A (plane, head) tile is 2 KiB (16 rows of 128 bytes); a packed tile holds
+// [member 0 | member 1] nibble rows of 64 bytes, element e of a row in byte
+// e / 2 (low nibble when e is even).  Lane L owns the 32 bytes [32L, 32L+32)
+// of each member's TARGET tile, i.e. the 16 packed bytes [16L, 16L+16) of
+// that member's half.
+constexpr int kTile8 = kPage * kHeadDim;   // 2 KiB
+
+// Four bytes (one nibble of each, in the low nibble) -> bytes 0 and 2 of the
+// result hold nibbles (0 | 1 << 4) and (2 | 3 << 4).
+__device__ __forceinline__ uint32_t pair_nibbles(uint32_t t) { return t | (t >> 4); }
+
+// 32 TARGET bytes -> 16 bytes of their high (hi = true) or low nibbles.
+__device__ __forceinline__ u32x4 pack_nibbles(const u32x4 (&x)[2], bool hi) {
+  uint32_t w[8];
+#pragma unroll
+  for (int q = 0; q < 8; ++q) {
+    const uint32_t in = x[q >> 2][q & 3];
+    w[q] = pair_nibbles(hi ? (in >> 4) & 0x0F0F0F0Fu : in & 0x0F0F0F0Fu);
+  }
+  return u32x4{perm(w[1], w[0], 0x06040200u), perm(w[3], w[2], 0x06040200u), perm(w[5], w[4], 0x06040200u),
+               perm(w[7], w[6], 0x06040200u)};
+}
+
+// 4 bytes of high nibbles + 4 bytes of low nibbles -> 8 TARGET bytes.
+__device__ __forceinline__ u32x2 join_nibbles(uint32_t h, uint32_t l) {
+  const uint32_t even = ((h & 0x0F0F0F0Fu) << 4) | (l & 0x0F0F0F0Fu);
+  const uint32_t odd = (h & 0xF0F0F0F0u) | ((l >> 4) & 0x0F0F0F0Fu);
+  return u32x2{perm(odd, even, 0x05010400u), perm(odd, even, 0x07030602u)};
+}
+
+__device__ __forceinline__ uint8_t* layer_pool8(const TransitionArgs& a) {
+  return reinterpret_cast<uint8_t*>(layer_pool(a));
+}
+
+__global__ __launch_bounds__(64) void demote8_kernel(TransitionArgs a) {
+  const int tile = blockIdx.x;
+  const int i = blockIdx.y;
+  const int lane = threadIdx.x;
+  const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  const int32_t* row = a.bt + (size_t)s * a.max_blocks;
+  const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTile8;
+  uint8_t* pool = layer_pool8(a);
+  uint8_t* t0 = pool + (size_t)row[2 * j] * block_bytes + (size_t)tile * kTile8;
+  const uint8_t* t1 = pool + (size_t)row[2 * j + 1] * block_bytes + (size_t)tile * kTile8;
+  u32x4 x0[2], x1[2];
+#pragma unroll
+  for (int r = 0; r < 2; ++r) {
+    x0[r] = *reinterpret_cast<const u32x4*>(t0 + 32 * lane + 16 * r);
+    x1[r] = *reinterpret_cast<const u32x4*>(t1 + 32 * lane + 16 * r);
+  }
+  wait_all_loads();
+  *reinterpret_cast<u32x4*>(t0 + 16 * lane) = pack_nibbles(x0, true);
+  *reinterpret_cast<u32x4*>(t0 + kTile8 / 2 + 16 * lane) = pack_nibbles(x1, true);
+  if (a.lo) {
+    uint8_t* lo = a.lo + ((size_t)i * a.num_layers + blockIdx.z) * block_bytes + (size_t)tile * kTile8;
+    *reinterpret_cast<u32x4*>(lo + 16 * lane) = pack_nibbles(x0, false);
+    *reinterpret_cast<u32x4*>(lo + kTile8 / 2 + 16 * lane) = pack_nibbles(x1, false);
+  }
+}
+
+__global__ __launch_bounds__(64) void refine8_kernel(TransitionArgs a) {
+  const int tile = blockIdx.x;
+  const int i = blockIdx.y;
+  const int lane = threadIdx.x;
+  const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTile8;
+  uint8_t* pool = layer_pool8(a);
+  uint8_t* tp = pool + (size_t)a.bt[(size_t)s * a.max_blocks + 2 * j] * block_bytes + (size_t)tile * kTile8;
+  uint8_t* tq = pool + (size_t)a.new_blocks[i] * block_bytes + (size_t)tile * kTile8;
+  const uint8_t* lo = a.staged ? tq : a.lo + ((size_t)i * a.num_layers + blockIdx.z) * block_bytes + (size_t)tile * kTile8;
+  u32x4 h[2], l[2];
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    h[m] = *reinterpret_cast<const u32x4*>(tp + m * (kTile8 / 2) + 16 * lane);
+    l[m] = *reinterpret_cast<const u32x4*>(lo + m * (kTile8 / 2) + 16 * lane);
+  }
+  wait_all_loads();
+#pragma unroll
+  for (int m = 0; m < 2; ++m) {
+    uint8_t* dst = m ? tq : tp;
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const u32x2 a0 = join_nibbles(h[m][2 * r], l[m][2 * r]);
+      const u32x2 a1 = join_nibbles(h[m][2 * r + 1], l[m][2 * r + 1]);
+      *reinterpret_cast<u32x4*>(dst + 32 * lane + 16 * r) = u32x4{a0.x, a0.y, a1.x, a1.y};
+    }
+  }
+}
+
 __global__ __launch_bounds__(256) void refine_commit_kernel(TransitionArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
@@ -141,7 +231,27 @@ __global__ __launch_bounds__(256) void refine_commit_kernel(TransitionArgs a) {
   tg[2 * j + 1] = 0;
 }
 
-// One wave per new token: 2*Hkv rows of 256 B, 16 lanes per row.
+// One wave per new token: 2*Hkv rows of 256 B (16 lanes per row), or of
+// 128 B for 1-byte elements (8 lanes per row).
+__global__ __launch_bounds__(64) void append8_kernel(AppendArgs a) {
+  const int i = blockIdx.x;
+  const int lane = threadIdx.x;
+  const int slot = a.slots[i];
+  const int blk = slot / kPage, off = slot % kPage;
+  const int hkv = a.num_kv_heads;
+  const size_t block_bytes = (size_t)2 * hkv * kTile8;
+  const int c = lane & 7;
+  const uint8_t* k = reinterpret_cast<const uint8_t*>(a.k);
+  const uint8_t* v = reinterpret_cast<const uint8_t*>(a.v);
+  uint8_t* pool = reinterpret_cast<uint8_t*>(a.pool);
+  for (int r = lane >> 3; r < 2 * hkv; r += 8) {
+    const int plane = r / hkv, h = r % hkv;
+    const uint8_t* src = (plane ? v : k) + ((size_t)i * hkv + h) * kHeadDim + 16 * c;
+    uint8_t* dst = pool + (size_t)blk * block_bytes + (size_t)r * kTile8 + off * kHeadDim + 16 * c;
+    *reinterpret_cast<u32x4*>(dst) = *reinterpret_cast<const u32x4*>(src);
+  }
+}
+
 __global__ __launch_bounds__(64) void append_kernel(AppendArgs a) {
   const int i = blockIdx.x;
   const int lane = threadIdx.x;
@@ -162,7 +272,8 @@ __global__ __launch_bounds__(64) void append_kernel(AppendArgs a) {
 
 hipError_t launch_demote(const TransitionArgs& a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  hipLaunchKernelGGL(demote_kernel, dim3(2 * a.num_kv_heads, a.n, a.num_layers), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(a.elem8 ? demote8_kernel : demote_kernel, dim3(2 * a.num_kv_heads, a.n, a.num_layers),
+                     dim3(64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(demote_commit_kernel, dim3((a.n + 255) / 256), dim3(256), 0, st, a);
@@ -171,7 +282,8 @@ hipError_t launch_demote(const TransitionArgs& a, hipStream_t st) {
 
 hipError_t launch_refine(const TransitionArgs& a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  hipLaunchKernelGGL(refine_kernel, dim3(2 * a.num_kv_heads, a.n, a.num_layers), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(a.elem8 ? refine8_kernel : refine_kernel, dim3(2 * a.num_kv_heads, a.n, a.num_layers),
+                     dim3(64), 0, st, a);
   hipError_t e = hipGetLastError();
   if (e != hipSuccess) return e;
   hipLaunchKernelGGL(refine_commit_kernel, dim3((a.n + 255) / 256), dim3(256), 0, st, a);
@@ -180,7 +292,7 @@ hipError_t launch_refine(const TransitionArgs& a, hipStream_t st) {
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;
-  hipLaunchKernelGGL(append_kernel, dim3(a.n), dim3(64), 0, st, a);
+  hipLaunchKernelGGL(a.elem8 ? append8_kernel : append_kernel, dim3(a.n), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 

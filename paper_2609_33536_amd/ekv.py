@@ -16,7 +16,7 @@ _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libekv.so")
 
 OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
-DTYPE_BF16, DTYPE_FP16, DTYPE_FP32 = 0, 1, 2
+DTYPE_BF16, DTYPE_FP16, DTYPE_FP32, DTYPE_E5M2 = 0, 1, 2, 3
 MODE_NATIVE, MODE_STRUCTURED, MODE_GENERAL = 0, 1, 2
 HEAD_DIM, PAGE = 128, 16
 
@@ -129,9 +129,10 @@ def dtype_code(torch_dtype):
 
 
 def make_pool(kv, num_kv_heads, dtype_name="bf16"):
-    """Describe a device pool tensor of 16-bit words [NB][2][Hkv][16][128]."""
+    """Describe a device pool tensor [NB][2][Hkv][16][128] of 16-bit words
+    (bf16, fp16) or bytes (e5m2)."""
     nb = kv.numel() // (2 * num_kv_heads * PAGE * HEAD_DIM)
-    code = {"bf16": DTYPE_BF16, "fp16": DTYPE_FP16}[dtype_name]
+    code = {"bf16": DTYPE_BF16, "fp16": DTYPE_FP16, "e5m2": DTYPE_E5M2}[dtype_name]
     return Pool(_ptr(kv), nb, num_kv_heads, PAGE, HEAD_DIM, code)
 
 

@@ -99,8 +99,9 @@ class PagedKV:
     def __init__(self, pool_words, block_table, seq_lens, free_ids, num_kv_heads, dtype="bf16",
                  device="cuda"):
         import torch
+        elem = np.uint8 if dtype == "e5m2" else np.int16
         kv = pool_words if isinstance(pool_words, torch.Tensor) else torch.from_numpy(
-            np.ascontiguousarray(pool_words).view(np.int16))
+            np.ascontiguousarray(pool_words).view(elem))
         self.kv = kv.to(device).contiguous()
         self.num_kv_heads = num_kv_heads
         self.dtype = dtype
@@ -116,7 +117,8 @@ class PagedKV:
 
     @property
     def block_bytes(self):
-        return 2 * self.num_kv_heads * ekv.PAGE * ekv.HEAD_DIM * 2
+        elem = 1 if self.dtype == "e5m2" else 2
+        return 2 * self.num_kv_heads * ekv.PAGE * ekv.HEAD_DIM * elem
 
     def _upload(self, arr):
         """Host array -> device through a fresh pinned buffer (stream-ordered,

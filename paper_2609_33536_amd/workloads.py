@@ -1,6 +1,7 @@
 """Seeded synthetic inputs for the mixed-fidelity paged-attention path.
 
-This module only makes inputs: random 16-bit K/V/Q words, block tables that
+This module only makes inputs: random 16-bit K/V/Q words (or FP8 E5M2 K/V
+bytes, rounded by torch), block tables that
 scatter each sequence over a shuffled physical pool, sequence lengths, and
 the lists of pairs a caller chooses to demote.  It performs none of the
 method's arithmetic (no encoding, no attention, no transitions), so both
@@ -36,12 +37,27 @@ def f32_to_fp16_words(x):
     return np.asarray(x, dtype=np.float32).astype(np.float16).view(np.uint16)
 
 
+def f32_to_e5m2_bytes(x):
+    """Round float32 to FP8 E5M2 bytes with torch's own conversion."""
+    import torch
+    t = torch.from_numpy(np.ascontiguousarray(x, dtype=np.float32)).to(torch.float8_e5m2)
+    return t.view(torch.uint8).numpy().copy()
+
+
 def to_words(x, dtype):
+    """16-bit words (bf16, fp16) or bytes (e5m2) of float32 values."""
     if dtype == "bf16":
         return f32_to_bf16_words(x)
     if dtype == "fp16":
         return f32_to_fp16_words(x)
+    if dtype == "e5m2":
+        return f32_to_e5m2_bytes(x)
     raise ValueError(dtype)
+
+
+def query_dtype(dtype):
+    """Queries of an 8-bit (e5m2) pool are fp16; otherwise the pool dtype."""
+    return "fp16" if dtype == "e5m2" else dtype
 
 
 def complete_pairs(seq_len, page=PAGE):
@@ -108,7 +124,7 @@ def make_decode_case(seq_lens, num_q_heads, num_kv_heads, *, head_dim=HEAD_DIM,
                 vals[:, plane, c // head_dim, :, c % head_dim] *= 10.0
     pool = to_words(vals, dtype)
     if garbage_tail:
-        junk = lambda shape: rng.integers(0, 1 << 16, size=shape, dtype=np.uint16)
+        junk = lambda shape: rng.integers(0, np.iinfo(pool.dtype).max + 1, size=shape, dtype=pool.dtype)
         for s in range(bsz):
             rem = int(seq_lens[s]) % page
             if rem:
@@ -116,7 +132,7 @@ def make_decode_case(seq_lens, num_q_heads, num_kv_heads, *, head_dim=HEAD_DIM,
                 pool[last, :, :, rem:, :] = junk(pool[last, :, :, rem:, :].shape)
         if len(free):
             pool[free] = junk(pool[free].shape)
-    q = to_words(rng.standard_normal((bsz, num_q_heads, head_dim), dtype=np.float32), dtype)
+    q = to_words(rng.standard_normal((bsz, num_q_heads, head_dim), dtype=np.float32), query_dtype(dtype))
     pairs = choose_pairs(rng, seq_lens, base_fraction, placement, page)
     return {
         "pool": pool, "block_table": bt, "tags": np.zeros((bsz, max_blocks), dtype=np.uint8),
