@@ -392,6 +392,8 @@ def main():
             "mean over the f=0.25/0.5/1 launches of PMC FETCH_SIZE and WRITE_SIZE, each scaled by "
             "what it reads for a 1 GiB device copy")
     result["controller"] = controller_cost(ekv, tpool.mirror)
+    print("[bench] 8-bit TARGET / 4-bit BASE decode", file=sys.stderr, flush=True)
+    result["decode_8bit"] = decode_8bit(torch, ekv, kvpool, workloads, stream, seq_lens, scale)
     print("[bench] asynchronous promotion", file=sys.stderr, flush=True)
     result["async_promotion"] = async_promotion_cost(torch, kvpool, tpool, cand, stream)
     print("[bench] multi-layer transitions", file=sys.stderr, flush=True)
@@ -401,6 +403,54 @@ def main():
         result["cpu_baseline"], result["parity"] = cpu_baseline(dec, outs, pf)
     print(json.dumps(result), flush=True)
     return 0
+
+
+def decode_8bit(torch, ekv, kvpool, workloads, stream, seq_lens, scale, reps=20):
+    """The same 8B decode layer over an 8-bit TARGET (FP8 E5M2) / 4-bit BASE
+    pool at BASE fraction 0, 0.5 and 1 (random pairs): median event time of
+    the decode launch; algorithmic bytes count 1 B per TARGET and 0.5 B per
+    BASE element of every visible token, fp16 Q and O, and the metadata."""
+    base = workloads.make_decode_case_torch(seq_lens, HQ, HKV, seed=SEED + 5, outlier_channels=10,
+                                            spare_blocks=64, dtype="e5m2")
+    q = base["q"]
+    out = torch.empty((B, HQ, D), dtype=torch.float16, device="cuda")
+    res = []
+    for k, f in enumerate((0.0, 0.5, 1.0)):
+        kv = kvpool.PagedKV(base["pool"].clone(), base["block_table"], seq_lens, base["free"], HKV, "e5m2")
+        pairs = workloads.choose_pairs(np.random.default_rng(SEED * 2000 + k), seq_lens, f, "random")
+        if len(pairs):
+            kv.demote(pairs, emit_lo=False)
+            kv.commit()
+        mode = kv.relower()
+        batch = kv.batch(HQ)
+        ws = torch.zeros(ekv.decode_workspace_bytes(kv.pool, batch), dtype=torch.uint8, device="cuda")
+        times = []
+        for r in range(reps + 3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            ekv.attn_decode(kv.pool, batch, q, out, scale, ws)
+            e1.record(stream)
+            e1.synchronize()
+            if r >= 3:
+                times.append(e0.elapsed_time(e1))
+        ms = float(np.median(times))
+        tags = kv.mirror.tags
+        nbytes = 0
+        for s, length in enumerate(seq_lens):
+            nblk = -(-int(length) // PAGE)
+            per_tok = np.where(tags[s, :nblk] == 1, 0.5, 1.0) * (2 * HKV * D)
+            full = int(length) // PAGE
+            nbytes += int((per_tok[:full] * PAGE).sum()) + (
+                int(per_tok[full] * (int(length) - full * PAGE)) if nblk > full else 0)
+        blocks = sum(-(-int(l) // PAGE) for l in seq_lens)
+        nbytes += 2 * B * HQ * D * 2 + blocks * 4 + (blocks if mode == 2 else 0) + B * 4
+        res.append({"base_fraction": f, "mode": ["native", "structured", "general"][mode], "ms": round(ms, 5),
+                    "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1), "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+                    "tokens_per_s": round(B / (ms * 1e-3), 1), "bytes": nbytes})
+        del kv, ws
+    del base
+    torch.cuda.empty_cache()
+    return res
 
 
 def async_promotion_cost(torch, kvpool, kv, cand, stream, pairs=256):

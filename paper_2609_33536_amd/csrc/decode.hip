@@ -228,19 +228,21 @@ __device__ __forceinline__ void wait_vm4(int n) {
 }
 
 // ---- 8-bit TARGET / 4-bit BASE slots -------------------------------------
-// A slot holds the K and V tiles of 32 tokens laid out exactly as a 16-bit
-// packed BASE pair ([member 0 | member 1] rows of 128 bytes, swizzled as in
-// dma_offsets), so the byte path reads both formats alike.  A TARGET pair
-// arrives so directly, member m from its own block; a BASE pair arrives as
-// its packed nibbles (2 KiB per tile) in the upper half of the slot and is
-// expanded in place before use.
+// The ring is cut into 4 KiB units.  A TARGET pair takes two: its K and its
+// V tiles, each laid out exactly as one plane of a 16-bit packed BASE pair
+// ([member 0 | member 1] rows of 128 bytes, swizzled as in dma_offsets) and
+// read by the same byte path, member m fetched from its own block.  A BASE
+// pair takes one: K nibbles at +0 and V nibbles at +2 KiB, expanded to bytes
+// in registers.  So the bytes in flight do not shrink when pairs are BASE.
 
-// Linear copy of a 2 KiB tile: lane L's 16 bytes of load r land at dst + 1024 r + 16 L.
-__device__ __forceinline__ void dma_linear2(const char* src, char* dst, int lane) {
+// A BASE pair's packed nibble tile (2 KiB: [member][16 rows][64 bytes]),
+// 16-byte chunk c of row t stored at chunk position c ^ ((t >> 2) & 3) so
+// that the operand reads below spread over the banks.  nib[r]: the source
+// offset lane L fetches with load r (LDS destination 1024 r + 16 L).
+__device__ __forceinline__ void dma_nibbles(const char* tile, const uint32_t (&nib)[2], char* dst) {
 #pragma unroll
   for (int r = 0; r < 2; ++r)
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + 1024 * r + 16 * lane),
-                                     (lds_ptr)(dst + 1024 * r), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile + nib[r]), (lds_ptr)(dst + 1024 * r), 16, 0, 0);
 }
 
 // A TARGET pair's tile: loads 0, 1 (member 0) from tile0, 2, 3 (member 1) from tile1.
@@ -261,37 +263,11 @@ __device__ __forceinline__ void dma_member0_bytes(const char* tile0, const uint3
                                      0);
 }
 
-// 8 bytes of nibbles (element 2k low, 2k+1 high in byte k) -> 16 element
+// 4 bytes of nibbles (element 2k low, 2k+1 high in byte k) -> 8 element
 // bytes, each nibble in the high half with a zero low half.
-__device__ __forceinline__ u32x4 expand_nibbles(u32x2 w) {
-  u32x4 r;
-#pragma unroll
-  for (int h = 0; h < 2; ++h) {
-    const uint32_t even = (w[h] << 4) & 0xF0F0F0F0u, odd = w[h] & 0xF0F0F0F0u;
-    r[2 * h] = perm(odd, even, 0x05010400u);
-    r[2 * h + 1] = perm(odd, even, 0x07030602u);
-  }
-  return r;
-}
-
-// Expand a BASE pair's nibbles (K at +4 KiB, V at +6 KiB) into the byte
-// layout over the whole slot.  Lane L takes member L / 32, row (L / 2) % 16,
-// half L % 2 of both planes; the wave reads all it needs before it writes.
-__device__ __forceinline__ void expand_nibbles_in_slot(char* sb, int lane) {
-  const int m = lane >> 5, t = (lane >> 1) & 15, hh = lane & 1;
-  const char* nk = sb + kTileBytes + m * (kTileBytes / 4) + t * (kHeadDim / 2) + 32 * hh;
-  const u32x4 k0 = *reinterpret_cast<const u32x4*>(nk), k1 = *reinterpret_cast<const u32x4*>(nk + 16);
-  const u32x4 v0 = *reinterpret_cast<const u32x4*>(nk + kTileBytes / 2);
-  const u32x4 v1 = *reinterpret_cast<const u32x4*>(nk + kTileBytes / 2 + 16);
-  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
-  const u32x2 kw[4] = {k0.xy, k0.zw, k1.xy, k1.zw}, vw[4] = {v0.xy, v0.zw, v1.xy, v1.zw};
-  char* row = sb + m * (kTileBytes / 2) + t * kHeadDim;
-#pragma unroll
-  for (int c = 0; c < 4; ++c) {
-    const int pos = 16 * ((4 * hh + c) ^ tau(t));
-    *reinterpret_cast<u32x4*>(row + pos) = expand_nibbles(kw[c]);
-    *reinterpret_cast<u32x4*>(row + kTileBytes + pos) = expand_nibbles(vw[c]);
-  }
+__device__ __forceinline__ u32x2 expand4(uint32_t w) {
+  const uint32_t even = (w << 4) & 0xF0F0F0F0u, odd = w & 0xF0F0F0F0u;
+  return u32x2{perm(odd, even, 0x05010400u), perm(odd, even, 0x07030602u)};
 }
 
 __device__ __forceinline__ int wave_sum_int(int x) {
@@ -523,6 +499,19 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
 #pragma unroll
   for (int h = 0; h < 2; ++h) rk_b[h] = n * kHeadDim + 16 * ((2 * g + h) ^ tau(n));
   const DmaOffsets dma = dma_offsets(lane);
+  // 8-bit format: nibble-tile load offsets and nibble-operand read offsets
+  constexpr int kUnit = kTileBytes;   // 4 KiB
+  uint32_t nib[2], rv4[4], rk4 = 0;
+  if constexpr (F8) {
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      const int p = 64 * r + lane, t = (p >> 2) & 15;
+      nib[r] = (p >> 6) * (kTileBytes / 4) + t * (kHeadDim / 2) + 16 * ((p & 3) ^ ((t >> 2) & 3));
+    }
+    rk4 = n * (kHeadDim / 2) + 16 * (g ^ ((n >> 2) & 3));
+#pragma unroll
+    for (int i = 0; i < 4; ++i) rv4[i] = (4 * g + i) * (kHeadDim / 2) + 16 * ((n >> 2) ^ g) + 4 * (n & 3);
+  }
 
   // a (plane, head) tile: 4 KiB of 16-bit words, or 2 KiB of bytes (F8)
   constexpr int kTile = F8 ? kTileBytes / 2 : kTileBytes;
@@ -575,12 +564,16 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     const char* src = reinterpret_cast<const char*>(a.pool) + (size_t)phys * block_bytes + (size_t)icur.kvh * kTile;
     char* dst = sm.ring[islot];
     if constexpr (F8) {
+      char* ring0 = &sm.ring[0][0];
+      char* dk = ring0 + kUnit * islot;
+      char* dv = ring0 + kUnit * (islot + 1 == 2 * NSLOT ? 0 : islot + 1);
+      int units = 2;
       if (base) {
-        // packed nibbles, as stored, into the upper half of the slot (expanded on use)
-        dma_linear2(src, dst + kTileBytes, lane);
-        dma_linear2(src + v_off, dst + kTileBytes + kTileBytes / 2, lane);
+        dma_nibbles(src, nib, dk);
+        dma_nibbles(src + v_off, nib, dk + kTileBytes / 2);
         ops += 4;
         ib += 2;
+        units = 1;
       } else if (ib + 1 < icur.b1) {
         // a whole TARGET pair: member m's rows from its own block, in the
         // layout of a 16-bit packed BASE pair (bytes, member-major)
@@ -588,17 +581,20 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
         phys1 = (unsigned)phys1 < (unsigned)a.num_blocks ? phys1 : 0;
         const char* src1 = reinterpret_cast<const char*>(a.pool) + (size_t)phys1 * block_bytes +
                            (size_t)icur.kvh * kTile;
-        dma_pair_bytes(src, src1, dma.base, dst);
-        dma_pair_bytes(src + v_off, src1 + v_off, dma.base, dst + kTileBytes);
+        dma_pair_bytes(src, src1, dma.base, dk);
+        dma_pair_bytes(src + v_off, src1 + v_off, dma.base, dv);
         ops += 8;
         ib += 2;
       } else {
         // the sequence's last block, alone: member 0 only
-        dma_member0_bytes(src, dma.base, dst);
-        dma_member0_bytes(src + v_off, dma.base, dst + kTileBytes);
+        dma_member0_bytes(src, dma.base, dk);
+        dma_member0_bytes(src + v_off, dma.base, dv);
         ops += 4;
         ib += 1;
       }
+      islot += units;
+      if (islot >= 2 * NSLOT) islot -= 2 * NSLOT;
+      n_issued += units;
     } else {
       if (base) {
         dma_tile(src, dma.base, dst);
@@ -609,9 +605,9 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       }
       ops += 8;
       ib += base ? 2 : 1;
+      islot = islot + 1 == NSLOT ? 0 : islot + 1;
+      ++n_issued;
     }
-    islot = islot + 1 == NSLOT ? 0 : islot + 1;
-    ++n_issued;
     issue_done = ib >= icur.b1 && !i_has_next;
   };
 
@@ -682,36 +678,51 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     }
   };
 
+  // ring capacity: NSLOT slots, or (8-bit) 2 NSLOT units of which a slot takes up to two
+  auto ring_has_room = [&]() {
+    return F8 ? n_issued - n_consumed + 2 <= 2 * NSLOT : n_issued - n_consumed < NSLOT;
+  };
 #pragma unroll
-  for (int k = 0; k < NSLOT - 1; ++k)
-    if (!issue_done) issue_slot();
+  for (int k = 0; k < (F8 ? 2 * NSLOT - 2 : NSLOT - 1); ++k)
+    if (!issue_done && ring_has_room()) issue_slot();
 
   while (true) {
-    // keep the ring full: NSLOT slots issued and not yet consumed
+    // keep the ring full
 #pragma unroll
     for (int u = 0; u < 2; ++u)
-      if (!issue_done && n_issued - n_consumed < NSLOT) issue_slot();
+      if (!issue_done && ring_has_room()) issue_slot();
     if constexpr (F8) {
       // one slot: a BASE pair (nibbles), a TARGET pair, or the lone last block
       const bool base = block_is_base(cmode, ctag, ccur.b0, cb);
       const bool lone = !base && cb + 1 >= ccur.b1;
       c_ops += (base || lone) ? 4 : 8;
       wait_vm4(ops - c_ops);
-      char* sb = sm.ring[cslot];
-      if (base) expand_nibbles_in_slot(sb, lane);
+      const char* ring0 = &sm.ring[0][0];
+      const char* kb = ring0 + kUnit * cslot;
+      const char* vb = ring0 + kUnit * (cslot + 1 == 2 * NSLOT ? 0 : cslot + 1);
       u32x4 k[2][4], v[2][4];
       f32x4 sc[2];
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
-        const char* mb = sb + m * (kTileBytes / 2);
-        const u32x4 k0 = *reinterpret_cast<const u32x4*>(mb + rk_b[0]);
-        const u32x4 k1 = *reinterpret_cast<const u32x4*>(mb + rk_b[1]);
-        k[m][0].xy = k0.xy;
-        k[m][1].xy = k0.zw;
-        k[m][2].xy = k1.xy;
-        k[m][3].xy = k1.zw;
+        if (base) {
+          const char* mb = kb + m * (kTileBytes / 4);
+          const u32x4 kn = *reinterpret_cast<const u32x4*>(mb + rk4);
 #pragma unroll
-        for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mb + rv_b[i]);
+          for (int q = 0; q < 4; ++q) k[m][q].xy = expand4(kn[q]);
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[m][i].xy = expand4(*reinterpret_cast<const uint32_t*>(mb + kTileBytes / 2 + rv4[i]));
+        } else {
+          const char* mb = kb + m * (kTileBytes / 2);
+          const u32x4 k0 = *reinterpret_cast<const u32x4*>(mb + rk_b[0]);
+          const u32x4 k1 = *reinterpret_cast<const u32x4*>(mb + rk_b[1]);
+          k[m][0].xy = k0.xy;
+          k[m][1].xy = k0.zw;
+          k[m][2].xy = k1.xy;
+          k[m][3].xy = k1.zw;
+          const char* mv = vb + m * (kTileBytes / 2) - kTileBytes;   // rv_b counts from the K tile
+#pragma unroll
+          for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mv + rv_b[i]);
+        }
         sc[m] = qk_scores<T, true>(k[m], qop);
       }
       const bool tail = cb * kPage + 2 * kPage > ccur.len;
@@ -721,8 +732,10 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       if constexpr (kStack) softmax_pv_stacked<T, 2, G>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g, n);
       else softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
       cb += lone ? 1 : 2;
-      ++n_consumed;
-      cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
+      const int units = base ? 1 : 2;
+      n_consumed += units;
+      cslot += units;
+      if (cslot >= 2 * NSLOT) cslot -= 2 * NSLOT;
     } else {
     c_ops += 8;
     wait_vm<NSLOT - 1>(ops - c_ops);

@@ -198,8 +198,8 @@ def make_decode_case_torch(seq_lens, num_q_heads, num_kv_heads, *, seed, outlier
     """Large-workload variant of :func:`make_decode_case` that draws the
     values on the GPU with a seeded torch generator.  Block placement and
     lengths come from NumPy as before.  Returns device tensors for the pool
-    (16-bit words as int16 [NB][2][Hkv][16][128]) and the query, NumPy arrays
-    for the rest."""
+    (16-bit words as int16, or e5m2 bytes as uint8, [NB][2][Hkv][16][128])
+    and the query (fp16 for e5m2 pools), NumPy arrays for the rest."""
     import torch
     rng = np.random.default_rng(seed)
     seq_lens = np.asarray(seq_lens, dtype=np.int32)
@@ -216,7 +216,8 @@ def make_decode_case_torch(seq_lens, num_q_heads, num_kv_heads, *, seed, outlier
         bt[s, :nblk[s]] = perm[pos:pos + nblk[s]]
         pos += nblk[s]
     free = np.sort(perm[used:]).astype(np.int32)
-    tdtype = torch.bfloat16 if dtype == "bf16" else torch.float16
+    tdtype = {"bf16": torch.bfloat16, "fp16": torch.float16, "e5m2": torch.float8_e5m2}[dtype]
+    qdtype = torch.float16 if dtype == "e5m2" else tdtype
     gen = torch.Generator(device=device)
     gen.manual_seed(int(seed))
     pool = torch.empty((nb, 2, num_kv_heads, PAGE, HEAD_DIM), dtype=tdtype, device=device)
@@ -233,8 +234,9 @@ def make_decode_case_torch(seq_lens, num_q_heads, num_kv_heads, *, seed, outlier
                         dtype=torch.float32)
         pool[b0:b1] = (x * scale).to(tdtype)
     q = torch.randn((bsz, num_q_heads, HEAD_DIM), generator=gen, device=device,
-                    dtype=torch.float32).to(tdtype)
-    return {"pool": pool.view(torch.int16), "q": q, "block_table": bt, "seq_lens": seq_lens,
+                    dtype=torch.float32).to(qdtype)
+    words = pool.view(torch.uint8) if dtype == "e5m2" else pool.view(torch.int16)
+    return {"pool": words, "q": q, "block_table": bt, "seq_lens": seq_lens,
             "free": free, "dtype": dtype, "num_kv_heads": num_kv_heads}
 
 
