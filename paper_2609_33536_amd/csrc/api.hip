@@ -234,6 +234,9 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
   // LDS ring depth: the deepest ring that still lets 4 workgroups (one per
   // SIMD) share a CU's 160 KiB with their window buffers.
   a.slots = group <= 4 ? 4 : (group == 8 ? 3 : 2);
+  // 8-bit pools holding BASE pairs: per-pair work outweighs the halved bytes,
+  // so twice the waves per SIMD (a shallower ring) pay more than depth
+  if (pool->dtype == EKV_DTYPE_E5M2 && batch->mode != EKV_MODE_NATIVE) a.slots = 2;
   if (const char* env = getenv("EKV_DECODE_SLOTS")) a.slots = std::max(2, std::min(4, atoi(env)));
   a.scale_log2 = log2e_scale(scale);
   return hip_status(ekv::launch_decode(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
