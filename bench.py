@@ -155,7 +155,7 @@ def reduce_pmc(directory):
         per_launch[counter] = [float(np.mean(d[nf + i::nf])) * scale[counter] for i in range(nf)]
     hbm = [f + w for f, w in zip(per_launch["FETCH_SIZE"], per_launch["WRITE_SIZE"])]
     out = {"source_digest": source_digest(),
-           "kernel": "decode_kernel<Bf16, 4, true, 4>",
+           "kernel": "decode_kernel<Bf16, 4, true, 4, false>",
            "base_fractions": dec["base_fractions"],
            "fetch_scale": round(scale["FETCH_SIZE"], 5), "write_scale": round(scale["WRITE_SIZE"], 5),
            "fetch_bytes": [round(v) for v in per_launch["FETCH_SIZE"]],
@@ -383,7 +383,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": (traffic["hbm_bytes_per_launch"] if traffic else None),
-                     "kernel": "decode_kernel<Bf16, 4, true, 4> (ekv_attn_decode, elastic path)",
+                     "kernel": "decode_kernel<Bf16, 4, true, 4, false> (ekv_attn_decode, 16-bit elastic path)",
                      "algorithmic_bytes_per_launch": round(sum(decode_bytes_f[k] for k in ELASTIC) / len(ELASTIC)),
                      "avg_launch_ms": round(sum(el_ms) / len(el_ms), 5)},
     }
