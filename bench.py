@@ -236,8 +236,8 @@ def build_prefill(torch, kvpool, workloads):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported in this build "
-              "(sharding across GPUs is described in DESIGN.md but not built)", file=sys.stderr)
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(sharding across GPUs is not built)", file=sys.stderr)
         return 2
     if args.reduce_pmc:
         reduce_pmc(args.reduce_pmc)
