@@ -253,6 +253,28 @@ ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pai
                              hipStream_t stream);
 
 /*
+ * Staging copy of asynchronous promotion (App. B.2: the restore from the CPU
+ * backing runs while the BASE mapping stays executable).  For i < n, copies
+ * one block's bytes (2 * num_kv_heads * page_size * head_dim elements of the
+ * pool's dtype) from h_src[i] into pool block h_new_blocks[i], the block
+ * reserved for pair i, ready for ekv_refine_staged.
+ *   h_src         host array [n] of addresses; each range must be memory the
+ *                 current device can read: its own device memory, or pinned
+ *                 host memory mapped for it (hipHostMalloc; read over the
+ *                 host link by the copy kernel, without a DMA copy per block).
+ *                 Both ends of every range are looked up before anything is
+ *                 enqueued; an address the runtime does not know (pageable
+ *                 host memory) is EKV_ERR_INVALID.
+ *   h_new_blocks  host int32 [n]: distinct blocks in [0, num_blocks).
+ * The sources are caller-owned and must stay valid and unchanged until the
+ * stream has passed this call; the destination blocks must not be read or
+ * written by other work meanwhile.  No table or tag is touched.
+ * Errors: EKV_ERR_INVALID, EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.
+ */
+ekv_status ekv_stage_blocks(const ekv_pool* pool, int32_t n, const void* const* h_src,
+                            const int32_t* h_new_blocks, hipStream_t stream);
+
+/*
  * Multi-layer transitions: the same pairs demoted (or refined) in every
  * layer's pool of a model in one launch.  In paged serving every layer has
  * its own pool and all layers share one block table, so a pair is one

@@ -353,6 +353,71 @@ ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pai
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
 }
 
+// The device address of [p, p + bytes) if the whole range is memory the
+// current device can read (its own memory, or pinned host memory mapped for
+// it), else an error.  Both ends are looked up: they must lie in memory the
+// runtime knows and map to device addresses exactly bytes - 1 apart.
+static ekv_status device_readable(const void* p, size_t bytes, int device, const uint8_t** out) {
+  hipPointerAttribute_t a0{}, a1{};
+  const char* last = static_cast<const char*>(p) + bytes - 1;
+  const bool known = hipPointerGetAttributes(&a0, p) == hipSuccess && hipPointerGetAttributes(&a1, last) == hipSuccess;
+  if (!known) {
+    (void)hipGetLastError();   // the failed lookup must not surface as a launch error
+    return fail(EKV_ERR_INVALID, "source %p is not memory the device can read (unpinned host memory?)", p);
+  }
+  for (const hipPointerAttribute_t* a : {&a0, &a1}) {
+    const bool ok = (a->type == hipMemoryTypeHost || (a->type == hipMemoryTypeDevice && a->device == device)) &&
+                    a->devicePointer != nullptr;
+    if (!ok) return fail(EKV_ERR_INVALID, "source %p is not mapped for the current device", p);
+  }
+  const char* d0 = static_cast<const char*>(a0.devicePointer);
+  const char* d1 = static_cast<const char*>(a1.devicePointer);
+  if (d1 - d0 != static_cast<ptrdiff_t>(bytes - 1))
+    return fail(EKV_ERR_INVALID, "source %p does not cover one block's bytes in one mapping", p);
+  *out = reinterpret_cast<const uint8_t*>(d0);
+  return EKV_OK;
+}
+
+ekv_status ekv_stage_blocks(const ekv_pool* pool, int32_t n, const void* const* h_src,
+                            const int32_t* h_new_blocks, hipStream_t stream) {
+  ekv_status st = check_pool(pool);
+  if (st != EKV_OK) return st;
+  if (n < 0) return fail(EKV_ERR_INVALID, "negative n");
+  if (n == 0) return EKV_OK;
+  if (!h_src || !h_new_blocks) return fail(EKV_ERR_INVALID, "h_src and h_new_blocks are required");
+  const int64_t block_bytes = (int64_t)2 * pool->num_kv_heads * pool->page_size * pool->head_dim *
+                              (pool->dtype == EKV_DTYPE_E5M2 ? 1 : 2);
+  std::vector<uint8_t> used((size_t)pool->num_blocks, 0);
+  for (int i = 0; i < n; ++i) {
+    const int b = h_new_blocks[i];
+    if (b < 0 || b >= pool->num_blocks) return fail(EKV_ERR_INVALID, "new block %d out of range", b);
+    if (used[b]) return fail(EKV_ERR_INVALID, "new block %d listed twice", b);
+    used[b] = 1;
+    if (!h_src[i]) return fail(EKV_ERR_INVALID, "source %d is NULL", i);
+  }
+  int device = 0;
+  if (hipGetDevice(&device) != hipSuccess) return hip_status(hipGetLastError(), "hipGetDevice");
+  // every source is checked before anything is enqueued
+  std::vector<const uint8_t*> dev((size_t)n);
+  for (int i = 0; i < n; ++i) {
+    st = device_readable(h_src[i], (size_t)block_bytes, device, &dev[i]);
+    if (st != EKV_OK) return st;
+  }
+  for (int first = 0; first < n; first += ekv::kStageMax) {
+    ekv::StageArgs a{};
+    a.pool = static_cast<uint8_t*>(pool->kv);
+    a.block_bytes = block_bytes;
+    a.n = std::min(n - first, ekv::kStageMax);
+    for (int k = 0; k < a.n; ++k) {
+      a.src[k] = dev[first + k];
+      a.dst[k] = h_new_blocks[first + k];
+    }
+    st = hip_status(ekv::launch_stage(a, stream), "ekv_stage_blocks launch");
+    if (st != EKV_OK) return st;
+  }
+  return EKV_OK;
+}
+
 ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
                              const int32_t* pairs, const int32_t* new_blocks, int32_t* block_table,
                              uint8_t* tags, int32_t batch, int32_t max_blocks, const uint8_t* lo_in,

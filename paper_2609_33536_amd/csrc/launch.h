@@ -52,6 +52,18 @@ struct TransitionArgs {
 hipError_t launch_demote(const TransitionArgs& a, hipStream_t st);
 hipError_t launch_refine(const TransitionArgs& a, hipStream_t st);
 
+// Block copies of one launch; the addresses travel in the kernel arguments.
+constexpr int kStageMax = 256;
+struct StageArgs {
+  uint8_t* pool;
+  int64_t block_bytes;                  // a multiple of 4096
+  const uint8_t* src[kStageMax];        // device-readable address of source i's block bytes
+  int32_t dst[kStageMax];               // destination block of source i
+  int32_t n;                            // 1..kStageMax
+};
+
+hipError_t launch_stage(const StageArgs& a, hipStream_t st);
+
 struct AppendArgs {
   uint16_t* pool;
   const int32_t* slots;

@@ -19,6 +19,12 @@
 // BASE (App. B.2): every wave reads its whole P and Q tiles before writing
 // either, so rebuilding Q over its own staged bytes is still tile-local.
 //
+// The staging copy of asynchronous promotion moves each pair's backed-up
+// refinement bytes into its new block.  Its sources are usually pinned host
+// memory mapped for the device, so the copy is a kernel that reads over the
+// host link: one launch keeps thousands of 16-byte reads in flight, where
+// one DMA copy per block pays a fixed cost per block.
+//
 // A multi-layer call transforms the same pairs in every layer's pool in one
 // launch (grid z = layer): the layers share one block table, as the layers
 // of a paged serving runtime do, so the table is read by every layer's
@@ -268,7 +274,21 @@ __global__ __launch_bounds__(64) void append_kernel(AppendArgs a) {
   }
 }
 
+// One 4 KiB piece of one block per workgroup, 16 bytes a lane.
+__global__ __launch_bounds__(256) void stage_kernel(StageArgs a) {
+  const int i = blockIdx.y;
+  const size_t off = (size_t)blockIdx.x * 4096 + 16 * threadIdx.x;
+  const u32x4 v = *reinterpret_cast<const u32x4*>(a.src[i] + off);
+  *reinterpret_cast<u32x4*>(a.pool + (size_t)a.dst[i] * a.block_bytes + off) = v;
+}
+
 }  // namespace
+
+hipError_t launch_stage(const StageArgs& a, hipStream_t st) {
+  if (a.n == 0) return hipSuccess;
+  hipLaunchKernelGGL(stage_kernel, dim3((unsigned)(a.block_bytes / 4096), a.n), dim3(256), 0, st, a);
+  return hipGetLastError();
+}
 
 hipError_t launch_demote(const TransitionArgs& a, hipStream_t st) {
   if (a.n == 0) return hipSuccess;

@@ -71,6 +71,7 @@ SIGNATURES = {
     "ekv_demote": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _I, _I, _P, _P, _S]),
     "ekv_refine": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_refine_staged": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _S]),
+    "ekv_stage_blocks": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _S]),
     "ekv_demote_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _I, _I, _P, _P, _S]),
     "ekv_refine_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_check_transition": (_I, [_I, _P, _I, _P, _P, _P, _I, _I, _I, _I, _P]),
@@ -203,6 +204,17 @@ def refine_staged(pool, pairs, new_blocks, block_table, tags, stream=None):
     bsz, max_blocks = block_table.shape
     _check(lib().ekv_refine_staged(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(new_blocks),
                                    _ptr(block_table), _ptr(tags), bsz, max_blocks, _stream(stream)))
+
+
+def stage_blocks(pool, sources, new_blocks, stream=None):
+    """Copy one block's bytes from each source address (device memory or
+    pinned host memory) into the blocks new_blocks (host int32 array)."""
+    srcs = np.ascontiguousarray([int(a) for a in sources], dtype=np.uint64)
+    new, np_ = _host(new_blocks, np.int32)
+    if len(srcs) != len(new):
+        raise EkvError(ERR_INVALID, "one new block per source")
+    _check(lib().ekv_stage_blocks(ctypes.byref(pool), len(new), srcs.ctypes.data_as(ctypes.c_void_p), np_,
+                                  _stream(stream)))
 
 
 def demote_layers(pool, layer_kv, pairs, block_table, tags, freed_out, lo_out=None, stream=None):

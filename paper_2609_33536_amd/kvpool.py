@@ -75,6 +75,13 @@ class HostMirror:
         self.reserved.update((int(s), int(j)) for s, j in pairs)
         return new
 
+    def cancel_refine(self, pairs, new):
+        """Undo :meth:`reserve_refine`: the blocks go back to the head of the
+        free pool in their order and the pairs are no longer reserved."""
+        self.free.extendleft(reversed(np.asarray(new, dtype=np.int32).tolist()))
+        for s, j in np.asarray(pairs, dtype=np.int32).reshape(-1, 2):
+            self.reserved.discard((int(s), int(j)))
+
     def publish_refine(self, pairs, new):
         """Apply the table update of a refinement (after its device work)."""
         for i, (s, j) in enumerate(np.asarray(pairs, dtype=np.int32).reshape(-1, 2)):
@@ -188,8 +195,8 @@ class AsyncPromotion:
     Demotion runs on the compute stream and emits the pair's refinement
     bytes; a copy stream moves them into pinned host memory (the CPU
     backing).  Promotion reserves one free block Q per pair and copies the
-    backing into Q on the copy stream; the pair stays BASE and executable
-    meanwhile.  :meth:`publish` orders the compute stream after a finished
+    backing into Q on the copy stream, with one kernel that reads the pinned
+    memory directly; the pair stays BASE and executable meanwhile.  :meth:`publish` orders the compute stream after a finished
     copy and runs the staged refinement, which rebuilds the pair and
     publishes the mapping.  Both streams have the default priority.
     """
@@ -200,6 +207,7 @@ class AsyncPromotion:
         self.copy = copy_stream if copy_stream is not None else torch.cuda.Stream()
         self.backing = {}     # (s, j) -> (pinned uint8 [block bytes], event: backing complete)
         self.inflight = []    # (copy-done event, pairs, new blocks, pinned sources)
+        self.last_copy = None  # (start, end) events of the last promotion's copy on the copy stream
 
     def demote(self, pairs, stream=None):
         """Demote on ``stream`` and back the refinement bytes up to the host.
@@ -232,18 +240,23 @@ class AsyncPromotion:
         if missing:
             raise ekv.EkvError(ekv.ERR_INVALID, f"no CPU backing for pairs {missing[:4]}")
         new = self.kv.mirror.reserve_refine(pairs)
-        nbytes = self.kv.block_bytes
-        flat = self.kv.kv.view(-1).view(torch.uint8)
-        sources = []
-        with torch.cuda.stream(self.copy):
-            for i, (s, j) in enumerate(pairs):
-                host, done = self.backing.pop((int(s), int(j)))
-                self.copy.wait_event(done)
-                q = int(new[i])
-                flat[q * nbytes:(q + 1) * nbytes].copy_(host, non_blocking=True)
-                sources.append(host)
-        ev = torch.cuda.Event()
+        keys = [(int(s), int(j)) for s, j in pairs]
+        sources = [self.backing[k][0] for k in keys]
+        for done in {id(self.backing[k][1]): self.backing[k][1] for k in keys}.values():
+            self.copy.wait_event(done)
+        # one copy kernel reads every pair's backing over the host link
+        start = torch.cuda.Event(enable_timing=True)
+        start.record(self.copy)
+        try:
+            ekv.stage_blocks(self.kv.pool, [h.data_ptr() for h in sources], new, self.copy)
+        except ekv.EkvError:
+            self.kv.mirror.cancel_refine(pairs, new)
+            raise
+        for k in keys:
+            del self.backing[k]
+        ev = torch.cuda.Event(enable_timing=True)
         ev.record(self.copy)
+        self.last_copy = (start, ev)
         self.inflight.append((ev, pairs, new, sources))
         return new
 

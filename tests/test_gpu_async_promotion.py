@@ -1,10 +1,12 @@
 """Asynchronous promotion from pinned CPU backing (App. B.2) on the GPU:
 demotion backs the refinement bytes up to pinned host memory on a copy
 stream; promotion reserves the new block and copies the backing into it
-while the pair stays BASE; decode during the copy sees the BASE pair;
-publishing runs the staged refinement.  Against the oracle: backing bytes,
-every pool byte of the live blocks, block table, tags and free FIFO
-bit-exact; decode before and after publication within tolerance."""
+(ekv_stage_blocks: one kernel reading the pinned memory) while the pair
+stays BASE; decode during the copy sees the BASE pair; publishing runs the
+staged refinement.  Against the oracle: backing bytes, every pool byte of
+the live blocks, block table, tags and free FIFO bit-exact; decode before
+and after publication within tolerance.  The staging copy on its own: every
+pool byte, from pinned and device sources, and its argument checks."""
 
 import numpy as np
 import pytest
@@ -121,3 +123,52 @@ def test_promotion_needs_backing_and_rejects_double_promotion():
         eng.promote(case["pairs"][1:2])     # already in flight (and its backing consumed)
     eng.publish(wait=True)
     torch.cuda.synchronize()
+
+
+@pytest.mark.parametrize("hkv,dtype,n", [(1, "e5m2", 3), (2, "bf16", 300), (8, "bf16", 256), (8, "e5m2", 129)])
+def test_stage_blocks_pinned_and_device_sources(hkv, dtype, n):
+    """The staging copy: sources in pinned host memory and in device memory
+    (mixed, in shuffled order, more than one launch's worth), destinations
+    scattered over the pool; every pool byte checked."""
+    torch = require_gpu()
+    block_bytes = 2 * hkv * PAGE * 128 * (1 if dtype == "e5m2" else 2)
+    nb = n + 37
+    rng = np.random.default_rng(72 + n + hkv)
+    pool_h = rng.integers(0, 256, size=(nb, block_bytes), dtype=np.uint8)
+    dev = torch.from_numpy(pool_h.copy()).cuda()
+    pool = ekv.make_pool(dev if dtype == "e5m2" else dev.view(torch.int16), hkv, dtype)
+    src_h = rng.integers(0, 256, size=(n, block_bytes), dtype=np.uint8)
+    pinned = torch.from_numpy(src_h.copy()).pin_memory()
+    on_dev = torch.from_numpy(src_h.copy()).cuda()
+    order = rng.permutation(n)
+    addrs = [(pinned if k % 3 else on_dev)[int(order[k])].data_ptr() for k in range(n)]
+    new = rng.choice(nb, n, replace=False).astype(np.int32)
+    print(f"stage_blocks: Hkv={hkv} {dtype} n={n}", flush=True)
+    ekv.stage_blocks(pool, addrs, new)
+    torch.cuda.synchronize()
+    want = pool_h.copy()
+    want[new] = src_h[order]
+    assert np.array_equal(dev.cpu().numpy(), want)
+
+
+def test_stage_blocks_rejects_bad_arguments_before_enqueueing():
+    torch = require_gpu()
+    hkv, nb = 2, 8
+    block_bytes = 2 * hkv * PAGE * 128 * 2
+    dev = torch.zeros((nb, block_bytes), dtype=torch.uint8, device="cuda")
+    pool = ekv.make_pool(dev.view(torch.int16), hkv, "bf16")
+    pinned = torch.full((2, block_bytes), 7, dtype=torch.uint8).pin_memory()
+    pageable = np.full((2, block_bytes), 9, dtype=np.uint8)
+    good = pinned[0].data_ptr()
+    for addrs, new in [([good, pageable.ctypes.data], [1, 2]),     # pageable host memory
+                       ([good, pinned[1].data_ptr()], [3, 3]),     # a block listed twice
+                       ([good], [nb]),                             # out of range
+                       ([good, 0], [1, 2])]:                       # NULL source
+        with pytest.raises(ekv.EkvError):
+            ekv.stage_blocks(pool, addrs, np.array(new, dtype=np.int32))
+    ekv.stage_blocks(pool, [], np.zeros(0, dtype=np.int32))       # nothing to do
+    torch.cuda.synchronize()
+    assert int(dev.sum()) == 0                                      # nothing was enqueued
+    ekv.stage_blocks(pool, [good], np.array([5], dtype=np.int32))   # the library is still usable
+    torch.cuda.synchronize()
+    assert int(dev[5].min()) == 7 and int(dev.sum()) == 7 * block_bytes
