@@ -94,6 +94,19 @@ __device__ __forceinline__ float max3(float a, float b, float c) {
   return r;
 }
 
+// v *= f in v's own registers.  The rescale of the output accumulators is a
+// rare branch; multiplying in place keeps the accumulators in the same
+// registers on both sides of it, where a plain multiply lets the compiler
+// give the result new registers and copy all 64 on the common path.
+__device__ __forceinline__ void scale_in_place(f32x16& v, float f) {
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    float x = v[i];
+    asm("v_mul_f32 %0, %0, %1" : "+v"(x) : "v"(f));
+    v[i] = x;
+  }
+}
+
 __device__ __forceinline__ void barrier() {
   asm volatile("" ::: "memory");
   __builtin_amdgcn_s_barrier();
@@ -116,8 +129,10 @@ __device__ __forceinline__ void wait_slots(int n) {
   }
 }
 
+// At least two waves per SIMD (at most 256 registers): with one, the matrix
+// cores idle through every softmax.
 template <typename T, int G, bool ELASTIC>
-__global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
+__global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2))) void prefill_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(16))) char ring[kPfRing][kSlotBytes];
   __shared__ int win_bt[kPfWindow];
   __shared__ int win_tag[kPfWindow];
@@ -195,25 +210,23 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
   const int dq = 16 * (g16 & 1);
   const int tr_a = i16 >> 2, tr_b = i16 & 3;   // 16-bit: key a, dims + 4b
   const int b8_a = i16 >> 1, b8_b = i16 & 1;   // 8-bit: key a, dims + 8b
-  // byte offsets inside a slot: K rows (per 16-dim step k), V^T rows (per
-  // 32-dim tile t and, for 16-bit elements, per half of the key step)
-  uint32_t off_kt[8], off_kb[8], off_vt[4][2], off_vb[4];
+  // byte offsets inside a slot.  The swizzles only flip the address bits
+  // that select the step, so each per-step offset is a per-lane base XOR a
+  // constant: K rows kt ^ 32k (16-bit) and kb ^ 16k (bytes) for the 16-dim
+  // step k; V^T rows vt[half] ^ 64t (16-bit, per half of the key step) and
+  // vb ^ 32t (bytes) for the 32-dim tile t.
+  const uint32_t off_kt = t_row * (2 * kHeadDim) + 16 * (h ^ (t_row & 1)) + 32 * (t_row >> 1);
+  const uint32_t off_kb = (n >> 4) * (kTileBytes / 2) + t_row * kHeadDim + 16 * tau(t_row) + 8 * h;
+  uint32_t off_vt[2];
 #pragma unroll
-  for (int k = 0; k < 8; ++k) {
-    off_kt[k] = t_row * (2 * kHeadDim) + 16 * ((2 * k + h) ^ t_row);
-    off_kb[k] = (n >> 4) * (kTileBytes / 2) + t_row * kHeadDim + 16 * (k ^ tau(t_row)) + 8 * h;
+  for (int half = 0; half < 2; ++half) {
+    const int key = 8 * half + 4 * h + tr_a;
+    const int x = 2 * (g16 & 1) + (tr_b >> 1);
+    off_vt[half] = kTileBytes + key * (2 * kHeadDim) + 16 * (x ^ (key & 3)) + 64 * (key >> 2) + 8 * (tr_b & 1);
   }
-#pragma unroll
-  for (int t = 0; t < 4; ++t) {
-    const int dd = 32 * t + dq + 4 * tr_b;
-#pragma unroll
-    for (int half = 0; half < 2; ++half) {
-      const int key = 8 * half + 4 * h + tr_a;
-      off_vt[t][half] = kTileBytes + key * (2 * kHeadDim) + 16 * ((dd >> 3) ^ key) + 2 * (dd & 7);
-    }
-    const int keyb = 8 * (b8_a >> 2) + 4 * h + (b8_a & 3);
-    off_vb[t] = kTileBytes + keyb * kHeadDim + 16 * (((32 * t + dq) >> 4) ^ tau(keyb)) + 8 * b8_b;
-  }
+  const int keyb = 8 * (b8_a >> 2) + 4 * h + (b8_a & 3);
+  const uint32_t off_vb =
+      kTileBytes + keyb * kHeadDim + 16 * ((g16 & 1) ^ (tau(keyb) & 1)) + 32 * (tau(keyb) >> 1) + 8 * b8_b;
 
   f32x16 o[4];
 #pragma unroll
@@ -267,17 +280,26 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
       const int key0 = cb * kPage;
       const int nkeys = base || two ? 32 : 16;
 
+      // The block kind only changes how the K and V operands are fetched:
+      // each fetch phase branches once on it (not once per step), so a
+      // phase's LDS reads are all in flight together, while the products
+      // and the accumulators stay in code common to both kinds.
       auto unit = [&](auto masked) {
         constexpr bool kMasked = decltype(masked)::value;
         // ---- S^T = K Q^T ----
+        u32x4 kop[8];
+        if (ELASTIC && base) {
+#pragma unroll
+          for (int k = 0; k < 8; ++k)
+            kop[k] = expand_base8(*reinterpret_cast<const u32x2*>(sa + (off_kb ^ (16 * k))));
+        } else {
+          const char* sk = n < 16 ? sa : sbk;   // the lane's key row is in its member's slot
+#pragma unroll
+          for (int k = 0; k < 8; ++k) kop[k] = *reinterpret_cast<const u32x4*>(sk + (off_kt ^ (32 * k)));
+        }
         f32x16 sc = f32x16{};
 #pragma unroll
-        for (int k = 0; k < 8; ++k) {
-          u32x4 kop;
-          if (base) kop = expand_base8(*reinterpret_cast<const u32x2*>(sa + off_kb[k]));
-          else kop = *reinterpret_cast<const u32x4*>((n < 16 ? sa : sbk) + off_kt[k]);
-          sc = Mma32<T>::mma(kop, qop[k], sc);
-        }
+        for (int k = 0; k < 8; ++k) sc = Mma32<T>::mma(kop[k], qop[k], sc);
 
         // ---- online softmax over this lane's 16 keys (+ lane ^ 32) ----
         if constexpr (kMasked) {
@@ -300,7 +322,7 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
           const float alpha = fast_exp2(m_run - m_new);
           l_run *= alpha;
 #pragma unroll
-          for (int t = 0; t < 4; ++t) o[t] *= alpha;
+          for (int t = 0; t < 4; ++t) scale_in_place(o[t], alpha);
           m_run = m_new;
         }
         // P = exp2(s c - m); its 16-bit head by truncation, the remainder
@@ -325,20 +347,23 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           if (kMasked && ks == 1 && nkeys < 32) break;
+          u32x4 vop[4];
+          if (ELASTIC && base) {
 #pragma unroll
-          for (int t = 0; t < 4; ++t) {
-            u32x4 vop;
-            if (base) {
+            for (int t = 0; t < 4; ++t) {
               const i32x2v raw =
-                  __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2)(sa + ks * (kTileBytes / 2) + off_vb[t]));
-              vop = expand_base8(u32x2{(uint32_t)raw[0], (uint32_t)raw[1]});
-            } else {
-              const char* sl = ks == 0 ? sa : sbk;
+                  __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2)(sa + ks * (kTileBytes / 2) + (off_vb ^ (32 * t))));
+              vop[t] = expand_base8(u32x2{(uint32_t)raw[0], (uint32_t)raw[1]});
+            }
+          } else {
+            const char* sl = ks == 0 ? sa : sbk;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
               uint32_t w[4];
 #pragma unroll
               for (int half = 0; half < 2; ++half) {
                 const u32x2 pr = __builtin_bit_cast(
-                    u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4)(sl + off_vt[t][half])));
+                    u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4)(sl + (off_vt[half] ^ (64 * t)))));
                 w[2 * half] = pr.x;
                 w[2 * half + 1] = pr.y;
               }
@@ -349,10 +374,13 @@ __global__ __launch_bounds__(64 * kPfWaves) void prefill_kernel(PrefillArgs a) {
                   if (key0 + key >= len) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
                 }
               }
-              vop = u32x4{w[0], w[1], w[2], w[3]};
+              vop[t] = u32x4{w[0], w[1], w[2], w[3]};
             }
-            o[t] = Mma32<T>::mma(vop, phi[ks], o[t]);
-            o[t] = Mma32<T>::mma(vop, plo[ks], o[t]);
+          }
+#pragma unroll
+          for (int t = 0; t < 4; ++t) {
+            o[t] = Mma32<T>::mma(vop[t], phi[ks], o[t]);
+            o[t] = Mma32<T>::mma(vop[t], plo[ks], o[t]);
           }
         }
       };
