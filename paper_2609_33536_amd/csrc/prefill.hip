@@ -29,7 +29,7 @@
 // keys a = 0..3 (0..7) of dim d + j.
 //
 // Column c sees keys p < lim(c) = prefix + (its chunk index) + 1.
-// Block-table entries and tags are staged in LDS per window of 256 blocks.
+// Block-table entries and tags are held in registers per window of 64 blocks.
 #include <type_traits>
 
 #include "attn_device.h"
@@ -40,7 +40,7 @@ namespace {
 constexpr int kPfWaves = 4;
 constexpr int kPfRing = 4;        // 8 KiB slots
 constexpr int kPfCols = 32;       // query columns per wave
-constexpr int kPfWindow = 256;    // blocks per metadata window
+constexpr int kPfWindow = 64;     // blocks per metadata window: one per lane
 
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef short i16x4v __attribute__((ext_vector_type(4)));
@@ -114,19 +114,15 @@ __device__ __forceinline__ void barrier() {
 }
 
 // Wait until at most 2n of this wave's vector memory instructions are in
-// flight (each ring slot costs a wave two loads); n is rounded down.
+// flight (each ring slot costs a wave two loads); 0 <= n < kPfRing, and a
+// larger n waits as for kPfRing - 1.
+static_assert(kPfRing == 4, "one wait per number of slots that may stay in flight");
 __device__ __forceinline__ void wait_slots(int n) {
   n = __builtin_amdgcn_readfirstlane(n);
-  switch (n < 0 ? 0 : (n > 7 ? 7 : n)) {
-    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-    case 1: asm volatile("s_waitcnt vmcnt(2)" ::: "memory"); break;
-    case 2: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
-    case 3: asm volatile("s_waitcnt vmcnt(6)" ::: "memory"); break;
-    case 4: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-    case 5: asm volatile("s_waitcnt vmcnt(10)" ::: "memory"); break;
-    case 6: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
-    default: asm volatile("s_waitcnt vmcnt(14)" ::: "memory"); break;
-  }
+  if (n >= 3) asm volatile("s_waitcnt vmcnt(6)" ::: "memory");
+  else if (n == 2) asm volatile("s_waitcnt vmcnt(4)" ::: "memory");
+  else if (n == 1) asm volatile("s_waitcnt vmcnt(2)" ::: "memory");
+  else asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
 }
 
 // At least two waves per SIMD (at most 256 registers): with one, the matrix
@@ -134,8 +130,6 @@ __device__ __forceinline__ void wait_slots(int n) {
 template <typename T, int G, bool ELASTIC>
 __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2))) void prefill_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(16))) char ring[kPfRing][kSlotBytes];
-  __shared__ int win_bt[kPfWindow];
-  __shared__ int win_tag[kPfWindow];
   constexpr int kTileTok = kPfWaves * kPfCols / G;
   const int s = blockIdx.z;
   const int kvh = blockIdx.y;
@@ -193,8 +187,10 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
     }
   }
 
-  // each wave loads quarter `wave` of every K and V tile of a slot
+  // each wave loads quarter `wave` of every K and V tile of a slot, at this
+  // LDS address (plus the slot's offset)
   const DmaOffsets dma = dma_offsets(lane + 64 * wave);
+  const uint32_t lds_wave = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_ptr)&ring[0][0] + 1024 * wave);
   const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTileBytes;
   const char* pool = reinterpret_cast<const char*>(a.pool) + (size_t)kvh * kTileBytes;
   const size_t v_off = (size_t)a.num_kv_heads * kTileBytes;
@@ -207,7 +203,6 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
   const int t_row = n & 15;
   const int g16 = lane >> 4;
   const int i16 = lane & 15;
-  const int dq = 16 * (g16 & 1);
   const int tr_a = i16 >> 2, tr_b = i16 & 3;   // 16-bit: key a, dims + 4b
   const int b8_a = i16 >> 1, b8_b = i16 & 1;   // 8-bit: key a, dims + 8b
   // byte offsets inside a slot.  The swizzles only flip the address bits
@@ -236,28 +231,33 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
 
   for (int w0 = 0; w0 < nblk; w0 += kPfWindow) {
     const int w1 = min(nblk, w0 + kPfWindow);
-    barrier();   // the ring and the window buffers are free
-    for (int i = tid; i < w1 - w0; i += 64 * kPfWaves) {
-      const int bt = btrow[w0 + i];
-      win_bt[i] = (unsigned)bt < (unsigned)a.num_blocks ? bt : 0;   // never leave the pool
-      win_tag[i] = (ELASTIC && use_tags) ? (int)tagrow[w0 + i] : 0;
+    barrier();   // the ring is free: every wave is done with the last window's units
+    // The window's metadata stays in registers: lane i holds the table entry
+    // of block w0 + i, and a 64-bit mask holds the BASE tags, so a DMA issue
+    // reads its block id with one lane read and no LDS round trip.
+    int bt_lane = 0;
+    bool base_lane = false;
+    if (w0 + lane < w1) {
+      const int bt = btrow[w0 + lane];
+      bt_lane = (unsigned)bt < (unsigned)a.num_blocks ? bt : 0;   // never leave the pool
+      if constexpr (ELASTIC)
+        base_lane = use_tags ? tagrow[w0 + lane] != 0 : (w0 + lane >= base_lo && w0 + lane < base_hi);
     }
-    asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)" ::: "memory");
-    barrier();
+    const uint64_t base_mask = __builtin_amdgcn_ballot_w64(base_lane);   // bit i: block w0 + i is BASE
 
     auto is_base = [&](int blk) -> bool {
       if constexpr (!ELASTIC) return false;
-      else return use_tags ? (win_tag[blk - w0] != 0) : (blk >= base_lo && blk < base_hi);
+      else return ((base_mask >> (blk - w0)) & 1) != 0;
     };
     int ib = w0, issued = 0, consumed = 0;
     auto issue = [&]() {
       const bool base = is_base(ib);
-      const char* src = pool + (size_t)win_bt[ib - w0] * block_bytes;
-      char* dst = ring[issued % kPfRing];
+      const char* src = pool + (size_t)(uint32_t)__builtin_amdgcn_readlane(bt_lane, ib - w0) * block_bytes;
+      const uint32_t dst = lds_wave + (uint32_t)(issued & (kPfRing - 1)) * kSlotBytes;
       const uint32_t off = base ? dma.base[0] : dma.tgt[0];
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off), (lds_ptr)(dst + 1024 * wave), 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + v_off + off),
-                                       (lds_ptr)(dst + kTileBytes + 1024 * wave), 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off), (lds_ptr)(size_t)dst, 16, 0, 0);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + v_off + off), (lds_ptr)(size_t)(dst + kTileBytes),
+                                       16, 0, 0);
       ib += base ? 2 : 1;
       ++issued;
     };
@@ -275,8 +275,8 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
       barrier();   // every wave's quarters have landed; the slots of the last unit are free
       while (ib < w1 && issued - consumed < kPfRing) issue();
 
-      const char* sa = ring[consumed % kPfRing];
-      const char* sbk = ring[(consumed + (two ? 1 : 0)) % kPfRing];
+      const char* sa = ring[consumed & (kPfRing - 1)];
+      const char* sbk = ring[(consumed + (two ? 1 : 0)) & (kPfRing - 1)];
       const int key0 = cb * kPage;
       const int nkeys = base || two ? 32 : 16;
 
