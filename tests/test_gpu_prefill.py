@@ -67,8 +67,12 @@ def test_prefill_dtypes(dtype, out_fp32):
     _run_prefill(c, 16, 4, out_fp32=out_fp32)
 
 
-def test_prefill_structured_and_general_agree():
-    c = workloads.make_prefill_case([1024, 640], [100, 37], 32, 8, seed=32, base_fraction=0.5,
+@pytest.mark.parametrize("prefix,chunk,fraction", [([1024, 640], [100, 37], 0.5),
+                                                   ([2000, 1500, 70], [90, 300, 5], 0.8)])
+def test_prefill_structured_and_general_agree(prefix, chunk, fraction):
+    """The BASE run of the second case crosses the kernel's 64-block
+    metadata windows (blocks 64 and 128) in both modes."""
+    c = workloads.make_prefill_case(prefix, chunk, 32, 8, seed=32, base_fraction=fraction,
                                     placement="oldest", spare_blocks=2)
     _run_prefill(c, 32, 8)
     _run_prefill(c, 32, 8, use_boundaries=False)
