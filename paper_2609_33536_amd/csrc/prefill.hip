@@ -87,6 +87,20 @@ __device__ __forceinline__ void split_p<Fp16>(float p0, float p1, uint32_t& hi, 
   lo = (uint32_t)e0 | ((uint32_t)e1 << 16);
 }
 
+// Prefill's TARGET tile layout: chunk c of token t at position c ^ sw(t),
+// sw(t) = 4 (t & 3) + (t >> 2).  The K reads (16 rows at one chunk per
+// 16 lanes) and the transposing V reads (4 rows x 4 consecutive chunks per
+// 32 lanes) then each touch 16 distinct 16-byte positions of a 256-byte
+// bank cycle, with no bank conflict; the decode layout (c ^ t) puts the
+// V reads' 4 x 2 chunks of a 16-lane group on only 4 positions.
+__device__ __forceinline__ int pf_swizzle(int t) { return 4 * (t & 3) + (t >> 2); }
+
+// Offset in a 4 KiB TARGET tile in HBM of the 16 B that land at LDS chunk p.
+__device__ __forceinline__ uint32_t pf_target_offset(int p) {
+  const int t = p >> 4, pos = p & 15;
+  return t * (2 * kHeadDim) + 16 * (pos ^ pf_swizzle(t));
+}
+
 // max of three floats in one instruction (finite or -inf inputs)
 __device__ __forceinline__ float max3(float a, float b, float c) {
   float r;
@@ -188,8 +202,10 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
   }
 
   // each wave loads quarter `wave` of every K and V tile of a slot, at this
-  // LDS address (plus the slot's offset)
+  // LDS address (plus the slot's offset); TARGET tiles in prefill's own
+  // swizzle, BASE tiles as in decode
   const DmaOffsets dma = dma_offsets(lane + 64 * wave);
+  const uint32_t dma_tgt = pf_target_offset(lane + 64 * wave);
   const uint32_t lds_wave = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_ptr)&ring[0][0] + 1024 * wave);
   const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTileBytes;
   const char* pool = reinterpret_cast<const char*>(a.pool) + (size_t)kvh * kTileBytes;
@@ -210,14 +226,16 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
   // constant: K rows kt ^ 32k (16-bit) and kb ^ 16k (bytes) for the 16-dim
   // step k; V^T rows vt[half] ^ 64t (16-bit, per half of the key step) and
   // vb ^ 32t (bytes) for the 32-dim tile t.
-  const uint32_t off_kt = t_row * (2 * kHeadDim) + 16 * (h ^ (t_row & 1)) + 32 * (t_row >> 1);
+  const int f_row = pf_swizzle(t_row);
+  const uint32_t off_kt = t_row * (2 * kHeadDim) + 16 * (h ^ (f_row & 1)) + 32 * (f_row >> 1);
   const uint32_t off_kb = (n >> 4) * (kTileBytes / 2) + t_row * kHeadDim + 16 * tau(t_row) + 8 * h;
   uint32_t off_vt[2];
 #pragma unroll
   for (int half = 0; half < 2; ++half) {
     const int key = 8 * half + 4 * h + tr_a;
     const int x = 2 * (g16 & 1) + (tr_b >> 1);
-    off_vt[half] = kTileBytes + key * (2 * kHeadDim) + 16 * (x ^ (key & 3)) + 64 * (key >> 2) + 8 * (tr_b & 1);
+    const int f = pf_swizzle(key);
+    off_vt[half] = kTileBytes + key * (2 * kHeadDim) + 16 * (x ^ (f & 3)) + 64 * (f >> 2) + 8 * (tr_b & 1);
   }
   const int keyb = 8 * (b8_a >> 2) + 4 * h + (b8_a & 3);
   const uint32_t off_vb =
@@ -254,7 +272,7 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
       const bool base = is_base(ib);
       const char* src = pool + (size_t)(uint32_t)__builtin_amdgcn_readlane(bt_lane, ib - w0) * block_bytes;
       const uint32_t dst = lds_wave + (uint32_t)(issued & (kPfRing - 1)) * kSlotBytes;
-      const uint32_t off = base ? dma.base[0] : dma.tgt[0];
+      const uint32_t off = base ? dma.base[0] : dma_tgt;
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off), (lds_ptr)(size_t)dst, 16, 0, 0);
       __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + v_off + off), (lds_ptr)(size_t)(dst + kTileBytes),
                                        16, 0, 0);
