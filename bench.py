@@ -71,6 +71,8 @@ def parse():
                          "into the decode traffic summary; no GPU use")
     ap.add_argument("--decode-only", action="store_true",
                     help="only the elastic decode launches (for PMC byte counters of that kernel)")
+    ap.add_argument("--prefill-only", action="store_true",
+                    help="only the chunked-prefill launches (for PMC counters of that kernel)")
     return ap.parse_args()
 
 
@@ -252,6 +254,16 @@ def main():
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     scale = 1.0 / math.sqrt(D)
+
+    if args.prefill_only:
+        pf = build_prefill(torch, kvpool, workloads)
+        pf_batch = pf["kv"].batch(HQ)
+        for _ in range(args.warmup + args.steps):
+            ekv.attn_prefill(pf["kv"].pool, pf_batch, pf["q"], pf["cu"], PF_CHUNK, pf["out"], scale)
+        torch.cuda.synchronize()
+        print(json.dumps({"prefill_only_launches": args.warmup + args.steps,
+                          "flops_per_launch": prefill_flops(PF_PREFIX, PF_CHUNK, PF_SEQS, HQ)}))
+        return 0
 
     print(f"[bench] building {WORKLOAD}: B={B} Hq={HQ} Hkv={HKV}", file=sys.stderr, flush=True)
     dec = build_decode(torch, kvpool, workloads, args.steps, args.warmup)
