@@ -409,6 +409,8 @@ def main():
             "mean over the f=0.25/0.5/1 launches of PMC FETCH_SIZE and WRITE_SIZE, each scaled by "
             "what it reads for a 1 GiB device copy")
     result["native_dispatch"] = native_dispatch(torch, ekv, pools[FRACTIONS.index(0.0)], q, outs[0], scale, stream)
+    print("[bench] 70B-shaped decode layer", file=sys.stderr, flush=True)
+    result["decode_70b"] = decode_70b(torch, ekv, kvpool, workloads, stream, scale)
     result["controller"] = controller_cost(ekv, tpool.mirror)
     print("[bench] 8-bit TARGET / 4-bit BASE decode", file=sys.stderr, flush=True)
     result["decode_8bit"] = decode_8bit(torch, ekv, kvpool, workloads, stream, seq_lens, scale)
@@ -445,6 +447,44 @@ def native_dispatch(torch, ekv, kv, q, out, scale, stream, reps=30):
     med = {k: float(np.median([a.elapsed_time(b) for a, b in v])) for k, v in times.items()}
     return {"native_ms": round(med["native"], 5), "elastic_forced_ms": round(med["elastic"], 5),
             "ratio": round(med["native"] / med["elastic"], 4), "acceptance": "ratio <= 1.02"}
+
+
+def decode_70b(torch, ekv, kvpool, workloads, stream, scale, reps=20):
+    """A Llama-3-70B-shaped decode layer: 256 sequences of 4096 tokens, 64
+    query / 8 KV heads, the oldest half of every sequence's pairs BASE
+    (structured), and the same launch forced through general mode (per-block
+    tags); median event times, algorithmic bytes as for the 8B layer."""
+    bsz, hq, length = 256, 64, 4096
+    seq_lens = np.full(bsz, length, dtype=np.int32)
+    case = workloads.make_decode_case_torch(seq_lens, hq, HKV, seed=2, spare_blocks=64)
+    pairs = workloads.choose_pairs(np.random.default_rng(2), seq_lens, 0.5, "oldest")
+    kv = kvpool.PagedKV(case["pool"], case["block_table"], seq_lens, case["free"], HKV)
+    kv.demote(pairs, emit_lo=False)
+    kv.commit()
+    mode = kv.relower()
+    out = torch.empty((bsz, hq, D), dtype=torch.bfloat16, device="cuda")
+    res = {"workload": f"{bsz} x {length} tokens, {hq}/{HKV} heads, oldest half of the pairs BASE"}
+    for name, b in (("structured", kv.batch(hq)), ("general", kv.batch(hq, mode=ekv.MODE_GENERAL,
+                                                                        use_boundaries=False))):
+        ws = ekv.decode_workspace(kv.pool, b)
+        times = []
+        for r in range(reps + 3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            ekv.attn_decode(kv.pool, b, case["q"], out, scale, ws)
+            e1.record(stream)
+            if r >= 3:
+                times.append((e0, e1))
+        torch.cuda.synchronize()
+        ms = float(np.median([a.elapsed_time(c) for a, c in times]))
+        nbytes = decode_bytes(seq_lens, kv.mirror.tags, hq, HKV, 2 if name == "general" else mode)
+        res[name] = {"ms": round(ms, 5), "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "bytes": nbytes,
+                     "tokens_per_s": round(bsz / (ms * 1e-3), 1)}
+        del ws
+    del kv, case
+    torch.cuda.empty_cache()
+    return res
 
 
 def decode_8bit(torch, ekv, kvpool, workloads, stream, seq_lens, scale, reps=20):
