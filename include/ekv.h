@@ -209,7 +209,10 @@ ekv_status ekv_append_kv(const ekv_pool* pool, const int32_t* slots, const void*
  * For each listed pair i = (s, j) (device int32 pairs[n][2]), with
  * b0 = block_table[s][2j] and b1 = block_table[s][2j+1]: the high bytes of
  * both blocks are packed into b0 in place; if lo_out is not NULL the low
- * bytes go to lo_out[i] (device uint8 [n][one block's bytes]); then
+ * bytes go to lo_out[i] (uint8 [n][one block's bytes], device memory or
+ * pinned host memory mapped for the device; a pinned host address is
+ * replaced by its device address after both ends of the range have been
+ * checked, see ekv_stage_blocks); then
  * block_table[s][2j+1] = b0, both tags = BASE and freed_out[i] = b1 (device
  * int32 [n]).  b1's bytes are not touched.  The caller returns freed_out[]
  * to its free pool only after the stream has passed this call.
@@ -225,7 +228,8 @@ ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs,
  * block Q = new_blocks[i] (device int32 [n]): member 0 is restored in place
  * into P and member 1 into Q from the high bytes in P and the refinement
  * bytes lo_in[i] (uint8 [n][one block's bytes], device memory or pinned
- * host memory mapped for the device); then block_table[s][2j+1] = Q and
+ * host memory mapped for the device, read over the host link; handled as
+ * lo_out of ekv_demote); then block_table[s][2j+1] = Q and
  * both tags = TARGET.  No attention call may read these pairs concurrently
  * on another stream.
  * Errors: EKV_ERR_INVALID, EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.

@@ -303,56 +303,6 @@ static ekv_status check_transition_args(const ekv_pool* pool, int32_t n, const i
   return EKV_OK;
 }
 
-ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int32_t* block_table,
-                      uint8_t* tags, int32_t batch, int32_t max_blocks, int32_t* freed_out,
-                      uint8_t* lo_out, hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (n == 0) return EKV_OK;
-  if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
-  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
-                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2};
-  return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
-}
-
-ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
-                             const int32_t* pairs, int32_t* block_table, uint8_t* tags, int32_t batch,
-                             int32_t max_blocks, int32_t* freed_out, uint8_t* lo_out, hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (!layer_kv || num_layers < 1 || num_layers > 65535)
-    return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
-  if (n == 0) return EKV_OK;
-  if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
-  ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
-                        freed_out, lo_out, n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2};
-  return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
-}
-
-ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
-                      const int32_t* new_blocks, int32_t* block_table, uint8_t* tags, int32_t batch,
-                      int32_t max_blocks, const uint8_t* lo_in, hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (n == 0) return EKV_OK;
-  if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
-  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2};
-  return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
-}
-
-ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pairs, const int32_t* new_blocks,
-                             int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,
-                             hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (n == 0) return EKV_OK;
-  if (!new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
-  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1, pool->dtype == EKV_DTYPE_E5M2};
-  return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
-}
-
 // The device address of [p, p + bytes) if the whole range is memory the
 // current device can read (its own memory, or pinned host memory mapped for
 // it), else an error.  Both ends are looked up: they must lie in memory the
@@ -378,6 +328,84 @@ static ekv_status device_readable(const void* p, size_t bytes, int device, const
   return EKV_OK;
 }
 
+// Refinement bytes may sit in pinned host memory: such a pointer is
+// replaced by its device address once the whole range has been checked.
+// Device pointers (and memory the runtime does not describe, such as
+// virtual-memory mappings) are passed on unchanged.
+static ekv_status resolve_lo(const uint8_t* p, size_t bytes, const uint8_t** out) {
+  *out = p;
+  hipPointerAttribute_t attr{};
+  if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
+    (void)hipGetLastError();
+    return EKV_OK;
+  }
+  if (attr.type != hipMemoryTypeHost) return EKV_OK;
+  int device = 0;
+  if (hipGetDevice(&device) != hipSuccess) return hip_status(hipGetLastError(), "hipGetDevice");
+  return device_readable(p, bytes, device, out);
+}
+
+static size_t block_bytes_of(const ekv_pool* pool) {
+  return (size_t)2 * pool->num_kv_heads * pool->page_size * pool->head_dim * (pool->dtype == EKV_DTYPE_E5M2 ? 1 : 2);
+}
+
+ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int32_t* block_table,
+                      uint8_t* tags, int32_t batch, int32_t max_blocks, int32_t* freed_out,
+                      uint8_t* lo_out, hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (n == 0) return EKV_OK;
+  if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
+  const uint8_t* lo = nullptr;
+  if (lo_out && (st = resolve_lo(lo_out, (size_t)n * block_bytes_of(pool), &lo)) != EKV_OK) return st;
+  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
+                        freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2};
+  return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
+}
+
+ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
+                             const int32_t* pairs, int32_t* block_table, uint8_t* tags, int32_t batch,
+                             int32_t max_blocks, int32_t* freed_out, uint8_t* lo_out, hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (!layer_kv || num_layers < 1 || num_layers > 65535)
+    return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
+  if (n == 0) return EKV_OK;
+  if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
+  const uint8_t* lo = nullptr;
+  if (lo_out && (st = resolve_lo(lo_out, (size_t)n * num_layers * block_bytes_of(pool), &lo)) != EKV_OK) return st;
+  ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
+                        freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2};
+  return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
+}
+
+ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
+                      const int32_t* new_blocks, int32_t* block_table, uint8_t* tags, int32_t batch,
+                      int32_t max_blocks, const uint8_t* lo_in, hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (n == 0) return EKV_OK;
+  if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
+  const uint8_t* lo = nullptr;
+  st = resolve_lo(lo_in, (size_t)n * block_bytes_of(pool), &lo);
+  if (st != EKV_OK) return st;
+  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
+                        nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2};
+  return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
+}
+
+ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pairs, const int32_t* new_blocks,
+                             int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,
+                             hipStream_t stream) {
+  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+  if (st != EKV_OK) return st;
+  if (n == 0) return EKV_OK;
+  if (!new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
+  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
+                        nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1, pool->dtype == EKV_DTYPE_E5M2};
+  return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
+}
+
 ekv_status ekv_stage_blocks(const ekv_pool* pool, int32_t n, const void* const* h_src,
                             const int32_t* h_new_blocks, hipStream_t stream) {
   ekv_status st = check_pool(pool);
@@ -385,8 +413,7 @@ ekv_status ekv_stage_blocks(const ekv_pool* pool, int32_t n, const void* const* 
   if (n < 0) return fail(EKV_ERR_INVALID, "negative n");
   if (n == 0) return EKV_OK;
   if (!h_src || !h_new_blocks) return fail(EKV_ERR_INVALID, "h_src and h_new_blocks are required");
-  const int64_t block_bytes = (int64_t)2 * pool->num_kv_heads * pool->page_size * pool->head_dim *
-                              (pool->dtype == EKV_DTYPE_E5M2 ? 1 : 2);
+  const int64_t block_bytes = (int64_t)block_bytes_of(pool);
   std::vector<uint8_t> used((size_t)pool->num_blocks, 0);
   for (int i = 0; i < n; ++i) {
     const int b = h_new_blocks[i];
@@ -428,8 +455,11 @@ ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
     return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
   if (n == 0) return EKV_OK;
   if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
+  const uint8_t* lo = nullptr;
+  st = resolve_lo(lo_in, (size_t)n * num_layers * block_bytes_of(pool), &lo);
+  if (st != EKV_OK) return st;
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo_in), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2};
+                        nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_layers launch");
 }
 

@@ -12,6 +12,7 @@ import numpy as np
 import pytest
 
 from oracle import attention as oatt
+from oracle import fp8 as ofp8
 from oracle import transitions as otr
 from paper_2609_33536_amd import ekv, kvpool, workloads
 from tests.gpu_util import check_attention, default_scale, host_safety_check, require_gpu, words_to_tensor
@@ -172,3 +173,56 @@ def test_stage_blocks_rejects_bad_arguments_before_enqueueing():
     ekv.stage_blocks(pool, [good], np.array([5], dtype=np.int32))   # the library is still usable
     torch.cuda.synchronize()
     assert int(dev[5].min()) == 7 and int(dev.sum()) == 7 * block_bytes
+
+
+@pytest.mark.parametrize("dtype,num_layers", [("bf16", 1), ("e5m2", 1), ("bf16", 3)])
+def test_refinement_bytes_in_pinned_host_memory(dtype, num_layers):
+    """Demotion writes the refinement bytes straight into pinned host memory
+    and refinement reads them back from there (the library passes the
+    device address of the mapping to its kernels): pools, tables, tags and
+    the bytes themselves bit-exact against the oracle."""
+    torch = require_gpu()
+    hkv = 2
+    c = workloads.make_decode_case([300, 1024, 77, 640], 4 * hkv, hkv, dtype=dtype, seed=73 + num_layers,
+                                   base_fraction=0.6, spare_blocks=40)
+    host_safety_check(c, c["pool"].shape)
+    ofmt = ofp8 if dtype == "e5m2" else otr
+    layers = [c["pool"]] + [np.random.default_rng(74 + k).integers(0, 2**16 if dtype == "bf16" else 2**8,
+                                                                  size=c["pool"].shape).astype(c["pool"].dtype)
+                            for k in range(num_layers - 1)]
+    dev = [torch.from_numpy(p.view(np.int16 if dtype == "bf16" else np.uint8).copy()).cuda() for p in layers]
+    pool = ekv.make_pool(dev[0], hkv, dtype)
+    pairs = c["pairs"]
+    n = len(pairs)
+    block_bytes = 2 * hkv * PAGE * 128 * (2 if dtype == "bf16" else 1)
+    bt = torch.from_numpy(c["block_table"].copy()).cuda()
+    tags = torch.from_numpy(c["tags"].copy()).cuda()
+    pairs_d = torch.from_numpy(pairs.copy()).cuda()
+    freed = torch.empty(n, dtype=torch.int32, device="cuda")
+    lo = torch.zeros((n, num_layers, block_bytes), dtype=torch.uint8).pin_memory()
+    print(f"pinned refinement bytes: {dtype} layers={num_layers} pairs={n}", flush=True)
+    if num_layers == 1:
+        ekv.demote(pool, pairs_d, bt, tags, freed, lo)
+    else:
+        layer_kv = torch.tensor([t.data_ptr() for t in dev], dtype=torch.int64, device="cuda")
+        ekv.demote_layers(pool, layer_kv, pairs_d, bt, tags, freed, lo)
+    torch.cuda.synchronize()
+    outs = [ofmt.demote(p, c["block_table"], c["tags"], pairs, c["seq_lens"]) for p in layers]
+    _, obt, otg, ofreed, _ = outs[0]
+    assert np.array_equal(freed.cpu().numpy(), ofreed)
+    for layer, (op, _, _, _, olo) in enumerate(outs):
+        assert np.array_equal(lo[:, layer].numpy().reshape(olo.shape), olo), layer
+    fifo = otr.FreeFifo(c["free"])
+    fifo.commit_freed(ofreed)
+    new = fifo.acquire(n)
+    new_d = torch.from_numpy(new).cuda()
+    if num_layers == 1:
+        ekv.refine(pool, pairs_d, new_d, bt, tags, lo)
+    else:
+        ekv.refine_layers(pool, layer_kv, pairs_d, new_d, bt, tags, lo)
+    torch.cuda.synchronize()
+    for layer, (op, obt_, otg_, _, olo) in enumerate(outs):
+        rp, rbt, rtg = ofmt.refine(op, obt_, otg_, pairs, new, olo, c["seq_lens"])
+        got = dev[layer].cpu().numpy().view(np.uint16 if dtype == "bf16" else np.uint8)
+        assert np.array_equal(got, rp), layer
+    assert np.array_equal(bt.cpu().numpy(), rbt) and np.array_equal(tags.cpu().numpy(), rtg)
