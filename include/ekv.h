@@ -42,6 +42,12 @@
  *     contents of device arrays (a tag that differs inside a pair, an
  *     already-BASE pair in a demotion list) are done by the ekv_check_*
  *     functions on host mirrors; the device calls assume valid lists.
+ *     Still, no device-side value makes a call touch memory outside the
+ *     arrays it was given: block-table entries and lengths are clamped into
+ *     the pool and the table, prefill query offsets into [0, total_q], and
+ *     append slots and transition-list entries that point outside the pool
+ *     or the table are skipped (a skipped demotion reports freed_out[i] =
+ *     -1).  Results for invalid lists are otherwise undefined.
  *   - Supported: head_dim 128, page_size 16, dtype bf16 or fp16,
  *     num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}.  Other shapes return
  *     EKV_ERR_UNSUPPORTED.

@@ -273,6 +273,7 @@ ekv_status ekv_attn_prefill(const ekv_pool* pool, const ekv_batch* batch, const 
   a.max_blocks = batch->max_blocks;
   a.max_q_len = max_q_len;
   a.num_blocks = pool->num_blocks;
+  a.total_q = total_q;
   a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
   a.scale_log2 = log2e_scale(scale);
   return hip_status(ekv::launch_prefill(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
@@ -287,7 +288,8 @@ ekv_status ekv_append_kv(const ekv_pool* pool, const int32_t* slots, const void*
   if (n == 0) return EKV_OK;
   if (!slots || !k || !v) return fail(EKV_ERR_INVALID, "slots, k and v are required");
   ekv::AppendArgs a{static_cast<uint16_t*>(pool->kv), slots, static_cast<const uint16_t*>(k),
-                    static_cast<const uint16_t*>(v), n, pool->num_kv_heads, pool->dtype == EKV_DTYPE_E5M2};
+                    static_cast<const uint16_t*>(v), n, pool->num_kv_heads, pool->dtype == EKV_DTYPE_E5M2,
+                    pool->num_blocks};
   return hip_status(ekv::launch_append(a, stream), "ekv_append_kv launch");
 }
 
@@ -359,7 +361,7 @@ ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int
   const uint8_t* lo = nullptr;
   if (lo_out && (st = resolve_lo(lo_out, (size_t)n * block_bytes_of(pool), &lo)) != EKV_OK) return st;
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
-                        freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2};
+                        freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
 }
 
@@ -375,7 +377,7 @@ ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
   const uint8_t* lo = nullptr;
   if (lo_out && (st = resolve_lo(lo_out, (size_t)n * num_layers * block_bytes_of(pool), &lo)) != EKV_OK) return st;
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
-                        freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2};
+                        freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
 }
 
@@ -390,7 +392,7 @@ ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
   st = resolve_lo(lo_in, (size_t)n * block_bytes_of(pool), &lo);
   if (st != EKV_OK) return st;
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2};
+                        nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
 }
 
@@ -402,7 +404,7 @@ ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pai
   if (n == 0) return EKV_OK;
   if (!new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1, pool->dtype == EKV_DTYPE_E5M2};
+                        nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
 }
 
@@ -459,7 +461,7 @@ ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
   st = resolve_lo(lo_in, (size_t)n * num_layers * block_bytes_of(pool), &lo);
   if (st != EKV_OK) return st;
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2};
+                        nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_layers launch");
 }
 

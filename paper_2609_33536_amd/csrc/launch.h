@@ -47,6 +47,8 @@ struct TransitionArgs {
   int32_t num_layers;        // 1 for a single-layer call
   int32_t staged;            // refine: pair i's refinement bytes are in block new_blocks[i] (lo unused)
   int32_t elem8;             // 8-bit TARGET / 4-bit BASE pool (else 16-bit / 8-bit)
+  int32_t batch;             // rows of bt and tags: pairs outside them are skipped
+  int32_t num_blocks;        // pool size: pairs whose blocks lie outside it are skipped
 };
 
 hipError_t launch_demote(const TransitionArgs& a, hipStream_t st);
@@ -71,6 +73,7 @@ struct AppendArgs {
   const uint16_t* v;
   int32_t n, num_kv_heads;
   int32_t elem8;             // 1-byte elements
+  int32_t num_blocks;        // pool size: slots outside it are skipped
 };
 
 hipError_t launch_append(const AppendArgs& a, hipStream_t st);
@@ -86,6 +89,7 @@ struct PrefillArgs {
   void* out;                 // [total][Hq][128]
   int32_t batch, num_kv_heads, num_q_heads, max_blocks, max_q_len, out_fp32;
   int32_t num_blocks;        // pool size: table entries are clamped into it
+  int32_t total_q;           // rows of q and out: query offsets are clamped into them
   float scale_log2;
 };
 

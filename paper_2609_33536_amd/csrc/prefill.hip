@@ -153,8 +153,9 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
   const int lane = tid & 63;
   const int n = lane & 31;     // MFMA column
   const int h = lane >> 5;     // half of the key / head-dim index space
-  const int q0 = a.cu_q[s];
-  const int nq = a.cu_q[s + 1] - q0;
+  // query rows of this sequence, clamped into q and out (never leave them)
+  const int q0 = min(max(a.cu_q[s], 0), a.total_q);
+  const int nq = min(max(a.cu_q[s + 1], q0), a.total_q) - q0;
   const int t_begin = tile * kTileTok;
   if (t_begin >= nq) return;   // uniform over the workgroup
   const int len = max(0, min(a.seq_lens[s], a.max_blocks * kPage));

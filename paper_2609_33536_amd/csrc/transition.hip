@@ -53,16 +53,35 @@ __device__ __forceinline__ size_t lo_offset(const TransitionArgs& a, int i, size
   return ((size_t)i * a.num_layers + blockIdx.z) * (2 * block_words);
 }
 
+// A list entry that points outside the arrays the call was given (a
+// sequence beyond the table, a pair beyond its row, a block beyond the
+// pool) is skipped by every kernel, so an invalid list cannot make a call
+// touch memory outside them.  Lists are validated on the host mirrors
+// (ekv_check_transition); for invalid lists the results are undefined.
+__device__ __forceinline__ bool pair_ok(const TransitionArgs& a, int s, int j) {
+  return (unsigned)s < (unsigned)a.batch && j >= 0 && 2 * j + 1 < a.max_blocks;
+}
+__device__ __forceinline__ bool block_ok(const TransitionArgs& a, int b) { return (unsigned)b < (unsigned)a.num_blocks; }
+// the pair's two table entries, or false
+__device__ __forceinline__ bool pair_blocks(const TransitionArgs& a, int s, int j, int& b0, int& b1) {
+  if (!pair_ok(a, s, j)) return false;
+  const int32_t* row = a.bt + (size_t)s * a.max_blocks;
+  b0 = row[2 * j];
+  b1 = row[2 * j + 1];
+  return block_ok(a, b0) && block_ok(a, b1);
+}
+
 __global__ __launch_bounds__(64) void demote_kernel(TransitionArgs a) {
   const int tile = blockIdx.x;   // plane * Hkv + head
   const int i = blockIdx.y;
   const int lane = threadIdx.x;
   const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
-  const int32_t* row = a.bt + (size_t)s * a.max_blocks;
+  int b0 = 0, b1 = 0;
+  if (!pair_blocks(a, s, j, b0, b1)) return;
   const size_t block_words = (size_t)2 * a.num_kv_heads * kTileWords;
   uint16_t* pool = layer_pool(a);
-  uint16_t* t0 = pool + (size_t)row[2 * j] * block_words + (size_t)tile * kTileWords;
-  const uint16_t* t1 = pool + (size_t)row[2 * j + 1] * block_words + (size_t)tile * kTileWords;
+  uint16_t* t0 = pool + (size_t)b0 * block_words + (size_t)tile * kTileWords;
+  const uint16_t* t1 = pool + (size_t)b1 * block_words + (size_t)tile * kTileWords;
 
   u32x4 w0[4], w1[4];
 #pragma unroll
@@ -93,10 +112,14 @@ __global__ __launch_bounds__(256) void demote_commit_kernel(TransitionArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
   const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  int b0 = 0, b1 = 0;
+  if (!pair_blocks(a, s, j, b0, b1)) {
+    a.freed[i] = -1;   // skipped entry: nothing was freed
+    return;
+  }
   int32_t* row = a.bt + (size_t)s * a.max_blocks;
   uint8_t* tg = a.tags + (size_t)s * a.max_blocks;
-  const int b0 = row[2 * j];
-  a.freed[i] = row[2 * j + 1];
+  a.freed[i] = b1;
   row[2 * j + 1] = b0;
   tg[2 * j] = 1;
   tg[2 * j + 1] = 1;
@@ -107,10 +130,13 @@ __global__ __launch_bounds__(64) void refine_kernel(TransitionArgs a) {
   const int i = blockIdx.y;
   const int lane = threadIdx.x;
   const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  int bp = 0, b1 = 0;
+  const int bq = a.new_blocks[i];
+  if (!pair_blocks(a, s, j, bp, b1) || !block_ok(a, bq)) return;
   const size_t block_words = (size_t)2 * a.num_kv_heads * kTileWords;
   uint16_t* pool = layer_pool(a);
-  uint16_t* tp = pool + (size_t)a.bt[(size_t)s * a.max_blocks + 2 * j] * block_words + (size_t)tile * kTileWords;
-  uint16_t* tq = pool + (size_t)a.new_blocks[i] * block_words + (size_t)tile * kTileWords;
+  uint16_t* tp = pool + (size_t)bp * block_words + (size_t)tile * kTileWords;
+  uint16_t* tq = pool + (size_t)bq * block_words + (size_t)tile * kTileWords;
   const uint8_t* packed = reinterpret_cast<const uint8_t*>(tp);
   // staged: the refinement bytes were copied into Q itself; its (plane, head)
   // tile holds exactly the bytes this wave rebuilds that tile from
@@ -177,11 +203,12 @@ __global__ __launch_bounds__(64) void demote8_kernel(TransitionArgs a) {
   const int i = blockIdx.y;
   const int lane = threadIdx.x;
   const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
-  const int32_t* row = a.bt + (size_t)s * a.max_blocks;
+  int b0 = 0, b1 = 0;
+  if (!pair_blocks(a, s, j, b0, b1)) return;
   const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTile8;
   uint8_t* pool = layer_pool8(a);
-  uint8_t* t0 = pool + (size_t)row[2 * j] * block_bytes + (size_t)tile * kTile8;
-  const uint8_t* t1 = pool + (size_t)row[2 * j + 1] * block_bytes + (size_t)tile * kTile8;
+  uint8_t* t0 = pool + (size_t)b0 * block_bytes + (size_t)tile * kTile8;
+  const uint8_t* t1 = pool + (size_t)b1 * block_bytes + (size_t)tile * kTile8;
   u32x4 x0[2], x1[2];
 #pragma unroll
   for (int r = 0; r < 2; ++r) {
@@ -203,10 +230,13 @@ __global__ __launch_bounds__(64) void refine8_kernel(TransitionArgs a) {
   const int i = blockIdx.y;
   const int lane = threadIdx.x;
   const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  int bp = 0, b1 = 0;
+  const int bq = a.new_blocks[i];
+  if (!pair_blocks(a, s, j, bp, b1) || !block_ok(a, bq)) return;
   const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTile8;
   uint8_t* pool = layer_pool8(a);
-  uint8_t* tp = pool + (size_t)a.bt[(size_t)s * a.max_blocks + 2 * j] * block_bytes + (size_t)tile * kTile8;
-  uint8_t* tq = pool + (size_t)a.new_blocks[i] * block_bytes + (size_t)tile * kTile8;
+  uint8_t* tp = pool + (size_t)bp * block_bytes + (size_t)tile * kTile8;
+  uint8_t* tq = pool + (size_t)bq * block_bytes + (size_t)tile * kTile8;
   const uint8_t* lo = a.staged ? tq : a.lo + ((size_t)i * a.num_layers + blockIdx.z) * block_bytes + (size_t)tile * kTile8;
   u32x4 h[2], l[2];
 #pragma unroll
@@ -231,6 +261,8 @@ __global__ __launch_bounds__(256) void refine_commit_kernel(TransitionArgs a) {
   const int i = blockIdx.x * blockDim.x + threadIdx.x;
   if (i >= a.n) return;
   const int s = a.pairs[2 * i], j = a.pairs[2 * i + 1];
+  int bp = 0, b1 = 0;
+  if (!pair_blocks(a, s, j, bp, b1) || !block_ok(a, a.new_blocks[i])) return;
   a.bt[(size_t)s * a.max_blocks + 2 * j + 1] = a.new_blocks[i];
   uint8_t* tg = a.tags + (size_t)s * a.max_blocks;
   tg[2 * j] = 0;
@@ -243,6 +275,7 @@ __global__ __launch_bounds__(64) void append8_kernel(AppendArgs a) {
   const int i = blockIdx.x;
   const int lane = threadIdx.x;
   const int slot = a.slots[i];
+  if (slot < 0 || slot / kPage >= a.num_blocks) return;   // outside the pool: skipped
   const int blk = slot / kPage, off = slot % kPage;
   const int hkv = a.num_kv_heads;
   const size_t block_bytes = (size_t)2 * hkv * kTile8;
@@ -262,6 +295,7 @@ __global__ __launch_bounds__(64) void append_kernel(AppendArgs a) {
   const int i = blockIdx.x;
   const int lane = threadIdx.x;
   const int slot = a.slots[i];
+  if (slot < 0 || slot / kPage >= a.num_blocks) return;   // outside the pool: skipped
   const int blk = slot / kPage, off = slot % kPage;
   const int hkv = a.num_kv_heads;
   const size_t block_words = (size_t)2 * hkv * kTileWords;
