@@ -179,3 +179,32 @@ def decode(q_words, pool, block_table, tags, seq_lens, scale=None):
             kh = h // group
             out[s, h] = attention._softmax_weighted(scale * (k[:, kh, :] @ q[s, h]), v[:, kh, :])
     return out
+
+
+def prefill(q_words, cu_q, pool, block_table, tags, seq_lens, scale=None):
+    """Chunked-prefill attention over an 8-bit pool (App. A: a chunk attends
+    its cached prefix and, causally, itself): q FP16 words uint16
+    [total_new][Hq][d], sequence s's rows at cu_q[s]..cu_q[s+1] with their
+    K/V already appended; row i of the chunk sees keys 0 .. seq_lens[s] -
+    n_s + i.  Float64 result [total_new][Hq][d]."""
+    q = np.asarray(q_words, dtype=np.uint16).view(np.float16).astype(np.float64)
+    total, hq, d = q.shape
+    hkv = pool.shape[2]
+    group = hq // hkv
+    if scale is None:
+        scale = 1.0 / np.sqrt(d)
+    out = np.zeros((total, hq, d), dtype=np.float64)
+    for s in range(len(seq_lens)):
+        r0, r1 = int(cu_q[s]), int(cu_q[s + 1])
+        n, length = r1 - r0, int(seq_lens[s])
+        if n == 0:
+            continue
+        if n > length:
+            raise ValueError("chunk longer than the sequence")
+        k, v = gather_sequence(pool, block_table[s], tags[s], length)
+        visible = np.arange(length)[None, :] <= (length - n + np.arange(n))[:, None]
+        for h in range(hq):
+            kh = h // group
+            scores = np.where(visible, scale * (q[r0:r1, h] @ k[:, kh, :].T), -np.inf)
+            out[r0:r1, h] = attention._softmax_weighted(scores, v[:, kh, :])
+    return out

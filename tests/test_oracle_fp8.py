@@ -2,8 +2,9 @@
 generalisation): the E5M2 decoding against torch's float8_e5m2 for all 256
 codes, the closed form of the BASE values, exact refinement for every
 byte, a hand-packed nibble row, the paged gather against a dense copy, the
-transition round trip on a whole pool, and attention against SDPA (f = 0)
-and against the truncated pool (f = 1)."""
+transition round trip on a whole pool, attention against SDPA (f = 0)
+and against the truncated pool (f = 1), and chunked prefill against causal
+SDPA and, with BASE pairs, against the truncated pool."""
 
 import numpy as np
 import torch
@@ -114,4 +115,39 @@ def test_attention_f0_matches_sdpa_and_f1_matches_truncated_pool():
         for m in range(2):
             trunc[bt[s, 2 * j + m]] &= 0xF0
     np.testing.assert_allclose(fp8.decode(q, p2, bt2, tg2, lens), fp8.decode(q, trunc, bt, tags, lens),
+                               rtol=0, atol=0)
+
+
+def test_prefill_matches_causal_sdpa_and_base_pairs_match_the_truncated_pool():
+    """Chunk row i of a sequence with context L and chunk n sees keys
+    0 .. L - n + i: against SDPA with that mask on the dense values, and,
+    with BASE pairs, equal to the same prefill over the pool whose BASE
+    members hold their truncated bytes."""
+    prefix, chunk = [40, 200, 3], [9, 56, 30]
+    lens = [p + c for p, c in zip(prefix, chunk)]
+    hq, hkv = 8, 2
+    rng = np.random.default_rng(6)
+    pool = rng.integers(0, 256, size=(48, 2, hkv, PAGE, 128), dtype=np.uint8)
+    pool = np.where((pool & 0x7C) == 0x7C, pool & 0xBF, pool).astype(np.uint8)    # no Inf/NaN codes
+    bt = np.arange(48, dtype=np.int32).reshape(3, 16)
+    tags = np.zeros((3, 16), dtype=np.uint8)
+    cu = np.concatenate([[0], np.cumsum(chunk)]).astype(np.int32)
+    q = (rng.standard_normal((int(cu[-1]), hq, 128)).astype(np.float16)).view(np.uint16)
+    out = fp8.prefill(q, cu, pool, bt, tags, lens)
+    for s, (length, n) in enumerate(zip(lens, chunk)):
+        k, v = fp8.gather_sequence(pool, bt[s], tags[s], length)
+        qs = torch.from_numpy(q[cu[s]:cu[s + 1]].view(np.float16).astype(np.float64)).permute(1, 0, 2)[None]
+        kk = torch.from_numpy(k).permute(1, 0, 2).repeat_interleave(hq // hkv, 0)[None]
+        vv = torch.from_numpy(v).permute(1, 0, 2).repeat_interleave(hq // hkv, 0)[None]
+        mask = torch.arange(length)[None, :] <= (length - n + torch.arange(n))[:, None]
+        ref = torch.nn.functional.scaled_dot_product_attention(qs, kk, vv, attn_mask=mask)[0].permute(1, 0, 2)
+        np.testing.assert_allclose(out[cu[s]:cu[s + 1]], ref.numpy(), rtol=1e-12, atol=1e-12)
+    pairs = np.array([(s, j) for s in range(3) for j in range(prefix[s] // 32) if j % 2 == 0], dtype=np.int32)
+    assert len(pairs) > 0
+    p2, bt2, tg2, _, _ = fp8.demote(pool, bt, tags, pairs, lens)
+    trunc = pool.copy()
+    for s, j in pairs:
+        for m in range(2):
+            trunc[bt[s, 2 * j + m]] &= 0xF0
+    np.testing.assert_allclose(fp8.prefill(q, cu, p2, bt2, tg2, lens), fp8.prefill(q, cu, trunc, bt, tags, lens),
                                rtol=0, atol=0)
