@@ -414,6 +414,8 @@ def main():
     result["controller"] = controller_cost(ekv, tpool.mirror)
     print("[bench] 8-bit TARGET / 4-bit BASE decode", file=sys.stderr, flush=True)
     result["decode_8bit"] = decode_8bit(torch, ekv, kvpool, workloads, stream, seq_lens, scale)
+    print("[bench] 8-bit TARGET / 4-bit BASE prefill", file=sys.stderr, flush=True)
+    result["prefill_8bit"] = prefill_8bit(torch, ekv, kvpool, workloads, stream, scale)
     print("[bench] asynchronous promotion", file=sys.stderr, flush=True)
     result["async_promotion"] = async_promotion_cost(torch, kvpool, tpool, cand, stream)
     print("[bench] multi-layer transitions", file=sys.stderr, flush=True)
@@ -533,6 +535,44 @@ def decode_8bit(torch, ekv, kvpool, workloads, stream, seq_lens, scale, reps=20)
     del base
     torch.cuda.empty_cache()
     return res
+
+
+def prefill_8bit(torch, ekv, kvpool, workloads, stream, scale, reps=20):
+    """The prefill workload of the main step (16 x (2048-token prefix, half of
+    its pairs BASE, + 512-token chunk), 32 query / 8 KV heads) over an 8-bit
+    TARGET (FP8 E5M2) / 4-bit BASE pool with FP16 queries and outputs: median
+    event time of the prefill launch; its products run on FP16 matrix cores,
+    so the peak is the dense FP16 one."""
+    c = workloads.make_prefill_case([PF_PREFIX] * PF_SEQS, [PF_CHUNK] * PF_SEQS, HQ, HKV, dtype="e5m2",
+                                    seed=PF_SEED, base_fraction=0.5, spare_blocks=2)
+    kv = kvpool.PagedKV(c["pool"], c["block_table"], c["seq_lens"], c["free"], HKV, "e5m2")
+    kv.append(torch.from_numpy(c["slots"]).cuda(), torch.from_numpy(np.ascontiguousarray(c["k_new"])).cuda(),
+              torch.from_numpy(np.ascontiguousarray(c["v_new"])).cuda())
+    if len(c["pairs"]):
+        kv.demote(c["pairs"], emit_lo=False)
+        kv.commit()
+    kv.relower()
+    batch = kv.batch(HQ)
+    q = torch.from_numpy(np.ascontiguousarray(c["q"]).view(np.int16)).cuda().view(torch.float16)
+    cu = torch.from_numpy(c["cu_q"]).cuda()
+    out = torch.empty((PF_SEQS * PF_CHUNK, HQ, D), dtype=torch.float16, device="cuda")
+    times = []
+    for r in range(reps + 3):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        ekv.attn_prefill(kv.pool, batch, q, cu, PF_CHUNK, out, scale)
+        e1.record(stream)
+        e1.synchronize()
+        if r >= 3:
+            times.append(e0.elapsed_time(e1))
+    ms = float(np.median(times))
+    flops = prefill_flops(PF_PREFIX, PF_CHUNK, PF_SEQS, HQ)
+    del kv, q, out
+    torch.cuda.empty_cache()
+    return {"ms": round(ms, 5), "TFLOP_per_s": round(flops / (ms * 1e-3) / 1e12, 1),
+            "mfma_peak_frac": round(flops / (ms * 1e-3) / 1e12 / MFMA_BF16_PEAK_TFLOPS, 4),
+            "new_tokens_per_s": round(PF_SEQS * PF_CHUNK / (ms * 1e-3), 1),
+            "base_pairs": int(len(c["pairs"])), "dtype": "e5m2 KV, fp16 q/out"}
 
 
 def async_promotion_cost(torch, kvpool, kv, cand, stream, pairs=256):

@@ -89,8 +89,8 @@ enum { EKV_DTYPE_BF16 = 0, EKV_DTYPE_FP16 = 1, EKV_DTYPE_FP32 = 2, EKV_DTYPE_E5M
  * each uint8 [page_size][head_dim / 2] with element e of a row in byte
  * e / 2, low nibble for even e.  Refinement nibbles ("lo") of a pair use the
  * same layout and fill exactly one 8-bit block.  Queries are FP16 and
- * outputs FP16 or FP32.  Supported: decode, append, demote, refine (also
- * multi-layer and staged); prefill returns EKV_ERR_UNSUPPORTED.
+ * outputs FP16 or FP32.  Every entry point accepts such a pool: decode,
+ * prefill, append, demote and refine (also multi-layer and staged).
  */
 
 /* Batch execution mode (§3.2; App. B.3): NATIVE for TARGET-only batches;
@@ -190,9 +190,9 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
  * of the chunk sees keys 0 .. seq_lens[s] - n_s + i (causal, inclusive),
  * where n_s = cu_q[s+1] - cu_q[s] and seq_lens[s] counts the whole context.
  * The prefix may mix TARGET and BASE blocks; the chunk's blocks are TARGET.
- *   q    device [total_q][num_q_heads][head_dim], pool dtype
+ *   q    device [total_q][num_q_heads][head_dim], pool dtype (FP16 for an 8-bit pool)
  *   cu_q device int32 [batch+1], nondecreasing, cu_q[0] = 0, cu_q[batch] = total_q
- *   out  device [total_q][num_q_heads][head_dim], out_dtype = pool dtype or EKV_DTYPE_FP32
+ *   out  device [total_q][num_q_heads][head_dim], out_dtype = the query dtype or EKV_DTYPE_FP32
  *   max_q_len  upper bound on every n_s (sizes the launch)
  * Errors: as ekv_attn_decode.
  */

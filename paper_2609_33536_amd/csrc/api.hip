@@ -253,9 +253,9 @@ ekv_status ekv_attn_prefill(const ekv_pool* pool, const ekv_batch* batch, const 
   if (total_q < 0 || max_q_len < 0) return fail(EKV_ERR_INVALID, "negative sizes");
   if (batch->batch == 0 || total_q == 0) return EKV_OK;
   if (!q || !out || !cu_q) return fail(EKV_ERR_INVALID, "q, cu_q and out are required");
-  if (pool->dtype == EKV_DTYPE_E5M2) return fail(EKV_ERR_UNSUPPORTED, "prefill over 8-bit pools is not built");
-  if (out_dtype != pool->dtype && out_dtype != EKV_DTYPE_FP32)
-    return fail(EKV_ERR_INVALID, "out_dtype must be the pool dtype or fp32");
+  const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
+  if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
+    return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
   if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
   if (max_q_len == 0) return EKV_OK;
   ekv::PrefillArgs a{};

@@ -93,6 +93,7 @@ struct PrefillArgs {
   float scale_log2;
 };
 
+// dtype: 0 bf16, 1 fp16, 3 8-bit (E5M2 TARGET / 4-bit BASE, FP16 queries).
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int group, bool elastic, hipStream_t st);
 
 }  // namespace ekv

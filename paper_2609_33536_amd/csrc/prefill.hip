@@ -101,6 +101,13 @@ __device__ __forceinline__ uint32_t pf_target_offset(int p) {
   return t * (2 * kHeadDim) + 16 * (pos ^ pf_swizzle(t));
 }
 
+// 8 nibbles (element e in byte e/2, low nibble for even e) -> 8 bytes,
+// each nibble in the high half of its byte (an executed 4-bit BASE value).
+__device__ __forceinline__ u32x2 widen_nibbles(uint32_t w) {
+  const uint32_t even = (w << 4) & 0xF0F0F0F0u, odd = w & 0xF0F0F0F0u;
+  return u32x2{perm(odd, even, 0x05010400u), perm(odd, even, 0x07030602u)};
+}
+
 // max of three floats in one instruction (finite or -inf inputs)
 __device__ __forceinline__ float max3(float a, float b, float c) {
   float r;
@@ -141,9 +148,14 @@ __device__ __forceinline__ void wait_slots(int n) {
 
 // At least two waves per SIMD (at most 256 registers): with one, the matrix
 // cores idle through every softmax.
-template <typename T, int G, bool ELASTIC>
+// F8: an 8-bit pool (FP8 E5M2 TARGET, 4-bit BASE).  A TARGET pair is
+// loaded into a slot in the byte layout of a packed 16-bit BASE pair (member
+// m from its own block) and a BASE pair's nibbles are staged and widened
+// into that layout, so every unit runs on the byte path with FP16 products.
+template <typename T, int G, bool ELASTIC, bool F8>
 __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2))) void prefill_kernel(PrefillArgs a) {
   __shared__ __attribute__((aligned(16))) char ring[kPfRing][kSlotBytes];
+  __shared__ __attribute__((aligned(16))) char nib[F8 ? kPfRing : 1][F8 ? kTileBytes : 16];
   constexpr int kTileTok = kPfWaves * kPfCols / G;
   const int s = blockIdx.z;
   const int kvh = blockIdx.y;
@@ -208,9 +220,15 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
   const DmaOffsets dma = dma_offsets(lane + 64 * wave);
   const uint32_t dma_tgt = pf_target_offset(lane + 64 * wave);
   const uint32_t lds_wave = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_ptr)&ring[0][0] + 1024 * wave);
-  const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTileBytes;
-  const char* pool = reinterpret_cast<const char*>(a.pool) + (size_t)kvh * kTileBytes;
-  const size_t v_off = (size_t)a.num_kv_heads * kTileBytes;
+  // a (plane, head) tile in HBM: 4 KiB of 16-bit words, or 2 KiB of bytes
+  constexpr int kTileP = F8 ? kTileBytes / 2 : kTileBytes;
+  const size_t block_bytes = (size_t)2 * a.num_kv_heads * kTileP;
+  const char* pool = reinterpret_cast<const char*>(a.pool) + (size_t)kvh * kTileP;
+  const size_t v_off = (size_t)a.num_kv_heads * kTileP;
+  // F8: offset of this lane's 16 B inside its member's tile (waves 0, 1 load
+  // member 0, waves 2, 3 member 1), and this wave's share of the staging area
+  const uint32_t dma_member = dma.base[0] - (uint32_t)(wave >> 1) * (kTileBytes / 2);
+  const uint32_t nib_wave = __builtin_amdgcn_readfirstlane((uint32_t)(size_t)(lds_ptr)&nib[0][0] + 512 * wave);
   const int32_t* btrow = a.bt + (size_t)s * a.max_blocks;
   const uint8_t* tagrow = a.tags ? a.tags + (size_t)s * a.max_blocks : nullptr;
 
@@ -273,11 +291,36 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
       const bool base = is_base(ib);
       const char* src = pool + (size_t)(uint32_t)__builtin_amdgcn_readlane(bt_lane, ib - w0) * block_bytes;
       const uint32_t dst = lds_wave + (uint32_t)(issued & (kPfRing - 1)) * kSlotBytes;
-      const uint32_t off = base ? dma.base[0] : dma_tgt;
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off), (lds_ptr)(size_t)dst, 16, 0, 0);
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + v_off + off), (lds_ptr)(size_t)(dst + kTileBytes),
-                                       16, 0, 0);
-      ib += base ? 2 : 1;
+      if constexpr (F8) {
+        if (base) {
+          // both members' nibbles (2 KiB per plane) to the staging area: this
+          // wave moves 512 B of K and of V with half its lanes
+          const uint32_t nd = nib_wave + (uint32_t)(issued & (kPfRing - 1)) * kTileBytes;
+          if (lane < 32) {
+            const char* ns = src + 512 * wave + 16 * lane;
+            __builtin_amdgcn_global_load_lds(static_cast<const void*>(ns), (lds_ptr)(size_t)nd, 16, 0, 0);
+            __builtin_amdgcn_global_load_lds(static_cast<const void*>(ns + v_off), (lds_ptr)(size_t)(nd + kTileBytes / 2),
+                                             16, 0, 0);
+          }
+          ib += 2;
+        } else {
+          // member m of a TARGET pair from its own block; a lone last block
+          // stands in for the missing member 1 (whose keys are masked)
+          const bool pair = ib + 1 < w1;
+          const int b1 = pair ? __builtin_amdgcn_readlane(bt_lane, ib + 1 - w0) : 0;
+          const char* srcm = (wave >> 1) && pair ? pool + (size_t)(uint32_t)b1 * block_bytes : src;
+          __builtin_amdgcn_global_load_lds(static_cast<const void*>(srcm + dma_member), (lds_ptr)(size_t)dst, 16, 0, 0);
+          __builtin_amdgcn_global_load_lds(static_cast<const void*>(srcm + v_off + dma_member),
+                                           (lds_ptr)(size_t)(dst + kTileBytes), 16, 0, 0);
+          ib += pair ? 2 : 1;
+        }
+      } else {
+        const uint32_t off = base ? dma.base[0] : dma_tgt;
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off), (lds_ptr)(size_t)dst, 16, 0, 0);
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + v_off + off),
+                                         (lds_ptr)(size_t)(dst + kTileBytes), 16, 0, 0);
+        ib += base ? 2 : 1;
+      }
       ++issued;
     };
 #pragma unroll
@@ -287,7 +330,7 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
     for (int cb = w0; cb < w1;) {
       // the unit: a BASE pair (one slot), two TARGET blocks, or a lone block
       const bool base = is_base(cb);
-      const bool two = !base && cb + 1 < w1;
+      const bool two = !F8 && !base && cb + 1 < w1;   // 8-bit units take one slot each
       const int nslots = two ? 2 : 1;
       while (issued < consumed + nslots) issue();   // (the ring normally runs ahead)
       wait_slots(issued - consumed - nslots);
@@ -297,7 +340,25 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
       const char* sa = ring[consumed & (kPfRing - 1)];
       const char* sbk = ring[(consumed + (two ? 1 : 0)) & (kPfRing - 1)];
       const int key0 = cb * kPage;
-      const int nkeys = base || two ? 32 : 16;
+      const bool full = base || cb + 1 < w1;   // two blocks in the unit (else the lone last one)
+      const int nkeys = full ? 32 : 16;
+      if constexpr (F8) {
+        if (base) {
+          // widen the staged nibbles: each lane makes one 16-byte chunk of K
+          // and one of V (member m, row t, chunk q at position q ^ tau(t))
+          const int p = lane + 64 * wave;
+          const int m = p >> 7, t = (p >> 3) & 15, qc = p & 7;
+          const char* ns = nib[consumed & (kPfRing - 1)] + m * (kTileBytes / 4) + t * (kHeadDim / 2) + 8 * qc;
+          char* bd = ring[consumed & (kPfRing - 1)] + m * (kTileBytes / 2) + t * kHeadDim + 16 * (qc ^ tau(t));
+#pragma unroll
+          for (int plane = 0; plane < 2; ++plane) {
+            const u32x2 x = *reinterpret_cast<const u32x2*>(ns + plane * (kTileBytes / 2));
+            const u32x2 lo = widen_nibbles(x.x), hi = widen_nibbles(x.y);
+            *reinterpret_cast<u32x4*>(bd + plane * kTileBytes) = u32x4{lo.x, lo.y, hi.x, hi.y};
+          }
+          barrier();   // the widened tiles are visible to every wave
+        }
+      }
 
       // The block kind only changes how the K and V operands are fetched:
       // each fetch phase branches once on it (not once per step), so a
@@ -307,7 +368,7 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
         constexpr bool kMasked = decltype(masked)::value;
         // ---- S^T = K Q^T ----
         u32x4 kop[8];
-        if (ELASTIC && base) {
+        if (F8 || (ELASTIC && base)) {
 #pragma unroll
           for (int k = 0; k < 8; ++k)
             kop[k] = expand_base8(*reinterpret_cast<const u32x2*>(sa + (off_kb ^ (16 * k))));
@@ -367,12 +428,19 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
         for (int ks = 0; ks < 2; ++ks) {
           if (kMasked && ks == 1 && nkeys < 32) break;
           u32x4 vop[4];
-          if (ELASTIC && base) {
+          if (F8 || (ELASTIC && base)) {
 #pragma unroll
             for (int t = 0; t < 4; ++t) {
               const i32x2v raw =
                   __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2)(sa + ks * (kTileBytes / 2) + (off_vb ^ (32 * t))));
               vop[t] = expand_base8(u32x2{(uint32_t)raw[0], (uint32_t)raw[1]});
+              if (F8 && kMasked) {   // 8-bit TARGET keys at or past the sequence end: zero V
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                  const int key = 16 * ks + 8 * (e >> 2) + 4 * h + (e & 3);
+                  if (key0 + key >= len) vop[t][e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+                }
+              }
             }
           } else {
             const char* sl = ks == 0 ? sa : sbk;
@@ -406,7 +474,7 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
       if (key0 + nkeys > lim_wave || nkeys < 32) unit(std::true_type{});
       else unit(std::false_type{});
       consumed += nslots;
-      cb += base || two ? 2 : 1;
+      cb += full ? 2 : 1;
     }
   }
 
@@ -427,23 +495,23 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
   }
 }
 
-template <typename T, int G>
+template <typename T, int G, bool F8>
 hipError_t launch_typed(const PrefillArgs& a, bool elastic, hipStream_t st) {
   constexpr int kTileTok = kPfWaves * kPfCols / G;
   dim3 grid((a.max_q_len + kTileTok - 1) / kTileTok, a.num_kv_heads, a.batch);
-  if (elastic) hipLaunchKernelGGL((prefill_kernel<T, G, true>), grid, dim3(64 * kPfWaves), 0, st, a);
-  else hipLaunchKernelGGL((prefill_kernel<T, G, false>), grid, dim3(64 * kPfWaves), 0, st, a);
+  if (elastic) hipLaunchKernelGGL((prefill_kernel<T, G, true, F8>), grid, dim3(64 * kPfWaves), 0, st, a);
+  else hipLaunchKernelGGL((prefill_kernel<T, G, false, F8>), grid, dim3(64 * kPfWaves), 0, st, a);
   return hipGetLastError();
 }
 
-template <typename T>
+template <typename T, bool F8>
 hipError_t launch_group(const PrefillArgs& a, int group, bool elastic, hipStream_t st) {
   switch (group) {
-    case 1: return launch_typed<T, 1>(a, elastic, st);
-    case 2: return launch_typed<T, 2>(a, elastic, st);
-    case 4: return launch_typed<T, 4>(a, elastic, st);
-    case 8: return launch_typed<T, 8>(a, elastic, st);
-    case 16: return launch_typed<T, 16>(a, elastic, st);
+    case 1: return launch_typed<T, 1, F8>(a, elastic, st);
+    case 2: return launch_typed<T, 2, F8>(a, elastic, st);
+    case 4: return launch_typed<T, 4, F8>(a, elastic, st);
+    case 8: return launch_typed<T, 8, F8>(a, elastic, st);
+    case 16: return launch_typed<T, 16, F8>(a, elastic, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -452,7 +520,8 @@ hipError_t launch_group(const PrefillArgs& a, int group, bool elastic, hipStream
 
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int group, bool elastic, hipStream_t st) {
   if (a.batch == 0 || a.max_q_len == 0) return hipSuccess;
-  return dtype == 0 ? launch_group<Bf16>(a, group, elastic, st) : launch_group<Fp16>(a, group, elastic, st);
+  if (dtype == 3) return launch_group<Fp16, true>(a, group, elastic, st);   // 8-bit pool, FP16 queries
+  return dtype == 0 ? launch_group<Bf16, false>(a, group, elastic, st) : launch_group<Fp16, false>(a, group, elastic, st);
 }
 
 }  // namespace ekv

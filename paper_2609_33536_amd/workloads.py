@@ -163,7 +163,7 @@ def make_prefill_case(prefix_lens, chunk_lens, num_q_heads, num_kv_heads, *,
             slots[cu[s] + i] = int(case["block_table"][s, t // page]) * page + t % page
     # BASE pairs only inside the prefix (new KV stays TARGET)
     case["pairs"] = choose_pairs(rng, prefix_lens, base_fraction, placement, page)
-    case["q"] = to_words(rng.standard_normal((n, num_q_heads, head_dim), dtype=np.float32), dtype)
+    case["q"] = to_words(rng.standard_normal((n, num_q_heads, head_dim), dtype=np.float32), query_dtype(dtype))
     case["k_new"] = to_words(rng.standard_normal((n, num_kv_heads, head_dim), dtype=np.float32), dtype)
     case["v_new"] = to_words(rng.standard_normal((n, num_kv_heads, head_dim), dtype=np.float32), dtype)
     case["cu_q"] = cu

@@ -2,8 +2,9 @@
 oracle: append, demote (with its refinement nibbles), refine (also staged
 and over several layers) bit for bit; decode of mixed pools (native,
 structured and general paths, every group size, ragged lengths with a lone
-last block) within the attention tolerance.  Prefill over such pools is not
-built and must say so."""
+last block) and chunked prefill over such pools (every BASE fraction, ragged
+chunks, structured and general, FP16 and FP32 output) within the attention
+tolerance."""
 
 import numpy as np
 import pytest
@@ -145,12 +146,53 @@ def test_append_e5m2_bit_exact():
     assert np.array_equal(dev.cpu().numpy(), ofp8.append(pool, slots, k, v))
 
 
-def test_prefill_over_e5m2_pool_is_unsupported():
+def _run_prefill(case, hq, hkv, *, use_boundaries=True, out_fp32=True):
     torch = require_gpu()
-    c = workloads.make_decode_case([64, 64], 8, 2, dtype="e5m2", seed=95, spare_blocks=2)
-    kv = kvpool.PagedKV(c["pool"], c["block_table"], c["seq_lens"], c["free"], 2, "e5m2")
-    q = torch.zeros((2, 8, 128), dtype=torch.float16, device="cuda")
-    cu = torch.tensor([0, 1, 2], dtype=torch.int32, device="cuda")
-    out = torch.zeros((2, 8, 128), dtype=torch.float16, device="cuda")
-    with pytest.raises(ekv.EkvError):
-        ekv.attn_prefill(kv.pool, kv.batch(8), q, cu, 1, out, default_scale())
+    host_safety_check(case, case["pool"].shape)
+    assert (case["slots"] >= 0).all() and (case["slots"] < case["pool"].shape[0] * PAGE).all()
+    kv = kvpool.PagedKV(case["pool"], case["block_table"], case["seq_lens"], case["free"], hkv, "e5m2")
+    kv.append(torch.from_numpy(case["slots"]).cuda(), _bytes_tensor(case["k_new"], torch),
+              _bytes_tensor(case["v_new"], torch))
+    opool = ofp8.append(case["pool"], case["slots"], case["k_new"], case["v_new"])
+    obt, otg = case["block_table"], case["tags"]
+    if len(case["pairs"]):
+        kv.demote(case["pairs"])
+        opool, obt, otg, _, _ = ofp8.demote(opool, obt, otg, case["pairs"], case["seq_lens"])
+    kv.relower()
+    q = words_to_tensor(case["q"], torch, "fp16")
+    out = torch.full((q.shape[0], hq, 128), float("nan"), dtype=torch.float32 if out_fp32 else torch.float16,
+                     device="cuda")
+    max_q = int(np.diff(case["cu_q"]).max())
+    print(f"prefill e5m2: B={len(case['seq_lens'])} Hq={hq} Hkv={hkv} rows={q.shape[0]} pairs={len(case['pairs'])} "
+          f"boundaries={use_boundaries} fp32={out_fp32}", flush=True)
+    ekv.attn_prefill(kv.pool, kv.batch(hq, use_boundaries=use_boundaries), q, torch.from_numpy(case["cu_q"]).cuda(),
+                     max_q, out, default_scale())
+    torch.cuda.synchronize()
+    ref = ofp8.prefill(case["q"], case["cu_q"], opool, obt, otg, case["seq_lens"])
+    return check_attention(out.float().cpu().numpy(), ref, out_fp32)
+
+
+@pytest.mark.parametrize("fraction", [0.0, 0.5, 1.0])
+@pytest.mark.parametrize("group", [1, 4, 16])
+def test_prefill_e5m2_groups_fractions_ragged(group, fraction):
+    hkv = 2
+    c = workloads.make_prefill_case([0, 17, 64, 100, 250, 33], [1, 40, 31, 7, 64, 90], hkv * group, hkv,
+                                    dtype="e5m2", seed=96 + group, base_fraction=fraction, spare_blocks=4)
+    _run_prefill(c, hkv * group, hkv)
+
+
+def test_prefill_e5m2_structured_general_and_fp16_output():
+    """The BASE run crosses the kernel's 64-block metadata windows."""
+    c = workloads.make_prefill_case([2000, 640, 70], [90, 37, 5], 32, 8, dtype="e5m2", seed=97,
+                                    base_fraction=0.8, placement="oldest", spare_blocks=2)
+    _run_prefill(c, 32, 8)
+    _run_prefill(c, 32, 8, use_boundaries=False)
+    _run_prefill(c, 32, 8, out_fp32=False)
+
+
+def test_prefill_e5m2_chunks_at_8b_shape():
+    """4 x (1024-token prefix, half of its pairs BASE, + 256-token chunk),
+    32 query / 8 KV heads: every output checked."""
+    c = workloads.make_prefill_case([1024] * 4, [256] * 4, 32, 8, dtype="e5m2", seed=98, base_fraction=0.5,
+                                    spare_blocks=2)
+    _run_prefill(c, 32, 8, out_fp32=False)
