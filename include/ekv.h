@@ -37,11 +37,14 @@
  *     never synchronises; errors detected on the host are returned before
  *     anything is enqueued; a launch failure returns EKV_ERR_HIP.
  *   - The library allocates no device memory.  Scratch space is passed in
- *     by the caller (see ekv_decode_workspace_bytes).
+ *     by the caller (see ekv_decode_workspace_bytes).  The one exception
+ *     is the EKV_DEBUG=1 mode of ekv_validate_batch, which also
+ *     synchronises.
  *   - Host-side checks cover shapes and pointers.  Checks that need the
  *     contents of device arrays (a tag that differs inside a pair, an
  *     already-BASE pair in a demotion list) are done by the ekv_check_*
- *     functions on host mirrors; the device calls assume valid lists.
+ *     functions on host mirrors, or on the device by the ekv_validate_*
+ *     functions; the other device calls assume valid lists.
  *     Still, no device-side value makes a call touch memory outside the
  *     arrays it was given: block-table entries and lengths are clamped into
  *     the pool and the table, prefill query offsets into [0, total_q], and
@@ -323,6 +326,74 @@ ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,
                                 const int32_t* h_seq_lens, int32_t batch, int32_t max_blocks,
                                 int32_t page_size, int32_t num_blocks,
                                 const int32_t* h_new_blocks);
+
+/*
+ * Device-side validation of the invariants the kernels rely on (§3.1: a
+ * pair's two blocks share one fidelity, and a BASE pair is two full blocks
+ * packed into one physical block; App. B.1: a transition starts from the
+ * opposite state).  The kernels themselves never leave their arrays on a
+ * violated invariant, but their results are then undefined; these calls
+ * find such inputs without a host copy of the metadata.
+ *
+ * Each call re-initialises report (device int32 [2 * EKV_VIOL_COUNT], caller
+ * owned) on the stream and then counts violations into it:
+ *   report[k]                    number of violations of kind k
+ *   report[EKV_VIOL_COUNT + k]   smallest index at which kind k occurs,
+ *                                0x7fffffff if none
+ * Batch indices are s * max_blocks + logical block (the checks of a whole
+ * sequence -- its length, its boundaries -- use block 0); list indices are
+ * the entry i of the pairs / new_blocks list.
+ * Asynchronous on the stream; nothing else is written.
+ *
+ * With EKV_DEBUG=1 in the environment, ekv_attn_decode, ekv_attn_prefill
+ * and every transition call run these checks first, synchronise the stream,
+ * and return EKV_ERR_INVALID (naming the first violation) without
+ * enqueuing anything else.  That mode allocates one report buffer per
+ * device on first use and is meant for debugging only.
+ */
+enum {
+  EKV_VIOL_SEQ_LEN = 0,       /* seq_lens[s] < 0, or beyond max_blocks*page_size or max_seq_len */
+  EKV_VIOL_BLOCK_RANGE = 1,   /* a visible logical block maps outside [0, num_blocks) */
+  EKV_VIOL_TAG_VALUE = 2,     /* a visible tag is neither TARGET nor BASE */
+  EKV_VIOL_PAIR_MIXED = 3,    /* the two visible blocks of a pair have different tags */
+  EKV_VIOL_BASE_PARTIAL = 4,  /* a pair executed as BASE is not two full blocks */
+  EKV_VIOL_BASE_ALIAS = 5,    /* a pair executed as BASE has two different table entries */
+  EKV_VIOL_MODE = 6,          /* mode / boundaries disagree with the tags (per pair), or bad boundaries (per s) */
+  EKV_VIOL_LIST_RANGE = 7,    /* list pair (s, j) outside the table, or a member maps outside the pool */
+  EKV_VIOL_LIST_STATE = 8,    /* list pair not TARGET (demotion) / not BASE (refinement) */
+  EKV_VIOL_LIST_PARTIAL = 9,  /* list pair not two full blocks (checked when seq_lens is given) */
+  EKV_VIOL_LIST_DUPLICATE = 10, /* list pair equal to an earlier entry */
+  EKV_VIOL_NEW_BLOCK = 11,    /* new block out of range or equal to an earlier one; or, with
+                                 seq_lens, a visible table entry holding a new block (index:
+                                 the new block's list entry) */
+  EKV_VIOL_COUNT = 12
+};
+
+/*
+ * Checks a batch as ekv_attn_decode / ekv_attn_prefill would execute it:
+ * per sequence its length; per visible logical block its table entry and
+ * tag; per visible pair mixed tags, and for a pair the batch mode executes
+ * as BASE (tags in GENERAL mode, boundaries in STRUCTURED mode when given,
+ * none in NATIVE mode) its two full blocks and shared table entry; the
+ * mode against the tags where both are given.
+ * Errors: EKV_ERR_INVALID (NULL pointers, sizes), EKV_ERR_HIP.
+ */
+ekv_status ekv_validate_batch(const ekv_pool* pool, const ekv_batch* batch, int32_t* report,
+                              hipStream_t stream);
+
+/*
+ * Checks a transition list (kind 0 demotion, 1 refinement) against the
+ * device block table and tags (both [batch][max_blocks]): each pair in
+ * range and mapping into the pool, in the starting state, and distinct; for
+ * a refinement with new_blocks [n], each new block in range and distinct.
+ * seq_lens (device [batch]) may be NULL; when given, pairs must be two full
+ * blocks and no visible table entry may hold a new block.
+ * Errors: EKV_ERR_INVALID (NULL pointers, sizes, kind), EKV_ERR_HIP.
+ */
+ekv_status ekv_validate_transition(const ekv_pool* pool, int32_t kind, int32_t n, const int32_t* pairs,
+                                   const int32_t* new_blocks, const int32_t* block_table,
+                                   const uint8_t* tags, const int32_t* seq_lens, int32_t batch,
+                                   int32_t max_blocks, int32_t* report, hipStream_t stream);
 
 /*
  * Pressure-aware fidelity control (§3.3, Alg. 1; defaults from App. B.1;

@@ -21,6 +21,9 @@ What it computes, and where the paper defines it:
   append of new TARGET KV, and the free-block FIFO (§3.1; §3.4; App. B.2).
 * ``lowering``   -- batch-level BASE indicator, per-sequence TARGET-BASE-
   TARGET boundaries or an explicit pair-mode table (§3.2; App. B.3).
+* ``validate``   -- the metadata invariants those steps rely on (pairs share
+  one fidelity, BASE pairs are two full blocks in one physical block,
+  transitions start from the opposite state; §3.1, App. B.1).
 
 Readings of points the paper leaves open (pair membership, which block of a
 pair survives demotion, the byte layout inside a packed block, where the

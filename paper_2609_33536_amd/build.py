@@ -15,7 +15,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libekv.so")
-SOURCES = ["api.hip", "control.hip", "decode.hip", "prefill.hip", "transition.hip"]
+SOURCES = ["api.hip", "control.hip", "decode.hip", "prefill.hip", "transition.hip", "validate.hip"]
 ARCH = "gfx950"
 
 FLAGS = [

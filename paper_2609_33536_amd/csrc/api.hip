@@ -6,6 +6,7 @@
 #include <cstdio>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <string>
 #include <vector>
 
@@ -119,6 +120,95 @@ DecodePlan plan_decode(const ekv_pool* p, const ekv_batch* b) {
 
 float log2e_scale(float scale) { return scale * 1.4426950408889634f; }
 
+// ---- device-side validation and the EKV_DEBUG mode ------------------------
+
+const char* violation_name(int k) {
+  static const char* const names[EKV_VIOL_COUNT] = {
+      "sequence length out of range", "table entry outside the pool", "tag value",
+      "pair with mixed tags", "BASE pair that is not two full blocks", "BASE pair with two table entries",
+      "mode or boundaries disagree with the tags", "list pair out of range", "list pair in the wrong state",
+      "list pair not two full blocks", "list pair listed twice", "new block out of range, repeated or in use"};
+  return k >= 0 && k < EKV_VIOL_COUNT ? names[k] : "unknown";
+}
+
+bool debug_mode() {
+  const char* e = getenv("EKV_DEBUG");
+  return e && e[0] && strcmp(e, "0") != 0;
+}
+
+ekv_status check_validate_batch(const ekv_pool* pool, const ekv_batch* batch, int32_t* report) {
+  ekv_status st = check_pool(pool);
+  if (st != EKV_OK) return st;
+  int group = 0;
+  if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
+  if (!report) return fail(EKV_ERR_INVALID, "report is required");
+  if ((long long)batch->batch * batch->max_blocks >= (1LL << 31))
+    return fail(EKV_ERR_UNSUPPORTED, "batch * max_blocks must be below 2^31");
+  return EKV_OK;
+}
+
+hipError_t enqueue_validate_batch(const ekv_pool* pool, const ekv_batch* batch, int32_t* report, hipStream_t stream) {
+  ekv::ValidateBatchArgs a{batch->seq_lens, batch->block_table, batch->tags,
+                           batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries, report,
+                           batch->batch, batch->max_blocks, pool->num_blocks, batch->max_seq_len, batch->mode};
+  return ekv::launch_validate_batch(a, stream);
+}
+
+// The report buffer of the debug mode: one per device, allocated on first use.
+ekv_status debug_report_buffer(int32_t** out) {
+  static std::mutex mu;
+  static std::vector<int32_t*> buffers;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return hip_status(hipGetLastError(), "hipGetDevice");
+  std::lock_guard<std::mutex> lock(mu);
+  if ((int)buffers.size() <= dev) buffers.resize(dev + 1, nullptr);
+  if (!buffers[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipMalloc(&p, 2 * EKV_VIOL_COUNT * sizeof(int32_t));
+    if (e != hipSuccess) return hip_status(e, "EKV_DEBUG report buffer");
+    buffers[dev] = static_cast<int32_t*>(p);
+  }
+  *out = buffers[dev];
+  return EKV_OK;
+}
+
+// Waits for the checks enqueued on the stream and turns the first reported
+// violation into EKV_ERR_INVALID.
+ekv_status debug_verdict(const int32_t* report, hipStream_t stream, const char* call) {
+  int32_t h[2 * EKV_VIOL_COUNT];
+  hipError_t e = hipMemcpyAsync(h, report, sizeof h, hipMemcpyDeviceToHost, stream);
+  if (e == hipSuccess) e = hipStreamSynchronize(stream);
+  if (e != hipSuccess) return hip_status(e, "EKV_DEBUG report read");
+  for (int k = 0; k < EKV_VIOL_COUNT; ++k)
+    if (h[k] > 0)
+      return fail(EKV_ERR_INVALID, "%s (EKV_DEBUG): %d violation(s): %s; first at index %d", call, h[k],
+                  violation_name(k), h[EKV_VIOL_COUNT + k]);
+  return EKV_OK;
+}
+
+ekv_status debug_check_batch(const ekv_pool* pool, const ekv_batch* batch, hipStream_t stream, const char* call) {
+  if ((long long)batch->batch * batch->max_blocks >= (1LL << 31))
+    return fail(EKV_ERR_UNSUPPORTED, "%s (EKV_DEBUG): batch * max_blocks must be below 2^31", call);
+  int32_t* report = nullptr;
+  ekv_status st = debug_report_buffer(&report);
+  if (st != EKV_OK) return st;
+  if ((st = hip_status(enqueue_validate_batch(pool, batch, report, stream), "EKV_DEBUG check launch")) != EKV_OK)
+    return st;
+  return debug_verdict(report, stream, call);
+}
+
+ekv_status debug_check_list(const ekv_pool* pool, int kind, int n, const int32_t* pairs, const int32_t* new_blocks,
+                            const int32_t* block_table, const uint8_t* tags, int batch, int max_blocks,
+                            hipStream_t stream, const char* call) {
+  int32_t* report = nullptr;
+  ekv_status st = debug_report_buffer(&report);
+  if (st != EKV_OK) return st;
+  ekv::ValidateListArgs a{pairs, new_blocks, block_table, tags, nullptr, report, n, kind, batch, max_blocks,
+                          pool->num_blocks};
+  if ((st = hip_status(ekv::launch_validate_list(a, stream), "EKV_DEBUG check launch")) != EKV_OK) return st;
+  return debug_verdict(report, stream, call);
+}
+
 }  // namespace
 
 extern "C" {
@@ -208,6 +298,8 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
   const DecodePlan plan = plan_decode(pool, batch);
   if (!ws || ws_bytes < plan.total)
     return fail(EKV_ERR_INVALID, "workspace of %zu bytes needed, %zu given", plan.total, ws_bytes);
+  if (plan.pairs_max >= (1LL << 30)) return fail(EKV_ERR_UNSUPPORTED, "batch too large for one decode call");
+  if (debug_mode() && (st = debug_check_batch(pool, batch, stream, "ekv_attn_decode")) != EKV_OK) return st;
   ekv::DecodeArgs a{};
   a.pool = static_cast<const uint16_t*>(pool->kv);
   a.q = static_cast<const uint16_t*>(q);
@@ -226,7 +318,6 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
   a.num_blocks = pool->num_blocks;
   a.len_cap = max_seq_blocks(batch) * ekv::kPage;
   if (batch->max_seq_len > 0) a.len_cap = std::min(a.len_cap, batch->max_seq_len);
-  if (plan.pairs_max >= (1LL << 30)) return fail(EKV_ERR_UNSUPPORTED, "batch too large for one decode call");
   a.max_splits = plan.max_pieces;
   a.min_chunk = plan.min_chunk;
   a.pairs_max = plan.pairs_max;
@@ -258,6 +349,7 @@ ekv_status ekv_attn_prefill(const ekv_pool* pool, const ekv_batch* batch, const 
     return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
   if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
   if (max_q_len == 0) return EKV_OK;
+  if (debug_mode() && (st = debug_check_batch(pool, batch, stream, "ekv_attn_prefill")) != EKV_OK) return st;
   ekv::PrefillArgs a{};
   a.pool = static_cast<const uint16_t*>(pool->kv);
   a.q = static_cast<const uint16_t*>(q);
@@ -360,6 +452,9 @@ ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int
   if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
   const uint8_t* lo = nullptr;
   if (lo_out && (st = resolve_lo(lo_out, (size_t)n * block_bytes_of(pool), &lo)) != EKV_OK) return st;
+  if (debug_mode() &&
+      (st = debug_check_list(pool, 0, n, pairs, nullptr, block_table, tags, batch, max_blocks, stream, "ekv_demote")) != EKV_OK)
+    return st;
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
                         freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
@@ -376,6 +471,9 @@ ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
   if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
   const uint8_t* lo = nullptr;
   if (lo_out && (st = resolve_lo(lo_out, (size_t)n * num_layers * block_bytes_of(pool), &lo)) != EKV_OK) return st;
+  if (debug_mode() && (st = debug_check_list(pool, 0, n, pairs, nullptr, block_table, tags, batch, max_blocks, stream,
+                                             "ekv_demote_layers")) != EKV_OK)
+    return st;
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
                         freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
@@ -391,6 +489,9 @@ ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
   const uint8_t* lo = nullptr;
   st = resolve_lo(lo_in, (size_t)n * block_bytes_of(pool), &lo);
   if (st != EKV_OK) return st;
+  if (debug_mode() &&
+      (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream, "ekv_refine")) != EKV_OK)
+    return st;
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
                         nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
@@ -403,6 +504,9 @@ ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pai
   if (st != EKV_OK) return st;
   if (n == 0) return EKV_OK;
   if (!new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
+  if (debug_mode() && (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream,
+                                             "ekv_refine_staged")) != EKV_OK)
+    return st;
   ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
                         nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
@@ -460,6 +564,9 @@ ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int
   const uint8_t* lo = nullptr;
   st = resolve_lo(lo_in, (size_t)n * num_layers * block_bytes_of(pool), &lo);
   if (st != EKV_OK) return st;
+  if (debug_mode() && (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream,
+                                             "ekv_refine_layers")) != EKV_OK)
+    return st;
   ekv::TransitionArgs a{nullptr, layer_kv, pairs, new_blocks, block_table, tags,
                         nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
   return hip_status(ekv::launch_refine(a, stream), "ekv_refine_layers launch");
@@ -513,6 +620,29 @@ ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,
     }
   }
   return EKV_OK;
+}
+
+ekv_status ekv_validate_batch(const ekv_pool* pool, const ekv_batch* batch, int32_t* report, hipStream_t stream) {
+  const ekv_status st = check_validate_batch(pool, batch, report);
+  if (st != EKV_OK) return st;
+  return hip_status(enqueue_validate_batch(pool, batch, report, stream), "ekv_validate_batch launch");
+}
+
+ekv_status ekv_validate_transition(const ekv_pool* pool, int32_t kind, int32_t n, const int32_t* pairs,
+                                   const int32_t* new_blocks, const int32_t* block_table, const uint8_t* tags,
+                                   const int32_t* seq_lens, int32_t batch, int32_t max_blocks, int32_t* report,
+                                   hipStream_t stream) {
+  const ekv_status st = check_pool(pool);
+  if (st != EKV_OK) return st;
+  if (kind != 0 && kind != 1) return fail(EKV_ERR_INVALID, "kind must be 0 (demotion) or 1 (refinement)");
+  if (n < 0 || batch < 0 || max_blocks < 2) return fail(EKV_ERR_INVALID, "bad sizes");
+  if (!report) return fail(EKV_ERR_INVALID, "report is required");
+  if (n > 0 && (!pairs || !block_table || !tags)) return fail(EKV_ERR_INVALID, "pairs, block_table and tags are required");
+  if ((long long)batch * max_blocks >= (1LL << 31))
+    return fail(EKV_ERR_UNSUPPORTED, "batch * max_blocks must be below 2^31");
+  ekv::ValidateListArgs a{pairs, kind == 1 ? new_blocks : nullptr, block_table, tags, seq_lens, report, n, kind,
+                          batch, max_blocks, pool->num_blocks};
+  return hip_status(ekv::launch_validate_list(a, stream), "ekv_validate_transition launch");
 }
 
 }  // extern "C"

@@ -96,4 +96,27 @@ struct PrefillArgs {
 // dtype: 0 bf16, 1 fp16, 3 8-bit (E5M2 TARGET / 4-bit BASE, FP16 queries).
 hipError_t launch_prefill(const PrefillArgs& a, int dtype, int group, bool elastic, hipStream_t st);
 
+struct ValidateBatchArgs {
+  const int32_t* seq_lens;   // [B]
+  const int32_t* bt;         // [B][max_blocks]
+  const uint8_t* tags;       // [B][max_blocks] or null
+  const int32_t* bounds;     // [B][2] or null
+  int32_t* report;           // [2 * EKV_VIOL_COUNT]
+  int32_t batch, max_blocks, num_blocks, max_seq_len, mode;
+};
+
+struct ValidateListArgs {
+  const int32_t* pairs;      // [n][2]
+  const int32_t* new_blocks; // [n] or null
+  const int32_t* bt;         // [B][max_blocks]
+  const uint8_t* tags;       // [B][max_blocks]
+  const int32_t* seq_lens;   // [B] or null
+  int32_t* report;           // [2 * EKV_VIOL_COUNT]
+  int32_t n, kind, batch, max_blocks, num_blocks;
+};
+
+// Both initialise the report, then count into it.
+hipError_t launch_validate_batch(const ValidateBatchArgs& a, hipStream_t st);
+hipError_t launch_validate_list(const ValidateListArgs& a, hipStream_t st);
+
 }  // namespace ekv

@@ -53,6 +53,11 @@ class CtrlState(ctypes.Structure):
 
 
 CTRL_SHORTAGE, CTRL_WATERMARK = 0, 1
+
+# violation kinds of the device-side checks, in the order of EKV_VIOL_*
+VIOLATIONS = ("seq_len", "block_range", "tag_value", "pair_mixed", "base_partial", "base_alias", "mode",
+              "list_range", "list_state", "list_partial", "list_duplicate", "new_block")
+NO_INDEX = 0x7FFFFFFF
 CTRL_EAGER_PROMOTION, CTRL_NO_PROMOTION = 1, 2
 
 
@@ -75,6 +80,8 @@ SIGNATURES = {
     "ekv_demote_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _I, _I, _P, _P, _S]),
     "ekv_refine_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_check_transition": (_I, [_I, _P, _I, _P, _P, _P, _I, _I, _I, _I, _P]),
+    "ekv_validate_batch": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _S]),
+    "ekv_validate_transition": (_I, [ctypes.POINTER(Pool), _I, _I, _P, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_ctrl_demotion": (_I, [ctypes.POINTER(CtrlConfig), ctypes.POINTER(CtrlState), _I, _I, _P, _P, _P,
                                _I, _I, _I, _P, _I, _P]),
     "ekv_ctrl_promotion": (_I, [ctypes.POINTER(CtrlConfig), ctypes.POINTER(CtrlState), _I, _I, _P, _P, _I,
@@ -245,6 +252,38 @@ def check_transition(kind, pairs, block_table, tags, seq_lens, num_blocks, new_b
     status = lib().ekv_check_transition(kind, pp, pairs.shape[0], bp, tgp, sp, bt.shape[0],
                                         bt.shape[1], page, num_blocks, nbp)
     return status == OK, (lib().ekv_last_error().decode() if status != OK else "")
+
+
+def _read_report(report, stream):
+    import torch
+    if stream is not None:
+        stream.synchronize()
+    else:
+        torch.cuda.current_stream().synchronize()
+    h = report.cpu().numpy()
+    n = len(VIOLATIONS)
+    return {name: (int(h[k]), int(h[n + k])) for k, name in enumerate(VIOLATIONS)}
+
+
+def validate_batch(pool, batch, stream=None):
+    """Device-side check of a batch's metadata.  Returns {kind: (count,
+    smallest index)} (index NO_INDEX when the count is 0); synchronises."""
+    import torch
+    report = torch.empty(2 * len(VIOLATIONS), dtype=torch.int32, device="cuda")
+    _check(lib().ekv_validate_batch(ctypes.byref(pool), ctypes.byref(batch), _ptr(report), _stream(stream)))
+    return _read_report(report, stream)
+
+
+def validate_transition(pool, kind, pairs, block_table, tags, seq_lens=None, new_blocks=None, stream=None):
+    """Device-side check of a demotion (kind 0) or refinement (kind 1) list;
+    as validate_batch."""
+    import torch
+    report = torch.empty(2 * len(VIOLATIONS), dtype=torch.int32, device="cuda")
+    bsz, max_blocks = block_table.shape
+    _check(lib().ekv_validate_transition(ctypes.byref(pool), kind, pairs.shape[0], _ptr(pairs), _ptr(new_blocks),
+                                         _ptr(block_table), _ptr(tags), _ptr(seq_lens), bsz, max_blocks,
+                                         _ptr(report), _stream(stream)))
+    return _read_report(report, stream)
 
 
 def ctrl_config(min_batch=16, decay=2, a_max=-1, sink_pairs=0, recent_pairs=0, policy=CTRL_SHORTAGE,
