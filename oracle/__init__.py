@@ -24,6 +24,12 @@ What it computes, and where the paper defines it:
 * ``validate``   -- the metadata invariants those steps rely on (pairs share
   one fidelity, BASE pairs are two full blocks in one physical block,
   transitions start from the opposite state; §3.1, App. B.1).
+* ``control``    -- the pressure-aware fidelity controller: shortage,
+  demotion count, surplus, decaying reserve and promotion budget, with the
+  rank orders of its candidates (§3.3, Alg. 1; App. B.1).
+* ``fp8``        -- the 8-bit TARGET (E5M2) / 4-bit BASE instance of the
+  same contract: encoding, packed nibble pairs, transitions, decode and
+  prefill (App. C.5, last paragraph).
 
 Readings of points the paper leaves open (pair membership, which block of a
 pair survives demotion, the byte layout inside a packed block, where the
@@ -35,4 +41,4 @@ formula (closed forms, exhaustive enumeration, brute force on tiny inputs,
 library routines, invariants); see the ``tests/test_oracle_*.py`` files.
 """
 
-from . import encoding, paged, attention, transitions, lowering  # noqa: F401
+from . import encoding, paged, attention, transitions, lowering, validate, control, fp8  # noqa: F401
