@@ -52,6 +52,22 @@ class _Report:
         self.first[kind] = min(self.first[kind], index)
 
 
+def full_pair(j, length, page):
+    """Pair j holds two full blocks of a sequence of this length (§3.1)."""
+    return 2 * page * (j + 1) <= length
+
+
+def executed_as_base(mode, by_range, b0, b1, j, t0, t1):
+    """Whether the attention kernels execute pair j as BASE: never in NATIVE
+    mode; by the range [b0, b1) in STRUCTURED mode when the sequence has one;
+    otherwise by the tag t0 of member 0 (t1 is member 1's)."""
+    if mode == NATIVE:
+        return False
+    if by_range:
+        return b0 <= j < b1
+    return t0 != 0
+
+
 def batch_violations(seq_lens, block_table, tags, boundaries, mode, num_blocks, max_seq_len=0, page=16):
     """Checks of a batch as the attention calls execute it.  tags and
     boundaries may be None."""
@@ -89,18 +105,14 @@ def batch_violations(seq_lens, block_table, tags, boundaries, mode, num_blocks, 
             t1 = int(tags[s, i + 1]) if (has1 and tags is not None) else t
             if has1 and t != t1:
                 rep.flag(PAIR_MIXED, idx)
-            exec_base = False
-            if mode == NATIVE:
-                if t != 0 or t1 != 0:
-                    rep.flag(MODE, idx)
-            elif structured and b0 >= 0:
-                exec_base = b0 <= j < b1
-                if tags is not None and (t != 0) != exec_base:
-                    rep.flag(MODE, idx)
-            else:
-                exec_base = t != 0
+            by_range = structured and b0 >= 0
+            exec_base = executed_as_base(mode, by_range, b0, b1, j, t, t1)
+            if mode == NATIVE and (t != 0 or t1 != 0):
+                rep.flag(MODE, idx)
+            if mode != NATIVE and by_range and tags is not None and (t != 0) != exec_base:
+                rep.flag(MODE, idx)
             if exec_base:
-                if 2 * page * (j + 1) > length:
+                if not full_pair(j, length, page):
                     rep.flag(BASE_PARTIAL, idx)
                 elif e1 != e:
                     rep.flag(BASE_ALIAS, idx)
@@ -130,7 +142,7 @@ def list_violations(kind, pairs, block_table, tags, num_blocks, seq_lens=None, n
             rep.flag(LIST_RANGE, i)
         if int(tags[s, 2 * j]) != want or int(tags[s, 2 * j + 1]) != want:
             rep.flag(LIST_STATE, i)
-        if seq_lens is not None and 2 * page * (j + 1) > int(seq_lens[s]):
+        if seq_lens is not None and not full_pair(j, int(seq_lens[s]), page):
             rep.flag(LIST_PARTIAL, i)
     if use_new and seq_lens is not None:
         for s in range(bsz):

@@ -130,3 +130,32 @@ def test_fp8_wrong_member_is_caught(monkeypatch):
     monkeypatch.setattr(ofp8, "block_bytes", member0)
     with pytest.raises(AssertionError):
         tf.test_gather_matches_dense_copy_and_base_reads_packed_member()
+
+
+# ---- metadata invariants ---------------------------------------------------
+
+from oracle import validate as ov
+from tests import test_oracle_validate as tv
+
+
+def test_validate_member1_tag_decides_is_caught(monkeypatch):
+    orig = ov.executed_as_base
+    monkeypatch.setattr(ov, "executed_as_base",
+                        lambda mode, by_range, b0, b1, j, t0, t1: orig(mode, by_range, b0, b1, j, t1, t0))
+    with pytest.raises(AssertionError):
+        tv.test_hand_built_batch_violations()
+
+
+def test_validate_off_by_one_full_pair_is_caught(monkeypatch):
+    monkeypatch.setattr(ov, "full_pair", lambda j, length, page: 2 * page * (j + 1) < length)
+    with pytest.raises(AssertionError):
+        tv.test_pairs_ending_at_the_length_are_full()
+
+
+def test_validate_last_instead_of_first_index_is_caught(monkeypatch):
+    def keep_last(self, kind, index):
+        self.counts[kind] += 1
+        self.first[kind] = index if self.first[kind] == ov.NONE else max(self.first[kind], index)
+    monkeypatch.setattr(ov._Report, "flag", keep_last)
+    with pytest.raises(AssertionError):
+        tv.test_hand_built_batch_violations()

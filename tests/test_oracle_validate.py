@@ -105,6 +105,20 @@ def test_hand_built_batch_violations():
     assert _found(*ov.batch_violations(lens, bt, None, b5, ov.STRUCTURED, nb)) == {ov.MODE: (1, 6)}
 
 
+def test_pairs_ending_at_the_length_are_full():
+    """Boundaries of 'two full blocks': a BASE pair ending exactly at the
+    sequence length is valid, one token short is not."""
+    nb = 30
+    bt = np.array([[10, 10, 12, 13]], dtype=np.int32)
+    tags = np.array([[1, 1, 0, 0]], dtype=np.uint8)
+    assert _found(*ov.batch_violations(np.array([32]), bt, tags, None, ov.GENERAL, nb)) == {}
+    assert _found(*ov.batch_violations(np.array([31]), bt, tags, None, ov.GENERAL, nb)) == {ov.BASE_PARTIAL: (1, 0)}
+    tg2 = np.zeros_like(tags)
+    assert _found(*ov.list_violations(0, [[0, 1]], np.array([[10, 11, 12, 13]]), tg2, nb, np.array([64]))) == {}
+    assert _found(*ov.list_violations(0, [[0, 1]], np.array([[10, 11, 12, 13]]), tg2, nb, np.array([63]))) == {
+        ov.LIST_PARTIAL: (1, 0)}
+
+
 def test_hand_built_list_violations():
     nb = 30
     bt, tags, lens, _ = _small()
