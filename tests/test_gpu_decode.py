@@ -20,8 +20,9 @@ from tests.gpu_util import check_attention, default_scale, host_safety_check, re
 pytestmark = pytest.mark.gpu
 
 
-def _run(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, min_chunk=None):
+def _run(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, min_chunk=None, scale=None):
     """Demote on both sides, decode on the GPU, compare everything."""
+    scale = default_scale() if scale is None else scale
     torch = require_gpu()
     dtype = case["dtype"]
     host_safety_check(case, case["pool"].shape)
@@ -52,8 +53,8 @@ def _run(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, 
         batch = kv.batch(hq, mode=mode, use_boundaries=use_boundaries)
         ws = ekv.decode_workspace(kv.pool, batch)
         print(f"decode: B={bsz} Hq={hq} Hkv={hkv} mode={mode} bounds={use_boundaries} "
-              f"min_chunk={min_chunk} fp32={out_fp32} {dtype}", flush=True)
-        ekv.attn_decode(kv.pool, batch, q, out, default_scale(), ws)
+              f"min_chunk={min_chunk} fp32={out_fp32} {dtype} scale={scale:.4f}", flush=True)
+        ekv.attn_decode(kv.pool, batch, q, out, scale, ws)
         torch.cuda.synchronize()
     finally:
         if min_chunk:
@@ -61,7 +62,7 @@ def _run(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, 
                 del os.environ["EKV_MIN_CHUNK"]
             else:
                 os.environ["EKV_MIN_CHUNK"] = old
-    ref = oatt.decode(case["q"], opool, obt, otg, case["seq_lens"], dtype)
+    ref = oatt.decode(case["q"], opool, obt, otg, case["seq_lens"], dtype, scale)
     got = out.float().cpu().numpy()
     return check_attention(got, ref, out_fp32), kv, opool, obt, otg
 
@@ -134,6 +135,15 @@ def test_dtypes_and_outputs(dtype, out_fp32):
     c = workloads.make_decode_case([200, 333, 32, 1024], 16, 4, dtype=dtype, seed=6, base_fraction=0.5,
                                    spare_blocks=2, outlier_channels=5)
     _run(c, 16, 4, out_fp32=out_fp32)
+
+
+@pytest.mark.parametrize("scale", [0.02, 0.3, -0.088])
+def test_decode_softmax_scales(scale):
+    """Other softmax scales, a negative one included (the kernels apply its
+    sign to Q): structured and general paths."""
+    c = workloads.make_decode_case([33, 700, 64, 1500], 16, 4, seed=44, base_fraction=0.5, spare_blocks=4)
+    _run(c, 16, 4, scale=scale)
+    _run(c, 16, 4, scale=scale, use_boundaries=False)
 
 
 def test_zero_length_and_single_token_sequences():

@@ -146,8 +146,9 @@ def test_append_e5m2_bit_exact():
     assert np.array_equal(dev.cpu().numpy(), ofp8.append(pool, slots, k, v))
 
 
-def _run_prefill(case, hq, hkv, *, use_boundaries=True, out_fp32=True):
+def _run_prefill(case, hq, hkv, *, use_boundaries=True, out_fp32=True, scale=None):
     torch = require_gpu()
+    scale = default_scale() if scale is None else scale
     host_safety_check(case, case["pool"].shape)
     assert (case["slots"] >= 0).all() and (case["slots"] < case["pool"].shape[0] * PAGE).all()
     kv = kvpool.PagedKV(case["pool"], case["block_table"], case["seq_lens"], case["free"], hkv, "e5m2")
@@ -166,9 +167,9 @@ def _run_prefill(case, hq, hkv, *, use_boundaries=True, out_fp32=True):
     print(f"prefill e5m2: B={len(case['seq_lens'])} Hq={hq} Hkv={hkv} rows={q.shape[0]} pairs={len(case['pairs'])} "
           f"boundaries={use_boundaries} fp32={out_fp32}", flush=True)
     ekv.attn_prefill(kv.pool, kv.batch(hq, use_boundaries=use_boundaries), q, torch.from_numpy(case["cu_q"]).cuda(),
-                     max_q, out, default_scale())
+                     max_q, out, scale)
     torch.cuda.synchronize()
-    ref = ofp8.prefill(case["q"], case["cu_q"], opool, obt, otg, case["seq_lens"])
+    ref = ofp8.prefill(case["q"], case["cu_q"], opool, obt, otg, case["seq_lens"], scale)
     return check_attention(out.float().cpu().numpy(), ref, out_fp32)
 
 
@@ -188,6 +189,16 @@ def test_prefill_e5m2_structured_general_and_fp16_output():
     _run_prefill(c, 32, 8)
     _run_prefill(c, 32, 8, use_boundaries=False)
     _run_prefill(c, 32, 8, out_fp32=False)
+
+
+@pytest.mark.parametrize("scale", [0.03, -0.1])
+def test_prefill_e5m2_empty_chunks_and_scales(scale):
+    """Empty chunks, an empty sequence and single-token chunks in one batch,
+    at other softmax scales (a negative one included)."""
+    c = workloads.make_prefill_case([100, 0, 300, 0, 64, 1], [20, 0, 0, 5, 33, 1], 8, 2, dtype="e5m2", seed=42,
+                                    base_fraction=0.5, spare_blocks=4)
+    _run_prefill(c, 8, 2, scale=scale)
+    _run_prefill(c, 8, 2, scale=scale, use_boundaries=False)
 
 
 def test_prefill_e5m2_chunks_at_8b_shape():

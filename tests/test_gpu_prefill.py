@@ -17,8 +17,9 @@ from tests.gpu_util import check_attention, default_scale, host_safety_check, re
 pytestmark = pytest.mark.gpu
 
 
-def _run_prefill(case, hq, hkv, *, out_fp32=True, use_boundaries=True):
+def _run_prefill(case, hq, hkv, *, out_fp32=True, use_boundaries=True, scale=None):
     torch = require_gpu()
+    scale = default_scale() if scale is None else scale
     dtype = case["dtype"]
     host_safety_check(case, case["pool"].shape)
     nb = case["pool"].shape[0]
@@ -44,9 +45,9 @@ def _run_prefill(case, hq, hkv, *, out_fp32=True, use_boundaries=True):
                      device="cuda")
     batch = kv.batch(hq, use_boundaries=use_boundaries)
     max_q = int(np.diff(case["cu_q"]).max())
-    ekv.attn_prefill(kv.pool, batch, q, cu, max_q, out, default_scale())
+    ekv.attn_prefill(kv.pool, batch, q, cu, max_q, out, scale)
     torch.cuda.synchronize()
-    ref = oatt.prefill(case["q"], case["cu_q"], opool, obt, otg, case["seq_lens"], dtype)
+    ref = oatt.prefill(case["q"], case["cu_q"], opool, obt, otg, case["seq_lens"], dtype, scale)
     return check_attention(out.float().cpu().numpy(), ref, out_fp32)
 
 
@@ -76,6 +77,17 @@ def test_prefill_structured_and_general_agree(prefix, chunk, fraction):
                                     placement="oldest", spare_blocks=2)
     _run_prefill(c, 32, 8)
     _run_prefill(c, 32, 8, use_boundaries=False)
+
+
+@pytest.mark.parametrize("scale", [0.03, -0.1])
+def test_prefill_empty_chunks_and_scales(scale):
+    """A batch mixing empty chunks (a 300-token prefix with no new token), an
+    empty sequence, single-token chunks and a first chunk with no prefix, at
+    other softmax scales, a negative one included."""
+    c = workloads.make_prefill_case([100, 0, 300, 0, 64, 1], [20, 0, 0, 5, 33, 1], 8, 2, seed=41,
+                                    base_fraction=0.5, spare_blocks=4)
+    _run_prefill(c, 8, 2, scale=scale)
+    _run_prefill(c, 8, 2, scale=scale, use_boundaries=False)
 
 
 def test_prefill_llama3_8b_chunk_full_size():
