@@ -242,7 +242,8 @@ def make_decode_case_torch(seq_lens, num_q_heads, num_kv_heads, *, seed, outlier
 
 def extract_sequences(pool_dev, block_table, seq_lens, seq_ids):
     """Host copy of just the blocks of ``seq_ids``, renumbered densely:
-    returns (pool uint16 [n][2][Hkv][16][128], block_table, seq_lens)."""
+    returns (pool [n][2][Hkv][16][128] of uint16 words, or uint8 bytes for a
+    1-byte pool, block_table, seq_lens)."""
     import torch
     page = PAGE
     blocks = []
@@ -252,5 +253,8 @@ def extract_sequences(pool_dev, block_table, seq_lens, seq_ids):
         bt[r, :nblk] = np.arange(len(blocks), len(blocks) + nblk)
         blocks.extend(int(b) for b in block_table[s, :nblk])
     idx = torch.as_tensor(np.array(blocks, dtype=np.int64), device=pool_dev.device)
-    host = pool_dev.index_select(0, idx).cpu().numpy().view(np.uint16)
+    if pool_dev.element_size() == 1:
+        host = pool_dev.view(torch.uint8).index_select(0, idx).cpu().numpy()
+    else:
+        host = pool_dev.index_select(0, idx).cpu().numpy().view(np.uint16)
     return host, bt, np.asarray(seq_lens, dtype=np.int32)[list(seq_ids)]

@@ -207,3 +207,50 @@ def test_prefill_e5m2_chunks_at_8b_shape():
     c = workloads.make_prefill_case([1024] * 4, [256] * 4, 32, 8, dtype="e5m2", seed=98, base_fraction=0.5,
                                     spare_blocks=2)
     _run_prefill(c, 32, 8, out_fp32=False)
+
+
+@pytest.mark.parametrize("fraction", [0.0, 0.5, 1.0])
+def test_decode_e5m2_8b_full_size_sampled(fraction):
+    """The 8B decode layer over an 8-bit pool as the benchmark runs it (64
+    sequences, context uniform in [2048, 8192], 1 % outlier channels, random
+    BASE pairs): sampled sequences against the oracle, FP16 and FP32 output."""
+    torch = require_gpu()
+    seq_lens = workloads.seq_lens_uniform(np.random.default_rng(1), 64, 2048, 8192)
+    case = workloads.make_decode_case_torch(seq_lens, 32, 8, seed=6, outlier_channels=10, spare_blocks=64,
+                                            dtype="e5m2")
+    k = [0.0, 0.5, 1.0].index(fraction)
+    pairs = workloads.choose_pairs(np.random.default_rng(2000 + k), seq_lens, fraction, "random")
+    kv = kvpool.PagedKV(case["pool"].clone(), case["block_table"], seq_lens, case["free"], 8, "e5m2")
+    if len(pairs):
+        kv.demote(pairs, emit_lo=False)
+        kv.commit()
+    mode = kv.relower()
+    print(f"8-bit 8b decode f={fraction}: pairs={len(pairs)} mode={mode}", flush=True)
+    batch = kv.batch(32)
+    ws = ekv.decode_workspace(kv.pool, batch)
+    sample = [0, 9, 22, 40, 63]
+    host, sbt, slens = workloads.extract_sequences(case["pool"], case["block_table"], seq_lens, sample)
+    rows = {s: r for r, s in enumerate(sample)}
+    sp = np.array([(rows[int(s)], int(j)) for s, j in pairs if int(s) in rows], dtype=np.int32).reshape(-1, 2)
+    tg = np.zeros(sbt.shape, dtype=np.uint8)
+    if len(sp):
+        host, sbt, tg, _, _ = ofp8.demote(host, sbt, tg, sp, slens)
+    q_words = case["q"].view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = ofp8.decode(q_words[sample], host, sbt, tg, slens)
+    for out_dtype in (torch.float16, torch.float32):
+        out = torch.full((64, 32, 128), float("nan"), dtype=out_dtype, device="cuda")
+        ekv.attn_decode(kv.pool, batch, case["q"], out, default_scale(), ws)
+        torch.cuda.synchronize()
+        got = out.float().cpu().numpy()
+        assert np.isfinite(got).all()
+        err, _ = check_attention(got[sample], ref, out_dtype == torch.float32)
+        print(f"  {out_dtype}: max abs err {err:.3e} on {len(sample)} sequences", flush=True)
+
+
+def test_prefill_e5m2_8b_full_size():
+    """The chunked-prefill workload over an 8-bit pool as the benchmark runs
+    it: 16 x (2048-token prefix, half its pairs BASE, + 512-token chunk), 32
+    query / 8 KV heads; every output checked."""
+    c = workloads.make_prefill_case([2048] * 16, [512] * 16, 32, 8, dtype="e5m2", seed=3, base_fraction=0.5,
+                                    spare_blocks=2)
+    _run_prefill(c, 32, 8, out_fp32=False)
