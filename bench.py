@@ -655,8 +655,9 @@ def transitions_all_layers(torch, ekv, stream, layers=32, pairs=TRANSITION_PAIRS
 def controller_cost(ekv, mirror, reps=200):
     """Host time of one control step (ekv_ctrl_demotion + ekv_ctrl_promotion,
     Alg. 1) over the 8B workload's host mirror at f=0.5: a shortage of 2
-    blocks (so B_min = 16 pairs are demoted) and a promotion budget of 16.
-    Arrays are marshalled once; the figure is the library's own work."""
+    blocks (so B_min = 16 pairs are demoted) and a promotion budget of 16;
+    and of the dispatch-metadata lowering (ekv_lower) of that mirror.
+    Arrays are marshalled once; the figures are the library's own work."""
     import ctypes
     cfg = ekv.ctrl_config(min_batch=16, decay=2, sink_pairs=1, recent_pairs=2)
     tags = np.ascontiguousarray(mirror.tags, dtype=np.uint8)
@@ -675,8 +676,17 @@ def controller_cost(ekv, mirror, reps=200):
         lib.ekv_ctrl_promotion(ctypes.byref(cfg), ctypes.byref(st), st.surplus + 16, 64, tp, lp, bsz,
                                max_blocks, PAGE, op, cap, ctypes.byref(n_p))
     us = (time.perf_counter() - t0) * 1e6 / reps
+    # the dispatch-metadata lowering of the same mirror (ekv_lower: mode and boundaries)
+    bounds = np.zeros((bsz, 2), dtype=np.int32)
+    bp = bounds.ctypes.data_as(ctypes.c_void_p)
+    mode = ctypes.c_int32(-1)
+    t0 = time.perf_counter()
+    for _ in range(reps):
+        lib.ekv_lower(tp, lp, bsz, max_blocks, PAGE, ctypes.byref(mode), bp)
+    lower_us = (time.perf_counter() - t0) * 1e6 / reps
     return {"host_us_per_step": round(us, 1), "demoted_pairs": n_d.value, "promoted_pairs": n_p.value,
-            "sequences": int(bsz), "note": "shortage 2 blocks, B_min 16, lambda 2, budget 16"}
+            "sequences": int(bsz), "lowering_us_per_step": round(lower_us, 2),
+            "note": "shortage 2 blocks, B_min 16, lambda 2, budget 16; lowering = ekv_lower of the same mirror"}
 
 
 def cpu_baseline(dec, outs, pf):

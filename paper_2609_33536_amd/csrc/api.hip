@@ -242,7 +242,23 @@ ekv_status ekv_lower(const uint8_t* h_tags, const int32_t* h_seq_lens, int32_t b
     const int nblk = (len + page_size - 1) / page_size;
     const uint8_t* row = h_tags + (size_t)s * max_blocks;
     int first = -1, last = -1, count = 0;
-    for (int j = 0; 2 * j < nblk; ++j) {
+    int j = 0;
+    // four full pairs (8 tag bytes) per step: every byte 0 or 1, the two
+    // bytes of each pair equal, and member 0's low bit marks a BASE pair;
+    // a word that fails a test is redone byte by byte below for the message
+    for (; 2 * j + 8 <= nblk; j += 4) {
+      uint64_t w;
+      std::memcpy(&w, row + 2 * j, 8);
+      if ((w & 0xFEFEFEFEFEFEFEFEull) || ((w ^ (w >> 8)) & 0x00FF00FF00FF00FFull)) break;
+      const uint64_t m = w & 0x0001000100010001ull;   // bit 16k: pair j + k is BASE
+      // selects, not branches: the BASE pattern is data and mispredicts
+      const int lo = j + __builtin_ctzll(m | (1ull << 63)) / 16;
+      const int hi = j + (63 - __builtin_clzll(m | 1ull)) / 16;
+      first = (first < 0 && m) ? lo : first;
+      last = m ? hi : last;
+      count += __builtin_popcountll(m);
+    }
+    for (; 2 * j < nblk; ++j) {
       const uint8_t a = row[2 * j];
       const uint8_t b = (2 * j + 1 < nblk) ? row[2 * j + 1] : a;
       if (a > 1 || b > 1) return fail(EKV_ERR_INVALID, "ekv_lower: tag value out of range");

@@ -56,6 +56,43 @@ def test_lower_matches_oracle(rows):
     assert np.array_equal(bounds, obounds)
 
 
+@settings(max_examples=300, deadline=None)
+@given(st.integers(0, 2**31 - 1), st.integers(1, 6), st.sampled_from([0.0, 0.02, 0.5, 0.98, 1.0]),
+       st.integers(0, 3))
+def test_lower_long_rows_match_oracle(seed, bsz, p_base, planted):
+    """Rows of 96 blocks (the library scans four pairs at a time): random and
+    clustered BASE pairs, lengths anywhere in the row, and now and then a
+    planted bad tag value or mixed pair, which both sides must reject."""
+    rng = np.random.default_rng(seed)
+    max_blocks = 96
+    lens = rng.integers(0, max_blocks * 16 + 1, size=bsz).astype(np.int32)
+    tags = np.zeros((bsz, max_blocks), dtype=np.uint8)
+    for s in range(bsz):
+        if rng.random() < 0.5:
+            pair = (rng.random(max_blocks // 2) < p_base).astype(np.uint8)
+        else:
+            a, b = sorted(rng.integers(0, max_blocks // 2 + 1, size=2))
+            pair = np.zeros(max_blocks // 2, dtype=np.uint8)
+            pair[a:b] = 1
+        tags[s] = np.repeat(pair, 2)
+    for _ in range(planted):
+        s, i = int(rng.integers(0, bsz)), int(rng.integers(0, max_blocks))
+        tags[s, i] = int(rng.integers(0, 3))
+    # the library also refuses a visible tag value above 1 (the oracle reads any nonzero tag as BASE)
+    bad_value = any((tags[s, :-(-int(lens[s]) // 16)] > 1).any() for s in range(bsz))
+    try:
+        omode, obounds = olow.lower(tags, lens, 16)
+    except olow.InvalidTags:
+        bad_value = True
+    if bad_value:
+        with pytest.raises(ekv.EkvError):
+            ekv.lower(tags, lens)
+        return
+    mode, bounds = ekv.lower(tags, lens)
+    assert mode == omode
+    assert np.array_equal(bounds, obounds)
+
+
 def test_lower_rejects_mixed_pair():
     tags = np.zeros((1, 4), dtype=np.uint8)
     tags[0, 0] = 1
