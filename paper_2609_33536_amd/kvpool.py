@@ -44,11 +44,11 @@ class HostMirror:
         (not yet back in the free pool)."""
         pairs = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
         self._validate(0, pairs)
-        freed = np.empty(len(pairs), dtype=np.int32)
-        for i, (s, j) in enumerate(pairs):
-            freed[i] = self.bt[s, 2 * j + 1]
-            self.bt[s, 2 * j + 1] = self.bt[s, 2 * j]
-            self.tags[s, 2 * j] = self.tags[s, 2 * j + 1] = 1
+        s, j = pairs[:, 0], pairs[:, 1]   # distinct pairs (validated): one write per entry
+        freed = self.bt[s, 2 * j + 1].copy()
+        self.bt[s, 2 * j + 1] = self.bt[s, 2 * j]
+        self.tags[s, 2 * j] = 1
+        self.tags[s, 2 * j + 1] = 1
         return freed
 
     def commit_freed(self, freed):
@@ -64,30 +64,33 @@ class HostMirror:
         if n > len(self.free):
             raise ekv.EkvError(ekv.ERR_INVALID, "not enough free blocks for refinement")
         new = np.array([self.free.popleft() for _ in range(n)], dtype=np.int32)
+        keys = list(zip(pairs[:, 0].tolist(), pairs[:, 1].tolist()))
         try:
             self._validate(1, pairs, new)
-            for s, j in pairs:
-                if (int(s), int(j)) in self.reserved:
-                    raise ekv.EkvError(ekv.ERR_INVALID, f"pair ({s},{j}) is already being promoted")
+            busy = [k for k in keys if k in self.reserved]
+            if busy:
+                raise ekv.EkvError(ekv.ERR_INVALID, f"pair {busy[0]} is already being promoted")
         except ekv.EkvError:
             self.free.extendleft(reversed(new.tolist()))
             raise
-        self.reserved.update((int(s), int(j)) for s, j in pairs)
+        self.reserved.update(keys)
         return new
 
     def cancel_refine(self, pairs, new):
         """Undo :meth:`reserve_refine`: the blocks go back to the head of the
         free pool in their order and the pairs are no longer reserved."""
         self.free.extendleft(reversed(np.asarray(new, dtype=np.int32).tolist()))
-        for s, j in np.asarray(pairs, dtype=np.int32).reshape(-1, 2):
-            self.reserved.discard((int(s), int(j)))
+        p = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
+        self.reserved.difference_update(zip(p[:, 0].tolist(), p[:, 1].tolist()))
 
     def publish_refine(self, pairs, new):
         """Apply the table update of a refinement (after its device work)."""
-        for i, (s, j) in enumerate(np.asarray(pairs, dtype=np.int32).reshape(-1, 2)):
-            self.bt[s, 2 * j + 1] = new[i]
-            self.tags[s, 2 * j] = self.tags[s, 2 * j + 1] = 0
-            self.reserved.discard((int(s), int(j)))
+        p = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
+        s, j = p[:, 0], p[:, 1]   # distinct pairs (validated at reservation)
+        self.bt[s, 2 * j + 1] = np.asarray(new, dtype=np.int32)
+        self.tags[s, 2 * j] = 0
+        self.tags[s, 2 * j + 1] = 0
+        self.reserved.difference_update(zip(s.tolist(), j.tolist()))
 
     def plan_refine(self, pairs):
         """Validate a refinement list, take one block per pair from the free
@@ -227,8 +230,8 @@ class AsyncPromotion:
             lo.record_stream(self.copy)
         done = torch.cuda.Event()
         done.record(self.copy)
-        for i, (s, j) in enumerate(pairs):
-            self.backing[(int(s), int(j))] = (host[i], done)
+        for key, row in zip(zip(pairs[:, 0].tolist(), pairs[:, 1].tolist()), host.unbind(0)):
+            self.backing[key] = (row, done)
         return freed, host_freed
 
     def promote(self, pairs):
@@ -236,11 +239,11 @@ class AsyncPromotion:
         returns the reserved blocks.  The pairs stay BASE until published."""
         import torch
         pairs = np.asarray(pairs, dtype=np.int32).reshape(-1, 2)
-        missing = [(int(s), int(j)) for s, j in pairs if (int(s), int(j)) not in self.backing]
+        keys = list(zip(pairs[:, 0].tolist(), pairs[:, 1].tolist()))
+        missing = [k for k in keys if k not in self.backing]
         if missing:
             raise ekv.EkvError(ekv.ERR_INVALID, f"no CPU backing for pairs {missing[:4]}")
         new = self.kv.mirror.reserve_refine(pairs)
-        keys = [(int(s), int(j)) for s, j in pairs]
         sources = [self.backing[k][0] for k in keys]
         for done in {id(self.backing[k][1]): self.backing[k][1] for k in keys}.values():
             self.copy.wait_event(done)
