@@ -270,6 +270,36 @@ __device__ __forceinline__ u32x2 expand4(uint32_t w) {
   return u32x2{perm(odd, even, 0x05010400u), perm(odd, even, 0x07030602u)};
 }
 
+// The same 4 bytes of nibbles as two byte planes, each nibble in the high
+// half of its byte: byte k of `even` holds element 2k, of `odd` element 2k+1.
+struct NibPlanes {
+  uint32_t even, odd;
+};
+__device__ __forceinline__ NibPlanes nib_planes(uint32_t w) { return {(w << 4) & 0xF0F0F0F0u, w & 0xF0F0F0F0u}; }
+
+// Byte selector that places byte k of the second source in the high byte
+// of the low half and byte k of the first source in the high byte of the
+// high half, with zero low bytes (two executed BASE words).
+__device__ __forceinline__ constexpr uint32_t word_pair_sel(int k) {
+  return 0x0Cu | ((uint32_t)k << 8) | (0x0Cu << 16) | ((uint32_t)(4 + k) << 24);
+}
+
+// 8 nibble elements straight to 16-bit words (the QK^T operand of BASE K):
+// word k holds elements 2k, 2k+1.
+__device__ __forceinline__ u32x4 nib_words(uint32_t w) {
+  const NibPlanes p = nib_planes(w);
+  return u32x4{perm(p.odd, p.even, word_pair_sel(0)), perm(p.odd, p.even, word_pair_sel(1)),
+               perm(p.odd, p.even, word_pair_sel(2)), perm(p.odd, p.even, word_pair_sel(3))};
+}
+
+// PV A operand j of BASE V straight from the planes of the lane's 4 tokens:
+// element j of tokens 0 and 1, then of tokens 2 and 3, as 16-bit words.
+__device__ __forceinline__ u32x2 nib_v_operand(const NibPlanes (&p)[4], int j) {
+  const uint32_t sel = word_pair_sel(j >> 1);
+  if (j & 1) return u32x2{perm(p[1].odd, p[0].odd, sel), perm(p[3].odd, p[2].odd, sel)};
+  return u32x2{perm(p[1].even, p[0].even, sel), perm(p[3].even, p[2].even, sel)};
+}
+
 __device__ __forceinline__ int wave_sum_int(int x) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) x += __shfl_xor(x, off);
@@ -700,18 +730,29 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       const char* ring0 = &sm.ring[0][0];
       const char* kb = ring0 + kUnit * cslot;
       const char* vb = ring0 + kUnit * (cslot + 1 == 2 * NSLOT ? 0 : cslot + 1);
-      u32x4 k[2][4], v[2][4];
       f32x4 sc[2];
+      u32x2 vop[2][8];
+      if (base) {
+        // nibbles straight to 16-bit operand words (a BASE pair is two full
+        // blocks: no tail to clear)
 #pragma unroll
-      for (int m = 0; m < 2; ++m) {
-        if (base) {
+        for (int m = 0; m < 2; ++m) {
           const char* mb = kb + m * (kTileBytes / 4);
           const u32x4 kn = *reinterpret_cast<const u32x4*>(mb + rk4);
+          u32x4 kw[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) k[m][q].xy = expand4(kn[q]);
+          for (int q = 0; q < 4; ++q) kw[q] = nib_words(kn[q]);
+          sc[m] = qk_scores<T, false>(kw, qop);
+          NibPlanes pv[4];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) v[m][i].xy = expand4(*reinterpret_cast<const uint32_t*>(mb + kTileBytes / 2 + rv4[i]));
-        } else {
+          for (int i = 0; i < 4; ++i) pv[i] = nib_planes(*reinterpret_cast<const uint32_t*>(mb + kTileBytes / 2 + rv4[i]));
+#pragma unroll
+          for (int j = 0; j < 8; ++j) vop[m][j] = nib_v_operand(pv, j);
+        }
+      } else {
+        u32x4 k[2][4], v[2][4];
+#pragma unroll
+        for (int m = 0; m < 2; ++m) {
           const char* mb = kb + m * (kTileBytes / 2);
           const u32x4 k0 = *reinterpret_cast<const u32x4*>(mb + rk_b[0]);
           const u32x4 k1 = *reinterpret_cast<const u32x4*>(mb + rk_b[1]);
@@ -722,13 +763,12 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
           const char* mv = vb + m * (kTileBytes / 2) - kTileBytes;   // rv_b counts from the K tile
 #pragma unroll
           for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mv + rv_b[i]);
+          sc[m] = qk_scores<T, true>(k[m], qop);
         }
-        sc[m] = qk_scores<T, true>(k[m], qop);
+        zero_tail_v<2>(v, cb * kPage, ccur.len, g);
+        v_operands<true, 2>(v, vop);
       }
       const bool tail = cb * kPage + 2 * kPage > ccur.len;
-      zero_tail_v<2>(v, cb * kPage, ccur.len, g);
-      u32x2 vop[2][8];
-      v_operands<true, 2>(v, vop);
       if constexpr (kStack) softmax_pv_stacked<T, 2, G>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g, n);
       else softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
       cb += lone ? 1 : 2;
