@@ -51,8 +51,8 @@
  *     append slots and transition-list entries that point outside the pool
  *     or the table are skipped (a skipped demotion reports freed_out[i] =
  *     -1).  Results for invalid lists are otherwise undefined.
- *   - Supported: head_dim 128, page_size 16, dtype bf16 or fp16,
- *     num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}.  Other shapes return
+ *   - Supported: head_dim 128, page_size 16, dtype bf16, fp16 or e5m2 (the
+ *     8-bit pools below), num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}.  Other shapes return
  *     EKV_ERR_UNSUPPORTED.
  *   - ekv_last_error() returns a text describing the last failure on the
  *     calling thread.
