@@ -1,0 +1,82 @@
+"""Decode and chunked prefill under HIP graph capture.
+
+A serving loop replays one captured graph per step.  The library's launches
+enqueue kernels only (no memset, no allocation, no host synchronisation;
+the decode's merge counters reset themselves), so they can be captured.
+Each replay here gets new query values in the captured input buffer, with
+the program's own eager launches and synchronisations in between, and must
+equal an eager call on the same inputs bit for bit (the work partition and
+the merge order do not depend on timing)."""
+
+import numpy as np
+import pytest
+
+from paper_2609_33536_amd import ekv, kvpool, workloads
+from tests.gpu_util import default_scale, require_gpu, words_to_tensor
+
+pytestmark = pytest.mark.gpu
+
+
+def test_decode_and_prefill_replay_from_a_graph():
+    torch = require_gpu()
+    rng = np.random.default_rng(61)
+    # decode: mixed pool, general mode, several pieces per (sequence, head)
+    c = workloads.make_decode_case([300, 1500, 64, 2047, 700], 16, 4, seed=61, base_fraction=0.5,
+                                   spare_blocks=4)
+    kv = kvpool.PagedKV(c["pool"], c["block_table"], c["seq_lens"], c["free"], 4)
+    kv.demote(c["pairs"])
+    kv.commit()
+    kv.relower()
+    batch = kv.batch(16)
+    ws = ekv.decode_workspace(kv.pool, batch)
+    q = words_to_tensor(c["q"], torch, "bf16").clone()
+    out = torch.empty((5, 16, 128), dtype=torch.float32, device="cuda")
+    # prefill over its own pool
+    p = workloads.make_prefill_case([100, 900, 0], [40, 77, 12], 16, 4, seed=62, base_fraction=0.5,
+                                    spare_blocks=4)
+    pkv = kvpool.PagedKV(p["pool"], p["block_table"], p["seq_lens"], p["free"], 4)
+    pkv.append(torch.from_numpy(p["slots"]).cuda(), words_to_tensor(p["k_new"], torch, "bf16"),
+               words_to_tensor(p["v_new"], torch, "bf16"))
+    if len(p["pairs"]):
+        pkv.demote(p["pairs"])
+        pkv.commit()
+    pkv.relower()
+    pbatch = pkv.batch(16)
+    pq = words_to_tensor(p["q"], torch, "bf16").clone()
+    cu = torch.from_numpy(p["cu_q"]).cuda()
+    pout = torch.empty((pq.shape[0], 16, 128), dtype=torch.float32, device="cuda")
+    max_q = int(np.diff(p["cu_q"]).max())
+    scale = default_scale()
+
+    def step():
+        ekv.attn_decode(kv.pool, batch, q, out, scale, ws)
+        ekv.attn_prefill(pkv.pool, pbatch, pq, cu, max_q, pout, scale)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):   # warm up off the capture (first-call set-up)
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    print("graph: capturing decode + prefill", flush=True)
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    for replay in range(4):
+        q.copy_(words_to_tensor(workloads.to_words(rng.standard_normal(q.shape, dtype=np.float32), "bf16"),
+                                torch, "bf16"))
+        pq.copy_(words_to_tensor(workloads.to_words(rng.standard_normal(pq.shape, dtype=np.float32), "bf16"),
+                                 torch, "bf16"))
+        torch.cuda.synchronize()
+        print(f"graph: replay {replay}", flush=True)
+        graph.replay()
+        torch.cuda.synchronize()
+        got, pgot = out.clone(), pout.clone()
+        out.fill_(float("nan"))
+        pout.fill_(float("nan"))
+        step()   # the same launches, eager
+        torch.cuda.synchronize()
+        assert torch.equal(got, out), f"decode replay {replay} differs from the eager call"
+        assert torch.equal(pgot, pout), f"prefill replay {replay} differs from the eager call"
+        assert torch.isfinite(got).all() and torch.isfinite(pgot).all()
