@@ -1,4 +1,4 @@
-"""Decode and chunked prefill under HIP graph capture.
+"""Decode, chunked prefill and the transitions under HIP graph capture.
 
 A serving loop replays one captured graph per step.  The library's launches
 enqueue kernels only (no memset, no allocation, no host synchronisation;
@@ -80,3 +80,47 @@ def test_decode_and_prefill_replay_from_a_graph():
         assert torch.equal(got, out), f"decode replay {replay} differs from the eager call"
         assert torch.equal(pgot, pout), f"prefill replay {replay} differs from the eager call"
         assert torch.isfinite(got).all() and torch.isfinite(pgot).all()
+
+
+def test_demote_refine_round_trip_replays_from_a_graph():
+    """A demotion and the refinement that undoes it (its freed blocks as the
+    new blocks, its refinement bytes as the input) in one graph: the
+    refinement reads the demotion's device outputs inside the graph, and
+    every replay leaves pool, table and tags exactly as they were."""
+    torch = require_gpu()
+    c = workloads.make_decode_case([300, 1500, 64, 2047, 700], 16, 4, seed=63, base_fraction=0.5,
+                                   spare_blocks=4)
+    dev = torch.from_numpy(c["pool"].view(np.int16).copy()).cuda()
+    pool = ekv.make_pool(dev, 4, "bf16")
+    bt = torch.from_numpy(c["block_table"].copy()).cuda()
+    tags = torch.from_numpy(c["tags"].copy()).cuda()
+    pairs = torch.from_numpy(c["pairs"].copy()).cuda()
+    n = pairs.shape[0]
+    assert n > 0
+    freed = torch.empty(n, dtype=torch.int32, device="cuda")
+    lo = torch.empty((n, 2 * 4 * 16 * 128 * 2), dtype=torch.uint8, device="cuda")
+
+    def round_trip():
+        ekv.demote(pool, pairs, bt, tags, freed, lo)
+        ekv.refine(pool, pairs, freed, bt, tags, lo)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        round_trip()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    assert np.array_equal(dev.cpu().numpy().view(np.uint16), c["pool"])
+    graph = torch.cuda.CUDAGraph()
+    print(f"graph: capturing demote + refine of {n} pairs", flush=True)
+    with torch.cuda.graph(graph):
+        round_trip()
+    for replay in range(3):
+        print(f"graph: replay {replay}", flush=True)
+        graph.replay()
+        torch.cuda.synchronize()
+        assert np.array_equal(dev.cpu().numpy().view(np.uint16), c["pool"]), replay
+        assert np.array_equal(bt.cpu().numpy(), c["block_table"]), replay
+        assert np.array_equal(tags.cpu().numpy(), c["tags"]), replay
+        assert np.array_equal(np.sort(freed.cpu().numpy()), np.sort(c["block_table"][c["pairs"][:, 0],
+                                                                                     2 * c["pairs"][:, 1] + 1]))
