@@ -108,17 +108,21 @@ __device__ __forceinline__ u32x2 widen_nibbles(uint32_t w) {
   return u32x2{perm(odd, even, 0x05010400u), perm(odd, even, 0x07030602u)};
 }
 
-// max of three floats in one instruction (finite or -inf inputs)
-__device__ __forceinline__ float max3(float a, float b, float c) {
-  float r;
-  asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
-  return r;
-}
+// max of three floats.  Written for the compiler, not as inline assembly:
+// its operands come straight from the matrix cores, and only the compiler
+// inserts the wait states a vector instruction needs before it may read an
+// MFMA result (inline assembly would read the registers while the products
+// are still being written).
+__device__ __forceinline__ float max3(float a, float b, float c) { return __builtin_fmaxf(__builtin_fmaxf(a, b), c); }
 
 // v *= f in v's own registers.  The rescale of the output accumulators is a
 // rare branch; multiplying in place keeps the accumulators in the same
 // registers on both sides of it, where a plain multiply lets the compiler
-// give the result new registers and copy all 64 on the common path.
+// give the result new registers and copy all 64 on the common path.  The
+// compiler cannot add the wait states an MFMA result needs before this
+// assembly reads it; it runs only after compiler code has read the unit's
+// S^T products (which waits for them), and a wave's products complete in
+// order, so the PV products into v have completed by then.
 __device__ __forceinline__ void scale_in_place(f32x16& v, float f) {
 #pragma unroll
   for (int i = 0; i < 16; ++i) {

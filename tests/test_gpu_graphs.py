@@ -124,3 +124,56 @@ def test_demote_refine_round_trip_replays_from_a_graph():
         assert np.array_equal(tags.cpu().numpy(), c["tags"]), replay
         assert np.array_equal(np.sort(freed.cpu().numpy()), np.sort(c["block_table"][c["pairs"][:, 0],
                                                                                      2 * c["pairs"][:, 1] + 1]))
+
+
+def test_concurrent_calls_on_two_streams():
+    """Two decodes (each with its own workspace) and a prefill on three
+    streams at the default priority, enqueued back to back with no ordering
+    between them: each result equals the same call run alone."""
+    torch = require_gpu()
+    cases = [workloads.make_decode_case([1200, 64, 2047, 700, 333], 16, 4, seed=70 + i, base_fraction=f,
+                                        spare_blocks=4) for i, f in enumerate((0.5, 1.0))]
+    runs = []
+    for c in cases:
+        kv = kvpool.PagedKV(c["pool"], c["block_table"], c["seq_lens"], c["free"], 4)
+        kv.demote(c["pairs"])
+        kv.commit()
+        kv.relower()
+        batch = kv.batch(16)
+        runs.append((kv, batch, ekv.decode_workspace(kv.pool, batch), words_to_tensor(c["q"], torch, "bf16")))
+    p = workloads.make_prefill_case([100, 900, 50], [40, 77, 12], 16, 4, seed=72, base_fraction=0.5,
+                                    spare_blocks=4)
+    pkv = kvpool.PagedKV(p["pool"], p["block_table"], p["seq_lens"], p["free"], 4)
+    pkv.append(torch.from_numpy(p["slots"]).cuda(), words_to_tensor(p["k_new"], torch, "bf16"),
+               words_to_tensor(p["v_new"], torch, "bf16"))
+    pkv.demote(p["pairs"])
+    pkv.commit()
+    pkv.relower()
+    pbatch, pq, cu = pkv.batch(16), words_to_tensor(p["q"], torch, "bf16"), torch.from_numpy(p["cu_q"]).cuda()
+    max_q, scale = int(np.diff(p["cu_q"]).max()), default_scale()
+    torch.cuda.synchronize()
+
+    def launch(k, out, stream):
+        if k < 2:
+            kv, batch, ws, q = runs[k]
+            ekv.attn_decode(kv.pool, batch, q, out, scale, ws, stream)
+        else:
+            ekv.attn_prefill(pkv.pool, pbatch, pq, cu, max_q, out, scale, stream)
+
+    shapes = [(5, 16, 128), (5, 16, 128), (pq.shape[0], 16, 128)]
+    alone = []
+    for k in range(3):
+        out = torch.full(shapes[k], float("nan"), dtype=torch.float32, device="cuda")
+        launch(k, out, torch.cuda.current_stream())
+        torch.cuda.synchronize()
+        alone.append(out)
+    streams = [torch.cuda.Stream() for _ in range(3)]
+    for rep in range(3):
+        outs = [torch.full(s, float("nan"), dtype=torch.float32, device="cuda") for s in shapes]
+        torch.cuda.synchronize()
+        print(f"streams: concurrent round {rep}", flush=True)
+        for k in range(3):
+            launch(k, outs[k], streams[k])
+        torch.cuda.synchronize()
+        for k in range(3):
+            assert torch.equal(outs[k], alone[k]), (rep, k)
