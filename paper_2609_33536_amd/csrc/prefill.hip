@@ -385,6 +385,53 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
 #pragma unroll
         for (int k = 0; k < 8; ++k) sc = Mma32<T>::mma(kop[k], qop[k], sc);
 
+        // V^T operands of key step ks (16 keys); step 0 is fetched before the
+        // softmax, so its LDS reads overlap the wait for the S^T products
+        struct VOps {
+          u32x4 t[4];
+        };
+        auto fetch_v = [&](int ks) -> VOps {
+          VOps r;
+          if (F8 || (ELASTIC && base)) {
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              const i32x2v raw =
+                  __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2)(sa + ks * (kTileBytes / 2) + (off_vb ^ (32 * t))));
+              r.t[t] = expand_base8(u32x2{(uint32_t)raw[0], (uint32_t)raw[1]});
+              if (F8 && kMasked) {   // 8-bit TARGET keys at or past the sequence end: zero V
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                  const int key = 16 * ks + 8 * (e >> 2) + 4 * h + (e & 3);
+                  if (key0 + key >= len) r.t[t][e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+                }
+              }
+            }
+          } else {
+            const char* sl = ks == 0 ? sa : sbk;
+#pragma unroll
+            for (int t = 0; t < 4; ++t) {
+              uint32_t w[4];
+#pragma unroll
+              for (int half = 0; half < 2; ++half) {
+                const u32x2 pr = __builtin_bit_cast(
+                    u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4)(sl + (off_vt[half] ^ (64 * t)))));
+                w[2 * half] = pr.x;
+                w[2 * half + 1] = pr.y;
+              }
+              if (kMasked) {   // keys at or past the sequence end: zero V (their slots hold anything)
+#pragma unroll
+                for (int e = 0; e < 8; ++e) {
+                  const int key = 16 * ks + 8 * (e >> 2) + 4 * h + (e & 3);
+                  if (key0 + key >= len) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
+                }
+              }
+              r.t[t] = u32x4{w[0], w[1], w[2], w[3]};
+            }
+          }
+          return r;
+        };
+        const VOps v0 = fetch_v(0);
+
         // ---- online softmax over this lane's 16 keys (+ lane ^ 32) ----
         if constexpr (kMasked) {
 #pragma unroll
@@ -431,47 +478,11 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
 #pragma unroll
         for (int ks = 0; ks < 2; ++ks) {
           if (kMasked && ks == 1 && nkeys < 32) break;
-          u32x4 vop[4];
-          if (F8 || (ELASTIC && base)) {
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              const i32x2v raw =
-                  __builtin_amdgcn_ds_read_tr8_b64_v2i32((lds_i32x2)(sa + ks * (kTileBytes / 2) + (off_vb ^ (32 * t))));
-              vop[t] = expand_base8(u32x2{(uint32_t)raw[0], (uint32_t)raw[1]});
-              if (F8 && kMasked) {   // 8-bit TARGET keys at or past the sequence end: zero V
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  const int key = 16 * ks + 8 * (e >> 2) + 4 * h + (e & 3);
-                  if (key0 + key >= len) vop[t][e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-                }
-              }
-            }
-          } else {
-            const char* sl = ks == 0 ? sa : sbk;
-#pragma unroll
-            for (int t = 0; t < 4; ++t) {
-              uint32_t w[4];
-#pragma unroll
-              for (int half = 0; half < 2; ++half) {
-                const u32x2 pr = __builtin_bit_cast(
-                    u32x2, __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_i16x4)(sl + (off_vt[half] ^ (64 * t)))));
-                w[2 * half] = pr.x;
-                w[2 * half + 1] = pr.y;
-              }
-              if (kMasked) {   // keys at or past the sequence end: zero V (their slots hold anything)
-#pragma unroll
-                for (int e = 0; e < 8; ++e) {
-                  const int key = 16 * ks + 8 * (e >> 2) + 4 * h + (e & 3);
-                  if (key0 + key >= len) w[e >> 1] &= (e & 1) ? 0x0000ffffu : 0xffff0000u;
-                }
-              }
-              vop[t] = u32x4{w[0], w[1], w[2], w[3]};
-            }
-          }
+          const VOps v = ks == 0 ? v0 : fetch_v(1);
 #pragma unroll
           for (int t = 0; t < 4; ++t) {
-            o[t] = Mma32<T>::mma(vop[t], phi[ks], o[t]);
-            o[t] = Mma32<T>::mma(vop[t], plo[ks], o[t]);
+            o[t] = Mma32<T>::mma(v.t[t], phi[ks], o[t]);
+            o[t] = Mma32<T>::mma(v.t[t], plo[ks], o[t]);
           }
         }
       };
