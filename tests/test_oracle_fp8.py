@@ -151,3 +151,52 @@ def test_prefill_matches_causal_sdpa_and_base_pairs_match_the_truncated_pool():
             trunc[bt[s, 2 * j + m]] &= 0xF0
     np.testing.assert_allclose(fp8.prefill(q, cu, p2, bt2, tg2, lens), fp8.prefill(q, cu, trunc, bt, tags, lens),
                                rtol=0, atol=0)
+
+
+def test_append_places_rows_by_flat_index():
+    """New TARGET rows land where plain index arithmetic on the flattened pool
+    says: byte (((blk * 2 + plane) * Hkv + h) * page + off) * d + c, with
+    blk = slot // page and off = slot % page; K goes to plane 0, V to plane 1,
+    and every other byte keeps its value (the 8-bit reading of §3.2: new KV
+    enters as TARGET)."""
+    nb, hkv, d = 6, 3, 128
+    rng = np.random.default_rng(11)
+    pool = rng.integers(0, 256, size=(nb, 2, hkv, PAGE, d), dtype=np.uint8)
+    slots = np.array([0, 17, 95, 40, 41, 63], dtype=np.int32)     # blocks 0, 1, 5, 2, 2, 3
+    n = len(slots)
+    # K bytes even, V bytes odd, so a swapped plane cannot match by chance
+    k_new = (2 * rng.integers(0, 128, size=(n, hkv, d))).astype(np.uint8)
+    v_new = (2 * rng.integers(0, 128, size=(n, hkv, d)) + 1).astype(np.uint8)
+    got = fp8.append(pool, slots, k_new, v_new).reshape(-1)
+    want = pool.reshape(-1).copy()
+    for i in range(n):
+        blk, off = int(slots[i]) // PAGE, int(slots[i]) % PAGE
+        for plane, rows in ((0, k_new), (1, v_new)):
+            for h in range(hkv):
+                base = (((blk * 2 + plane) * hkv + h) * PAGE + off) * d
+                want[base:base + d] = rows[i, h]
+    assert np.array_equal(got, want)
+    # the input pool is not modified
+    assert not np.shares_memory(got, pool)
+
+
+def test_append_then_gather_reads_the_new_tokens():
+    """A sequence whose last tokens were appended reads them back through the
+    (separately pinned) paged gather, decoded as E5M2."""
+    nb, hkv = 5, 2
+    pool = _pool(nb, hkv, 4)
+    bt = np.array([[4, 1, 3]], dtype=np.int32)
+    length = 40
+    tokens = np.arange(30, 40)
+    slots = np.array([bt[0, t // PAGE] * PAGE + t % PAGE for t in tokens], dtype=np.int32)
+    rng = np.random.default_rng(5)
+    k_new = rng.integers(0, 256, size=(len(tokens), hkv, 128), dtype=np.uint8)
+    v_new = rng.integers(0, 256, size=(len(tokens), hkv, 128), dtype=np.uint8)
+    p2 = fp8.append(pool, slots, k_new, v_new)
+    k, v = fp8.gather_sequence(p2, bt[0], np.zeros(3, dtype=np.uint8), length)
+    kk, vv = fp8.bytes_to_f64(k_new), fp8.bytes_to_f64(v_new)
+    np.testing.assert_array_equal(k[30:40], kk)
+    np.testing.assert_array_equal(v[30:40], vv)
+    k0, v0 = fp8.gather_sequence(pool, bt[0], np.zeros(3, dtype=np.uint8), 30)
+    np.testing.assert_array_equal(k[:30], k0)
+    np.testing.assert_array_equal(v[:30], v0)

@@ -159,3 +159,34 @@ def test_validate_last_instead_of_first_index_is_caught(monkeypatch):
     monkeypatch.setattr(ov._Report, "flag", keep_last)
     with pytest.raises(AssertionError):
         tv.test_hand_built_batch_violations()
+
+
+def test_fp8_append_mistakes_are_caught(monkeypatch):
+    """Swapped K/V planes, or a slot split on the wrong page size, in the
+    8-bit append fail its pins."""
+    from oracle import fp8
+    from tests import test_oracle_fp8 as tf
+
+    def swapped(pool, slots, k_new, v_new):
+        pool = np.array(pool, dtype=np.uint8, copy=True)
+        page = pool.shape[3]
+        for i, slot in enumerate(np.asarray(slots, dtype=np.int64)):
+            pool[int(slot) // page, 1, :, int(slot) % page, :] = k_new[i]
+            pool[int(slot) // page, 0, :, int(slot) % page, :] = v_new[i]
+        return pool
+
+    def wrong_split(pool, slots, k_new, v_new):
+        pool = np.array(pool, dtype=np.uint8, copy=True)
+        for i, slot in enumerate(np.asarray(slots, dtype=np.int64)):
+            blk, off = divmod(int(slot), 8)
+            blk %= pool.shape[0]
+            pool[blk, 0, :, off, :] = k_new[i]
+            pool[blk, 1, :, off, :] = v_new[i]
+        return pool
+
+    for bad in (swapped, wrong_split):
+        monkeypatch.setattr(fp8, "append", bad)
+        with pytest.raises(AssertionError):
+            tf.test_append_places_rows_by_flat_index()
+        with pytest.raises(AssertionError):
+            tf.test_append_then_gather_reads_the_new_tokens()
