@@ -54,6 +54,9 @@
  *   - Supported: head_dim 128, page_size 16, dtype bf16, fp16 or e5m2 (the
  *     8-bit pools below), num_q_heads / num_kv_heads in {1, 2, 4, 8, 16}.  Other shapes return
  *     EKV_ERR_UNSUPPORTED.
+ *   - No C++ exception crosses this interface: a host-side failure inside
+ *     the library (host memory exhausted) returns EKV_ERR_HOST, with nothing
+ *     enqueued.
  *   - ekv_last_error() returns a text describing the last failure on the
  *     calling thread.
  */
@@ -74,7 +77,8 @@ enum {
   EKV_OK = 0,
   EKV_ERR_INVALID = 1,      /* bad argument or transition list */
   EKV_ERR_UNSUPPORTED = 2,  /* valid but not implemented for this shape */
-  EKV_ERR_HIP = 3           /* a HIP runtime call failed */
+  EKV_ERR_HIP = 3,          /* a HIP runtime call failed */
+  EKV_ERR_HOST = 4          /* a host-side failure inside the library (out of host memory); nothing was enqueued */
 };
 
 enum { EKV_DTYPE_BF16 = 0, EKV_DTYPE_FP16 = 1, EKV_DTYPE_FP32 = 2, EKV_DTYPE_E5M2 = 3 };
@@ -218,14 +222,16 @@ ekv_status ekv_append_kv(const ekv_pool* pool, const int32_t* slots, const void*
  * For each listed pair i = (s, j) (device int32 pairs[n][2]), with
  * b0 = block_table[s][2j] and b1 = block_table[s][2j+1]: the high bytes of
  * both blocks are packed into b0 in place; if lo_out is not NULL the low
- * bytes go to lo_out[i] (uint8 [n][one block's bytes], device memory or
- * pinned host memory mapped for the device; a pinned host address is
- * replaced by its device address after both ends of the range have been
- * checked, see ekv_stage_blocks); then
+ * bytes go to lo_out[i] (uint8 [n][one block's bytes], device memory of the
+ * current device or pinned host memory mapped for it; both ends of the
+ * range are looked up before anything is enqueued, a pinned host address is
+ * replaced by its device address, and any other memory -- pageable host
+ * memory, another device's memory, memory the runtime cannot describe --
+ * is EKV_ERR_INVALID with nothing enqueued); then
  * block_table[s][2j+1] = b0, both tags = BASE and freed_out[i] = b1 (device
  * int32 [n]).  b1's bytes are not touched.  The caller returns freed_out[]
  * to its free pool only after the stream has passed this call.
- * Errors: EKV_ERR_INVALID, EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.
+ * Errors: EKV_ERR_INVALID, EKV_ERR_UNSUPPORTED, EKV_ERR_HIP, EKV_ERR_HOST.
  */
 ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs,
                       int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,

@@ -17,19 +17,17 @@
 
 namespace {
 
-thread_local std::string g_last_error;
+thread_local char g_last_error[512];
 
 }  // namespace
 
 namespace ekv {
 
 ekv_status fail(ekv_status s, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  vsnprintf(g_last_error, sizeof g_last_error, fmt, ap);
   va_end(ap);
-  g_last_error = buf;
   return s;
 }
 
@@ -219,186 +217,197 @@ const char* ekv_status_string(ekv_status s) {
     case EKV_ERR_INVALID: return "invalid argument";
     case EKV_ERR_UNSUPPORTED: return "unsupported";
     case EKV_ERR_HIP: return "HIP runtime error";
+    case EKV_ERR_HOST: return "host-side failure";
     default: return "unknown status";
   }
 }
 
-const char* ekv_last_error(void) { return g_last_error.c_str(); }
+const char* ekv_last_error(void) { return g_last_error; }
 
 const char* ekv_version(void) { return "0.1.0"; }
 
 ekv_status ekv_lower(const uint8_t* h_tags, const int32_t* h_seq_lens, int32_t batch,
                      int32_t max_blocks, int32_t page_size, int32_t* mode_out,
                      int32_t* h_boundaries_out) {
-  if (!mode_out || batch < 0 || max_blocks <= 0 || page_size <= 0)
-    return fail(EKV_ERR_INVALID, "ekv_lower: bad sizes or NULL mode_out");
-  if (batch > 0 && (!h_tags || !h_seq_lens || !h_boundaries_out))
-    return fail(EKV_ERR_INVALID, "ekv_lower: NULL array");
-  bool any_base = false, any_irregular = false;
-  for (int s = 0; s < batch; ++s) {
-    const int len = h_seq_lens[s];
-    if (len < 0 || (long long)len > (long long)max_blocks * page_size)
-      return fail(EKV_ERR_INVALID, "ekv_lower: sequence %d length %d out of range", s, len);
-    const int nblk = (len + page_size - 1) / page_size;
-    const uint8_t* row = h_tags + (size_t)s * max_blocks;
-    int first = -1, last = -1, count = 0;
-    int j = 0;
-    // four full pairs (8 tag bytes) per step: every byte 0 or 1, the two
-    // bytes of each pair equal, and member 0's low bit marks a BASE pair;
-    // a word that fails a test is redone byte by byte below for the message
-    for (; 2 * j + 8 <= nblk; j += 4) {
-      uint64_t w;
-      std::memcpy(&w, row + 2 * j, 8);
-      if ((w & 0xFEFEFEFEFEFEFEFEull) || ((w ^ (w >> 8)) & 0x00FF00FF00FF00FFull)) break;
-      const uint64_t m = w & 0x0001000100010001ull;   // bit 16k: pair j + k is BASE
-      // selects, not branches: the BASE pattern is data and mispredicts
-      const int lo = j + __builtin_ctzll(m | (1ull << 63)) / 16;
-      const int hi = j + (63 - __builtin_clzll(m | 1ull)) / 16;
-      first = (first < 0 && m) ? lo : first;
-      last = m ? hi : last;
-      count += __builtin_popcountll(m);
-    }
-    for (; 2 * j < nblk; ++j) {
-      const uint8_t a = row[2 * j];
-      const uint8_t b = (2 * j + 1 < nblk) ? row[2 * j + 1] : a;
-      if (a > 1 || b > 1) return fail(EKV_ERR_INVALID, "ekv_lower: tag value out of range");
-      if (a != b) return fail(EKV_ERR_INVALID, "ekv_lower: pair %d of sequence %d has mixed tags", j, s);
-      if (a) {
-        if (first < 0) first = j;
-        last = j;
-        ++count;
+  return ekv::guard("ekv_lower", [&]() -> ekv_status {
+    if (!mode_out || batch < 0 || max_blocks <= 0 || page_size <= 0)
+      return fail(EKV_ERR_INVALID, "ekv_lower: bad sizes or NULL mode_out");
+    if (batch > 0 && (!h_tags || !h_seq_lens || !h_boundaries_out))
+      return fail(EKV_ERR_INVALID, "ekv_lower: NULL array");
+    bool any_base = false, any_irregular = false;
+    for (int s = 0; s < batch; ++s) {
+      const int len = h_seq_lens[s];
+      if (len < 0 || (long long)len > (long long)max_blocks * page_size)
+        return fail(EKV_ERR_INVALID, "ekv_lower: sequence %d length %d out of range", s, len);
+      const int nblk = (len + page_size - 1) / page_size;
+      const uint8_t* row = h_tags + (size_t)s * max_blocks;
+      int first = -1, last = -1, count = 0;
+      int j = 0;
+      // four full pairs (8 tag bytes) per step: every byte 0 or 1, the two
+      // bytes of each pair equal, and member 0's low bit marks a BASE pair;
+      // a word that fails a test is redone byte by byte below for the message
+      for (; 2 * j + 8 <= nblk; j += 4) {
+        uint64_t w;
+        std::memcpy(&w, row + 2 * j, 8);
+        if ((w & 0xFEFEFEFEFEFEFEFEull) || ((w ^ (w >> 8)) & 0x00FF00FF00FF00FFull)) break;
+        const uint64_t m = w & 0x0001000100010001ull;   // bit 16k: pair j + k is BASE
+        // selects, not branches: the BASE pattern is data and mispredicts
+        const int lo = j + __builtin_ctzll(m | (1ull << 63)) / 16;
+        const int hi = j + (63 - __builtin_clzll(m | 1ull)) / 16;
+        first = (first < 0 && m) ? lo : first;
+        last = m ? hi : last;
+        count += __builtin_popcountll(m);
+      }
+      for (; 2 * j < nblk; ++j) {
+        const uint8_t a = row[2 * j];
+        const uint8_t b = (2 * j + 1 < nblk) ? row[2 * j + 1] : a;
+        if (a > 1 || b > 1) return fail(EKV_ERR_INVALID, "ekv_lower: tag value out of range");
+        if (a != b) return fail(EKV_ERR_INVALID, "ekv_lower: pair %d of sequence %d has mixed tags", j, s);
+        if (a) {
+          if (first < 0) first = j;
+          last = j;
+          ++count;
+        }
+      }
+      int32_t* out = h_boundaries_out + 2 * s;
+      if (count == 0) {
+        out[0] = out[1] = 0;
+      } else if (count == last - first + 1) {
+        any_base = true;
+        out[0] = first;
+        out[1] = last + 1;
+      } else {
+        any_base = any_irregular = true;
+        out[0] = out[1] = -1;
       }
     }
-    int32_t* out = h_boundaries_out + 2 * s;
-    if (count == 0) {
-      out[0] = out[1] = 0;
-    } else if (count == last - first + 1) {
-      any_base = true;
-      out[0] = first;
-      out[1] = last + 1;
-    } else {
-      any_base = any_irregular = true;
-      out[0] = out[1] = -1;
-    }
-  }
-  *mode_out = !any_base ? EKV_MODE_NATIVE : (any_irregular ? EKV_MODE_GENERAL : EKV_MODE_STRUCTURED);
-  return EKV_OK;
+    *mode_out = !any_base ? EKV_MODE_NATIVE : (any_irregular ? EKV_MODE_GENERAL : EKV_MODE_STRUCTURED);
+    return EKV_OK;
+  });
 }
 
 size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch) {
-  int group = 0;
+  int group = 0;   // (no allocation or exception on this path)
   if (check_pool(pool) != EKV_OK || check_attention_batch(pool, batch, &group) != EKV_OK) return 0;
   return plan_decode(pool, batch).total;
 }
 
 ekv_status ekv_decode_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
-  if (!ws && ws_bytes) return fail(EKV_ERR_INVALID, "ws is NULL");
-  if (ws_bytes % 4) return fail(EKV_ERR_INVALID, "ws_bytes must be a multiple of 4");
-  return hip_status(ekv::launch_zero_u32(static_cast<uint32_t*>(ws), ws_bytes / 4, stream),
-                    "ekv_decode_workspace_init launch");
+  return ekv::guard("ekv_decode_workspace_init", [&]() -> ekv_status {
+    if (!ws && ws_bytes) return fail(EKV_ERR_INVALID, "ws is NULL");
+    if (ws_bytes % 4) return fail(EKV_ERR_INVALID, "ws_bytes must be a multiple of 4");
+    return hip_status(ekv::launch_zero_u32(static_cast<uint32_t*>(ws), ws_bytes / 4, stream),
+                      "ekv_decode_workspace_init launch");
+  });
 }
 
 ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out,
                            int32_t out_dtype, float scale, void* ws, size_t ws_bytes,
                            hipStream_t stream) {
-  ekv_status st = check_pool(pool);
-  if (st != EKV_OK) return st;
-  int group = 0;
-  if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
-  if (batch->batch == 0) return EKV_OK;
-  if (!q || !out) return fail(EKV_ERR_INVALID, "q and out are required");
-  const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
-  if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
-    return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
-  if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
-  const DecodePlan plan = plan_decode(pool, batch);
-  if (!ws || ws_bytes < plan.total)
-    return fail(EKV_ERR_INVALID, "workspace of %zu bytes needed, %zu given", plan.total, ws_bytes);
-  if (plan.pairs_max >= (1LL << 30)) return fail(EKV_ERR_UNSUPPORTED, "batch too large for one decode call");
-  if (debug_mode() && (st = debug_check_batch(pool, batch, stream, "ekv_attn_decode")) != EKV_OK) return st;
-  ekv::DecodeArgs a{};
-  a.pool = static_cast<const uint16_t*>(pool->kv);
-  a.q = static_cast<const uint16_t*>(q);
-  a.seq_lens = batch->seq_lens;
-  a.bt = batch->block_table;
-  a.tags = batch->tags;
-  a.bounds = batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries;
-  a.counters = static_cast<uint32_t*>(ws);
-  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.ml_offset);
-  a.ws_o = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.o_offset);
-  a.out = out;
-  a.batch = batch->batch;
-  a.num_kv_heads = pool->num_kv_heads;
-  a.num_q_heads = batch->num_q_heads;
-  a.max_blocks = batch->max_blocks;
-  a.num_blocks = pool->num_blocks;
-  a.len_cap = max_seq_blocks(batch) * ekv::kPage;
-  if (batch->max_seq_len > 0) a.len_cap = std::min(a.len_cap, batch->max_seq_len);
-  a.max_splits = plan.max_pieces;
-  a.min_chunk = plan.min_chunk;
-  a.pairs_max = plan.pairs_max;
-  a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
-  // LDS ring depth: the deepest ring that still lets 4 workgroups (one per
-  // SIMD) share a CU's 160 KiB with their window buffers.
-  a.slots = group <= 4 ? 4 : (group == 8 ? 3 : 2);
-  // 8-bit pools holding BASE pairs: per-pair work outweighs the halved bytes,
-  // so twice the waves per SIMD (a shallower ring) pay more than depth
-  if (pool->dtype == EKV_DTYPE_E5M2 && batch->mode != EKV_MODE_NATIVE) a.slots = 2;
-  if (const char* env = getenv("EKV_DECODE_SLOTS")) a.slots = std::max(2, std::min(4, atoi(env)));
-  a.scale_log2 = log2e_scale(scale);
-  return hip_status(ekv::launch_decode(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
-                    "ekv_attn_decode launch");
+  return ekv::guard("ekv_attn_decode", [&]() -> ekv_status {
+    ekv_status st = check_pool(pool);
+    if (st != EKV_OK) return st;
+    int group = 0;
+    if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
+    if (batch->batch == 0) return EKV_OK;
+    if (!q || !out) return fail(EKV_ERR_INVALID, "q and out are required");
+    const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
+    if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
+      return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
+    if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
+    const DecodePlan plan = plan_decode(pool, batch);
+    if (!ws || ws_bytes < plan.total)
+      return fail(EKV_ERR_INVALID, "workspace of %zu bytes needed, %zu given", plan.total, ws_bytes);
+    if (plan.pairs_max >= (1LL << 30)) return fail(EKV_ERR_UNSUPPORTED, "batch too large for one decode call");
+    if (debug_mode() && (st = debug_check_batch(pool, batch, stream, "ekv_attn_decode")) != EKV_OK) return st;
+    ekv::DecodeArgs a{};
+    a.pool = static_cast<const uint16_t*>(pool->kv);
+    a.q = static_cast<const uint16_t*>(q);
+    a.seq_lens = batch->seq_lens;
+    a.bt = batch->block_table;
+    a.tags = batch->tags;
+    a.bounds = batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries;
+    a.counters = static_cast<uint32_t*>(ws);
+    a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.ml_offset);
+    a.ws_o = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.o_offset);
+    a.out = out;
+    a.batch = batch->batch;
+    a.num_kv_heads = pool->num_kv_heads;
+    a.num_q_heads = batch->num_q_heads;
+    a.max_blocks = batch->max_blocks;
+    a.num_blocks = pool->num_blocks;
+    a.len_cap = max_seq_blocks(batch) * ekv::kPage;
+    if (batch->max_seq_len > 0) a.len_cap = std::min(a.len_cap, batch->max_seq_len);
+    a.max_splits = plan.max_pieces;
+    a.min_chunk = plan.min_chunk;
+    a.pairs_max = plan.pairs_max;
+    a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
+    // LDS ring depth: the deepest ring that still lets 4 workgroups (one per
+    // SIMD) share a CU's 160 KiB with their window buffers.
+    a.slots = group <= 4 ? 4 : (group == 8 ? 3 : 2);
+    // 8-bit pools holding BASE pairs: per-pair work outweighs the halved bytes,
+    // so twice the waves per SIMD (a shallower ring) pay more than depth
+    if (pool->dtype == EKV_DTYPE_E5M2 && batch->mode != EKV_MODE_NATIVE) a.slots = 2;
+    if (const char* env = getenv("EKV_DECODE_SLOTS")) a.slots = std::max(2, std::min(4, atoi(env)));
+    a.scale_log2 = log2e_scale(scale);
+    return hip_status(ekv::launch_decode(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
+                      "ekv_attn_decode launch");
+  });
 }
 
 ekv_status ekv_attn_prefill(const ekv_pool* pool, const ekv_batch* batch, const void* q,
                             const int32_t* cu_q, int32_t total_q, int32_t max_q_len, void* out,
                             int32_t out_dtype, float scale, hipStream_t stream) {
-  ekv_status st = check_pool(pool);
-  if (st != EKV_OK) return st;
-  int group = 0;
-  if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
-  if (total_q < 0 || max_q_len < 0) return fail(EKV_ERR_INVALID, "negative sizes");
-  if (batch->batch == 0 || total_q == 0) return EKV_OK;
-  if (!q || !out || !cu_q) return fail(EKV_ERR_INVALID, "q, cu_q and out are required");
-  const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
-  if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
-    return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
-  if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
-  if (max_q_len == 0) return EKV_OK;
-  if (debug_mode() && (st = debug_check_batch(pool, batch, stream, "ekv_attn_prefill")) != EKV_OK) return st;
-  ekv::PrefillArgs a{};
-  a.pool = static_cast<const uint16_t*>(pool->kv);
-  a.q = static_cast<const uint16_t*>(q);
-  a.cu_q = cu_q;
-  a.seq_lens = batch->seq_lens;
-  a.bt = batch->block_table;
-  a.tags = batch->tags;
-  a.bounds = batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries;
-  a.out = out;
-  a.batch = batch->batch;
-  a.num_kv_heads = pool->num_kv_heads;
-  a.num_q_heads = batch->num_q_heads;
-  a.max_blocks = batch->max_blocks;
-  a.max_q_len = max_q_len;
-  a.num_blocks = pool->num_blocks;
-  a.total_q = total_q;
-  a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
-  a.scale_log2 = log2e_scale(scale);
-  return hip_status(ekv::launch_prefill(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
-                    "ekv_attn_prefill launch");
+  return ekv::guard("ekv_attn_prefill", [&]() -> ekv_status {
+    ekv_status st = check_pool(pool);
+    if (st != EKV_OK) return st;
+    int group = 0;
+    if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
+    if (total_q < 0 || max_q_len < 0) return fail(EKV_ERR_INVALID, "negative sizes");
+    if (batch->batch == 0 || total_q == 0) return EKV_OK;
+    if (!q || !out || !cu_q) return fail(EKV_ERR_INVALID, "q, cu_q and out are required");
+    const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
+    if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
+      return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
+    if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
+    if (max_q_len == 0) return EKV_OK;
+    if (debug_mode() && (st = debug_check_batch(pool, batch, stream, "ekv_attn_prefill")) != EKV_OK) return st;
+    ekv::PrefillArgs a{};
+    a.pool = static_cast<const uint16_t*>(pool->kv);
+    a.q = static_cast<const uint16_t*>(q);
+    a.cu_q = cu_q;
+    a.seq_lens = batch->seq_lens;
+    a.bt = batch->block_table;
+    a.tags = batch->tags;
+    a.bounds = batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries;
+    a.out = out;
+    a.batch = batch->batch;
+    a.num_kv_heads = pool->num_kv_heads;
+    a.num_q_heads = batch->num_q_heads;
+    a.max_blocks = batch->max_blocks;
+    a.max_q_len = max_q_len;
+    a.num_blocks = pool->num_blocks;
+    a.total_q = total_q;
+    a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
+    a.scale_log2 = log2e_scale(scale);
+    return hip_status(ekv::launch_prefill(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
+                      "ekv_attn_prefill launch");
+  });
 }
 
 ekv_status ekv_append_kv(const ekv_pool* pool, const int32_t* slots, const void* k, const void* v,
                          int32_t n, hipStream_t stream) {
-  ekv_status st = check_pool(pool);
-  if (st != EKV_OK) return st;
-  if (n < 0) return fail(EKV_ERR_INVALID, "negative n");
-  if (n == 0) return EKV_OK;
-  if (!slots || !k || !v) return fail(EKV_ERR_INVALID, "slots, k and v are required");
-  ekv::AppendArgs a{static_cast<uint16_t*>(pool->kv), slots, static_cast<const uint16_t*>(k),
-                    static_cast<const uint16_t*>(v), n, pool->num_kv_heads, pool->dtype == EKV_DTYPE_E5M2,
-                    pool->num_blocks};
-  return hip_status(ekv::launch_append(a, stream), "ekv_append_kv launch");
+  return ekv::guard("ekv_append_kv", [&]() -> ekv_status {
+    ekv_status st = check_pool(pool);
+    if (st != EKV_OK) return st;
+    if (n < 0) return fail(EKV_ERR_INVALID, "negative n");
+    if (n == 0) return EKV_OK;
+    if (!slots || !k || !v) return fail(EKV_ERR_INVALID, "slots, k and v are required");
+    ekv::AppendArgs a{static_cast<uint16_t*>(pool->kv), slots, static_cast<const uint16_t*>(k),
+                      static_cast<const uint16_t*>(v), n, pool->num_kv_heads, pool->dtype == EKV_DTYPE_E5M2,
+                      pool->num_blocks};
+    return hip_status(ekv::launch_append(a, stream), "ekv_append_kv launch");
+  });
 }
 
 static ekv_status check_transition_args(const ekv_pool* pool, int32_t n, const int32_t* pairs,
@@ -438,18 +447,13 @@ static ekv_status device_readable(const void* p, size_t bytes, int device, const
   return EKV_OK;
 }
 
-// Refinement bytes may sit in pinned host memory: such a pointer is
-// replaced by its device address once the whole range has been checked.
-// Device pointers (and memory the runtime does not describe, such as
-// virtual-memory mappings) are passed on unchanged.
+// Refinement bytes live in device memory of the current device or in pinned
+// host memory mapped for it (the CPU backing); the range is checked at both
+// ends with device_readable and replaced by its device address.  Anything
+// else -- pageable host memory, another device's memory, memory the runtime
+// cannot describe -- is EKV_ERR_INVALID before anything is enqueued, so the
+// kernels never touch memory they cannot reach.
 static ekv_status resolve_lo(const uint8_t* p, size_t bytes, const uint8_t** out) {
-  *out = p;
-  hipPointerAttribute_t attr{};
-  if (hipPointerGetAttributes(&attr, p) != hipSuccess) {
-    (void)hipGetLastError();
-    return EKV_OK;
-  }
-  if (attr.type != hipMemoryTypeHost) return EKV_OK;
   int device = 0;
   if (hipGetDevice(&device) != hipSuccess) return hip_status(hipGetLastError(), "hipGetDevice");
   return device_readable(p, bytes, device, out);
@@ -462,130 +466,142 @@ static size_t block_bytes_of(const ekv_pool* pool) {
 ekv_status ekv_demote(const ekv_pool* pool, int32_t n, const int32_t* pairs, int32_t* block_table,
                       uint8_t* tags, int32_t batch, int32_t max_blocks, int32_t* freed_out,
                       uint8_t* lo_out, hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (n == 0) return EKV_OK;
-  if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
-  const uint8_t* lo = nullptr;
-  if (lo_out && (st = resolve_lo(lo_out, (size_t)n * block_bytes_of(pool), &lo)) != EKV_OK) return st;
-  if (debug_mode() &&
-      (st = debug_check_list(pool, 0, n, pairs, nullptr, block_table, tags, batch, max_blocks, stream, "ekv_demote")) != EKV_OK)
-    return st;
-  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
-                        freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
-  return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
+  return ekv::guard("ekv_demote", [&]() -> ekv_status {
+    ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+    if (st != EKV_OK) return st;
+    if (n == 0) return EKV_OK;
+    if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
+    const uint8_t* lo = nullptr;
+    if (lo_out && (st = resolve_lo(lo_out, (size_t)n * block_bytes_of(pool), &lo)) != EKV_OK) return st;
+    if (debug_mode() &&
+        (st = debug_check_list(pool, 0, n, pairs, nullptr, block_table, tags, batch, max_blocks, stream, "ekv_demote")) != EKV_OK)
+      return st;
+    ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, nullptr, block_table, tags,
+                          freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
+    return hip_status(ekv::launch_demote(a, stream), "ekv_demote launch");
+  });
 }
 
 ekv_status ekv_demote_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
                              const int32_t* pairs, int32_t* block_table, uint8_t* tags, int32_t batch,
                              int32_t max_blocks, int32_t* freed_out, uint8_t* lo_out, hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (!layer_kv || num_layers < 1 || num_layers > 65535)
-    return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
-  if (n == 0) return EKV_OK;
-  if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
-  const uint8_t* lo = nullptr;
-  if (lo_out && (st = resolve_lo(lo_out, (size_t)n * num_layers * block_bytes_of(pool), &lo)) != EKV_OK) return st;
-  if (debug_mode() && (st = debug_check_list(pool, 0, n, pairs, nullptr, block_table, tags, batch, max_blocks, stream,
-                                             "ekv_demote_layers")) != EKV_OK)
-    return st;
-  ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
-                        freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
-  return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
+  return ekv::guard("ekv_demote_layers", [&]() -> ekv_status {
+    ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+    if (st != EKV_OK) return st;
+    if (!layer_kv || num_layers < 1 || num_layers > 65535)
+      return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
+    if (n == 0) return EKV_OK;
+    if (!freed_out) return fail(EKV_ERR_INVALID, "freed_out is required");
+    const uint8_t* lo = nullptr;
+    if (lo_out && (st = resolve_lo(lo_out, (size_t)n * num_layers * block_bytes_of(pool), &lo)) != EKV_OK) return st;
+    if (debug_mode() && (st = debug_check_list(pool, 0, n, pairs, nullptr, block_table, tags, batch, max_blocks, stream,
+                                               "ekv_demote_layers")) != EKV_OK)
+      return st;
+    ekv::TransitionArgs a{nullptr, layer_kv, pairs, nullptr, block_table, tags,
+                          freed_out, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
+    return hip_status(ekv::launch_demote(a, stream), "ekv_demote_layers launch");
+  });
 }
 
 ekv_status ekv_refine(const ekv_pool* pool, int32_t n, const int32_t* pairs,
                       const int32_t* new_blocks, int32_t* block_table, uint8_t* tags, int32_t batch,
                       int32_t max_blocks, const uint8_t* lo_in, hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (n == 0) return EKV_OK;
-  if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
-  const uint8_t* lo = nullptr;
-  st = resolve_lo(lo_in, (size_t)n * block_bytes_of(pool), &lo);
-  if (st != EKV_OK) return st;
-  if (debug_mode() &&
-      (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream, "ekv_refine")) != EKV_OK)
-    return st;
-  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
-  return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
+  return ekv::guard("ekv_refine", [&]() -> ekv_status {
+    ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+    if (st != EKV_OK) return st;
+    if (n == 0) return EKV_OK;
+    if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
+    const uint8_t* lo = nullptr;
+    st = resolve_lo(lo_in, (size_t)n * block_bytes_of(pool), &lo);
+    if (st != EKV_OK) return st;
+    if (debug_mode() &&
+        (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream, "ekv_refine")) != EKV_OK)
+      return st;
+    ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
+                          nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, 1, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
+    return hip_status(ekv::launch_refine(a, stream), "ekv_refine launch");
+  });
 }
 
 ekv_status ekv_refine_staged(const ekv_pool* pool, int32_t n, const int32_t* pairs, const int32_t* new_blocks,
                              int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,
                              hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (n == 0) return EKV_OK;
-  if (!new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
-  if (debug_mode() && (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream,
-                                             "ekv_refine_staged")) != EKV_OK)
-    return st;
-  ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
-                        nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
-  return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
+  return ekv::guard("ekv_refine_staged", [&]() -> ekv_status {
+    ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+    if (st != EKV_OK) return st;
+    if (n == 0) return EKV_OK;
+    if (!new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
+    if (debug_mode() && (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream,
+                                               "ekv_refine_staged")) != EKV_OK)
+      return st;
+    ekv::TransitionArgs a{static_cast<uint16_t*>(pool->kv), nullptr, pairs, new_blocks, block_table, tags,
+                          nullptr, nullptr, n, pool->num_kv_heads, max_blocks, 1, 1, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
+    return hip_status(ekv::launch_refine(a, stream), "ekv_refine_staged launch");
+  });
 }
 
 ekv_status ekv_stage_blocks(const ekv_pool* pool, int32_t n, const void* const* h_src,
                             const int32_t* h_new_blocks, hipStream_t stream) {
-  ekv_status st = check_pool(pool);
-  if (st != EKV_OK) return st;
-  if (n < 0) return fail(EKV_ERR_INVALID, "negative n");
-  if (n == 0) return EKV_OK;
-  if (!h_src || !h_new_blocks) return fail(EKV_ERR_INVALID, "h_src and h_new_blocks are required");
-  const int64_t block_bytes = (int64_t)block_bytes_of(pool);
-  std::vector<uint8_t> used((size_t)pool->num_blocks, 0);
-  for (int i = 0; i < n; ++i) {
-    const int b = h_new_blocks[i];
-    if (b < 0 || b >= pool->num_blocks) return fail(EKV_ERR_INVALID, "new block %d out of range", b);
-    if (used[b]) return fail(EKV_ERR_INVALID, "new block %d listed twice", b);
-    used[b] = 1;
-    if (!h_src[i]) return fail(EKV_ERR_INVALID, "source %d is NULL", i);
-  }
-  int device = 0;
-  if (hipGetDevice(&device) != hipSuccess) return hip_status(hipGetLastError(), "hipGetDevice");
-  // every source is checked before anything is enqueued
-  std::vector<const uint8_t*> dev((size_t)n);
-  for (int i = 0; i < n; ++i) {
-    st = device_readable(h_src[i], (size_t)block_bytes, device, &dev[i]);
+  return ekv::guard("ekv_stage_blocks", [&]() -> ekv_status {
+    ekv_status st = check_pool(pool);
     if (st != EKV_OK) return st;
-  }
-  for (int first = 0; first < n; first += ekv::kStageMax) {
-    ekv::StageArgs a{};
-    a.pool = static_cast<uint8_t*>(pool->kv);
-    a.block_bytes = block_bytes;
-    a.n = std::min(n - first, ekv::kStageMax);
-    for (int k = 0; k < a.n; ++k) {
-      a.src[k] = dev[first + k];
-      a.dst[k] = h_new_blocks[first + k];
+    if (n < 0) return fail(EKV_ERR_INVALID, "negative n");
+    if (n == 0) return EKV_OK;
+    if (!h_src || !h_new_blocks) return fail(EKV_ERR_INVALID, "h_src and h_new_blocks are required");
+    const int64_t block_bytes = (int64_t)block_bytes_of(pool);
+    std::vector<uint8_t> used((size_t)pool->num_blocks, 0);
+    for (int i = 0; i < n; ++i) {
+      const int b = h_new_blocks[i];
+      if (b < 0 || b >= pool->num_blocks) return fail(EKV_ERR_INVALID, "new block %d out of range", b);
+      if (used[b]) return fail(EKV_ERR_INVALID, "new block %d listed twice", b);
+      used[b] = 1;
+      if (!h_src[i]) return fail(EKV_ERR_INVALID, "source %d is NULL", i);
     }
-    st = hip_status(ekv::launch_stage(a, stream), "ekv_stage_blocks launch");
-    if (st != EKV_OK) return st;
-  }
-  return EKV_OK;
+    int device = 0;
+    if (hipGetDevice(&device) != hipSuccess) return hip_status(hipGetLastError(), "hipGetDevice");
+    // every source is checked before anything is enqueued
+    std::vector<const uint8_t*> dev((size_t)n);
+    for (int i = 0; i < n; ++i) {
+      st = device_readable(h_src[i], (size_t)block_bytes, device, &dev[i]);
+      if (st != EKV_OK) return st;
+    }
+    for (int first = 0; first < n; first += ekv::kStageMax) {
+      ekv::StageArgs a{};
+      a.pool = static_cast<uint8_t*>(pool->kv);
+      a.block_bytes = block_bytes;
+      a.n = std::min(n - first, ekv::kStageMax);
+      for (int k = 0; k < a.n; ++k) {
+        a.src[k] = dev[first + k];
+        a.dst[k] = h_new_blocks[first + k];
+      }
+      st = hip_status(ekv::launch_stage(a, stream), "ekv_stage_blocks launch");
+      if (st != EKV_OK) return st;
+    }
+    return EKV_OK;
+  });
 }
 
 ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
                              const int32_t* pairs, const int32_t* new_blocks, int32_t* block_table,
                              uint8_t* tags, int32_t batch, int32_t max_blocks, const uint8_t* lo_in,
                              hipStream_t stream) {
-  ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
-  if (st != EKV_OK) return st;
-  if (!layer_kv || num_layers < 1 || num_layers > 65535)
-    return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
-  if (n == 0) return EKV_OK;
-  if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
-  const uint8_t* lo = nullptr;
-  st = resolve_lo(lo_in, (size_t)n * num_layers * block_bytes_of(pool), &lo);
-  if (st != EKV_OK) return st;
-  if (debug_mode() && (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream,
-                                             "ekv_refine_layers")) != EKV_OK)
-    return st;
-  ekv::TransitionArgs a{nullptr, layer_kv, pairs, new_blocks, block_table, tags,
-                        nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
-  return hip_status(ekv::launch_refine(a, stream), "ekv_refine_layers launch");
+  return ekv::guard("ekv_refine_layers", [&]() -> ekv_status {
+    ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+    if (st != EKV_OK) return st;
+    if (!layer_kv || num_layers < 1 || num_layers > 65535)
+      return fail(EKV_ERR_INVALID, "layer_kv is required and num_layers must be in [1, 65535]");
+    if (n == 0) return EKV_OK;
+    if (!new_blocks || !lo_in) return fail(EKV_ERR_INVALID, "new_blocks and lo_in are required");
+    const uint8_t* lo = nullptr;
+    st = resolve_lo(lo_in, (size_t)n * num_layers * block_bytes_of(pool), &lo);
+    if (st != EKV_OK) return st;
+    if (debug_mode() && (st = debug_check_list(pool, 1, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream,
+                                               "ekv_refine_layers")) != EKV_OK)
+      return st;
+    ekv::TransitionArgs a{nullptr, layer_kv, pairs, new_blocks, block_table, tags,
+                          nullptr, const_cast<uint8_t*>(lo), n, pool->num_kv_heads, max_blocks, num_layers, 0, pool->dtype == EKV_DTYPE_E5M2, batch, pool->num_blocks};
+    return hip_status(ekv::launch_refine(a, stream), "ekv_refine_layers launch");
+  });
 }
 
 ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,
@@ -593,72 +609,78 @@ ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,
                                 const int32_t* h_seq_lens, int32_t batch, int32_t max_blocks,
                                 int32_t page_size, int32_t num_blocks,
                                 const int32_t* h_new_blocks) {
-  if (kind != 0 && kind != 1) return fail(EKV_ERR_INVALID, "kind must be 0 (demote) or 1 (refine)");
-  if (n < 0 || batch < 0 || max_blocks < 2 || page_size <= 0 || num_blocks <= 0)
-    return fail(EKV_ERR_INVALID, "bad sizes");
-  if (n == 0) return EKV_OK;
-  if (!h_pairs || !h_block_table || !h_tags || !h_seq_lens)
-    return fail(EKV_ERR_INVALID, "NULL host mirror");
-  const uint8_t want = kind == 0 ? EKV_TAG_TARGET : EKV_TAG_BASE;
-  std::vector<uint8_t> seen((size_t)batch * max_blocks, 0);
-  for (int i = 0; i < n; ++i) {
-    const int s = h_pairs[2 * i], j = h_pairs[2 * i + 1];
-    if (s < 0 || s >= batch || j < 0 || 2 * j + 1 >= max_blocks)
-      return fail(EKV_ERR_INVALID, "pair %d (%d,%d) out of range", i, s, j);
-    if ((long long)2 * page_size * (j + 1) > h_seq_lens[s])
-      return fail(EKV_ERR_INVALID, "pair %d (%d,%d) is not two full blocks", i, s, j);
-    uint8_t& mark = seen[(size_t)s * max_blocks + 2 * j];
-    if (mark) return fail(EKV_ERR_INVALID, "pair (%d,%d) listed twice", s, j);
-    mark = 1;
-    const uint8_t* row = h_tags + (size_t)s * max_blocks;
-    if (row[2 * j] != want || row[2 * j + 1] != want)
-      return fail(EKV_ERR_INVALID, "pair (%d,%d) is not in the expected state", s, j);
-    const int32_t* bt = h_block_table + (size_t)s * max_blocks;
-    for (int m = 0; m < 2; ++m)
-      if (bt[2 * j + m] < 0 || bt[2 * j + m] >= num_blocks)
-        return fail(EKV_ERR_INVALID, "pair (%d,%d) maps outside the pool", s, j);
-  }
-  if (kind == 1) {
-    if (!h_new_blocks) return fail(EKV_ERR_INVALID, "refinement needs new blocks");
-    std::vector<uint8_t> used((size_t)num_blocks, 0);
-    for (int s = 0; s < batch; ++s) {
-      const int nblk = (h_seq_lens[s] + page_size - 1) / page_size;
-      for (int i = 0; i < nblk && i < max_blocks; ++i) {
-        const int b = h_block_table[(size_t)s * max_blocks + i];
-        if (b >= 0 && b < num_blocks) used[b] = 1;
+  return ekv::guard("ekv_check_transition", [&]() -> ekv_status {
+    if (kind != 0 && kind != 1) return fail(EKV_ERR_INVALID, "kind must be 0 (demote) or 1 (refine)");
+    if (n < 0 || batch < 0 || max_blocks < 2 || page_size <= 0 || num_blocks <= 0)
+      return fail(EKV_ERR_INVALID, "bad sizes");
+    if (n == 0) return EKV_OK;
+    if (!h_pairs || !h_block_table || !h_tags || !h_seq_lens)
+      return fail(EKV_ERR_INVALID, "NULL host mirror");
+    const uint8_t want = kind == 0 ? EKV_TAG_TARGET : EKV_TAG_BASE;
+    std::vector<uint8_t> seen((size_t)batch * max_blocks, 0);
+    for (int i = 0; i < n; ++i) {
+      const int s = h_pairs[2 * i], j = h_pairs[2 * i + 1];
+      if (s < 0 || s >= batch || j < 0 || 2 * j + 1 >= max_blocks)
+        return fail(EKV_ERR_INVALID, "pair %d (%d,%d) out of range", i, s, j);
+      if ((long long)2 * page_size * (j + 1) > h_seq_lens[s])
+        return fail(EKV_ERR_INVALID, "pair %d (%d,%d) is not two full blocks", i, s, j);
+      uint8_t& mark = seen[(size_t)s * max_blocks + 2 * j];
+      if (mark) return fail(EKV_ERR_INVALID, "pair (%d,%d) listed twice", s, j);
+      mark = 1;
+      const uint8_t* row = h_tags + (size_t)s * max_blocks;
+      if (row[2 * j] != want || row[2 * j + 1] != want)
+        return fail(EKV_ERR_INVALID, "pair (%d,%d) is not in the expected state", s, j);
+      const int32_t* bt = h_block_table + (size_t)s * max_blocks;
+      for (int m = 0; m < 2; ++m)
+        if (bt[2 * j + m] < 0 || bt[2 * j + m] >= num_blocks)
+          return fail(EKV_ERR_INVALID, "pair (%d,%d) maps outside the pool", s, j);
+    }
+    if (kind == 1) {
+      if (!h_new_blocks) return fail(EKV_ERR_INVALID, "refinement needs new blocks");
+      std::vector<uint8_t> used((size_t)num_blocks, 0);
+      for (int s = 0; s < batch; ++s) {
+        const int nblk = (h_seq_lens[s] + page_size - 1) / page_size;
+        for (int i = 0; i < nblk && i < max_blocks; ++i) {
+          const int b = h_block_table[(size_t)s * max_blocks + i];
+          if (b >= 0 && b < num_blocks) used[b] = 1;
+        }
+      }
+      for (int i = 0; i < n; ++i) {
+        const int b = h_new_blocks[i];
+        if (b < 0 || b >= num_blocks) return fail(EKV_ERR_INVALID, "new block %d out of range", b);
+        if (used[b]) return fail(EKV_ERR_INVALID, "new block %d is in use", b);
+        used[b] = 1;
       }
     }
-    for (int i = 0; i < n; ++i) {
-      const int b = h_new_blocks[i];
-      if (b < 0 || b >= num_blocks) return fail(EKV_ERR_INVALID, "new block %d out of range", b);
-      if (used[b]) return fail(EKV_ERR_INVALID, "new block %d is in use", b);
-      used[b] = 1;
-    }
-  }
-  return EKV_OK;
+    return EKV_OK;
+  });
 }
 
 ekv_status ekv_validate_batch(const ekv_pool* pool, const ekv_batch* batch, int32_t* report, hipStream_t stream) {
-  const ekv_status st = check_validate_batch(pool, batch, report);
-  if (st != EKV_OK) return st;
-  return hip_status(enqueue_validate_batch(pool, batch, report, stream), "ekv_validate_batch launch");
+  return ekv::guard("ekv_validate_batch", [&]() -> ekv_status {
+    const ekv_status st = check_validate_batch(pool, batch, report);
+    if (st != EKV_OK) return st;
+    return hip_status(enqueue_validate_batch(pool, batch, report, stream), "ekv_validate_batch launch");
+  });
 }
 
 ekv_status ekv_validate_transition(const ekv_pool* pool, int32_t kind, int32_t n, const int32_t* pairs,
                                    const int32_t* new_blocks, const int32_t* block_table, const uint8_t* tags,
                                    const int32_t* seq_lens, int32_t batch, int32_t max_blocks, int32_t* report,
                                    hipStream_t stream) {
-  const ekv_status st = check_pool(pool);
-  if (st != EKV_OK) return st;
-  if (kind != 0 && kind != 1) return fail(EKV_ERR_INVALID, "kind must be 0 (demotion) or 1 (refinement)");
-  if (n < 0 || batch < 0 || max_blocks < 2) return fail(EKV_ERR_INVALID, "bad sizes");
-  if (!report) return fail(EKV_ERR_INVALID, "report is required");
-  if (n > 0 && (!pairs || !block_table || !tags)) return fail(EKV_ERR_INVALID, "pairs, block_table and tags are required");
-  if ((long long)batch * max_blocks >= (1LL << 31))
-    return fail(EKV_ERR_UNSUPPORTED, "batch * max_blocks must be below 2^31");
-  ekv::ValidateListArgs a{pairs, kind == 1 ? new_blocks : nullptr, block_table, tags, seq_lens, report, n, kind,
-                          batch, max_blocks, pool->num_blocks};
-  return hip_status(ekv::launch_validate_list(a, stream), "ekv_validate_transition launch");
+  return ekv::guard("ekv_validate_transition", [&]() -> ekv_status {
+    const ekv_status st = check_pool(pool);
+    if (st != EKV_OK) return st;
+    if (kind != 0 && kind != 1) return fail(EKV_ERR_INVALID, "kind must be 0 (demotion) or 1 (refinement)");
+    if (n < 0 || batch < 0 || max_blocks < 2) return fail(EKV_ERR_INVALID, "bad sizes");
+    if (!report) return fail(EKV_ERR_INVALID, "report is required");
+    if (n > 0 && (!pairs || !block_table || !tags)) return fail(EKV_ERR_INVALID, "pairs, block_table and tags are required");
+    if ((long long)batch * max_blocks >= (1LL << 31))
+      return fail(EKV_ERR_UNSUPPORTED, "batch * max_blocks must be below 2^31");
+    ekv::ValidateListArgs a{pairs, kind == 1 ? new_blocks : nullptr, block_table, tags, seq_lens, report, n, kind,
+                            batch, max_blocks, pool->num_blocks};
+    return hip_status(ekv::launch_validate_list(a, stream), "ekv_validate_transition launch");
+  });
 }
 
 }  // extern "C"

@@ -115,21 +115,14 @@ __device__ __forceinline__ u32x2 widen_nibbles(uint32_t w) {
 // are still being written).
 __device__ __forceinline__ float max3(float a, float b, float c) { return __builtin_fmaxf(__builtin_fmaxf(a, b), c); }
 
-// v *= f in v's own registers.  The rescale of the output accumulators is a
-// rare branch; multiplying in place keeps the accumulators in the same
-// registers on both sides of it, where a plain multiply lets the compiler
-// give the result new registers and copy all 64 on the common path.  The
-// compiler cannot add the wait states an MFMA result needs before this
-// assembly reads it; it runs only after compiler code has read the unit's
-// S^T products (which waits for them), and a wave's products complete in
-// order, so the PV products into v have completed by then.
+// v *= f, written for the compiler: the accumulators come straight from the
+// matrix cores, and only the compiler inserts the wait states a vector
+// instruction needs before it reads an MFMA result.  (On gfx950 the
+// multiplies stay in the accumulators' own registers: no copies on the
+// common path that skips the rescale.)
 __device__ __forceinline__ void scale_in_place(f32x16& v, float f) {
 #pragma unroll
-  for (int i = 0; i < 16; ++i) {
-    float x = v[i];
-    asm("v_mul_f32 %0, %0, %1" : "+v"(x) : "v"(f));
-    v[i] = x;
-  }
+  for (int i = 0; i < 16; ++i) v[i] *= f;
 }
 
 __device__ __forceinline__ void barrier() {
@@ -433,11 +426,16 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
         const VOps v0 = fetch_v(0);
 
         // ---- online softmax over this lane's 16 keys (+ lane ^ 32) ----
+        // Scores enter the softmax as s * c in log2 units.  Interior units fold
+        // c into the max and the exponent; masked units scale first and then
+        // set masked keys to -inf, so that a zero scale never multiplies an
+        // infinity (0 * -inf is NaN).
+        const float c = kMasked ? 1.0f : c_scale;
         if constexpr (kMasked) {
 #pragma unroll
           for (int r = 0; r < 16; ++r) {
             const int key = 8 * (r >> 2) + 4 * h + (r & 3);
-            if (key >= nkeys || key0 + key >= lim) sc[r] = -__builtin_inff();
+            sc[r] = (key >= nkeys || key0 + key >= lim) ? -__builtin_inff() : sc[r] * c_scale;
           }
         }
         const float m0 = max3(sc[0], sc[1], sc[2]), m1 = max3(sc[3], sc[4], sc[5]);
@@ -446,7 +444,7 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
         float mx = max3(max3(m0, m1, m2), max3(m3, m4, sc[15]), m0);
         {
           const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(mx), __float_as_uint(mx), false, false);
-          mx = max3(__uint_as_float(sw[0]), __uint_as_float(sw[1]), __uint_as_float(sw[1])) * c_scale;
+          mx = max3(__uint_as_float(sw[0]), __uint_as_float(sw[1]), __uint_as_float(sw[1])) * c;
         }
         if (__builtin_amdgcn_ballot_w64(mx > m_run + 8.0f)) {
           const float m_new = fmaxf(m_run, mx);
@@ -464,7 +462,7 @@ __global__ __launch_bounds__(64 * kPfWaves) __attribute__((amdgpu_waves_per_eu(2
         for (int ks = 0; ks < 2; ++ks) {
           float p[8];
 #pragma unroll
-          for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(sc[8 * ks + i], c_scale, -m_run));
+          for (int i = 0; i < 8; ++i) p[i] = fast_exp2(__builtin_fmaf(sc[8 * ks + i], c, -m_run));
           lsum[ks] = ((p[0] + p[1]) + (p[2] + p[3])) + ((p[4] + p[5]) + (p[6] + p[7]));
           uint32_t wh[4], wl[4];
 #pragma unroll

@@ -15,7 +15,7 @@ import numpy as np
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libekv.so")
 
-OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_HIP = 0, 1, 2, 3
+OK, ERR_INVALID, ERR_UNSUPPORTED, ERR_HIP, ERR_HOST = 0, 1, 2, 3, 4
 DTYPE_BF16, DTYPE_FP16, DTYPE_FP32, DTYPE_E5M2 = 0, 1, 2, 3
 MODE_NATIVE, MODE_STRUCTURED, MODE_GENERAL = 0, 1, 2
 HEAD_DIM, PAGE = 128, 16
@@ -112,7 +112,22 @@ def _check(status):
 
 
 def _ptr(t):
-    """Device pointer of a contiguous torch tensor, or None."""
+    """Device pointer of a contiguous torch GPU tensor, or None.  A CPU
+    tensor is refused here: its address is host memory no kernel may read
+    (pinned host buffers are passed with :func:`_host_ptr`)."""
+    if t is None:
+        return None
+    if not t.is_cuda:
+        raise EkvError(ERR_INVALID, "device argument must be a GPU tensor")
+    if not t.is_contiguous():
+        raise EkvError(ERR_INVALID, "tensor must be contiguous")
+    return t.data_ptr()
+
+
+def _host_ptr(t):
+    """Address of a contiguous tensor that may also live in pinned host
+    memory (the refinement bytes); the library itself checks that the
+    device can read it."""
     if t is None:
         return None
     if not t.is_contiguous():
@@ -197,13 +212,13 @@ def append_kv(pool, slots, k, v, stream=None):
 def demote(pool, pairs, block_table, tags, freed_out, lo_out=None, stream=None):
     bsz, max_blocks = block_table.shape
     _check(lib().ekv_demote(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(block_table),
-                            _ptr(tags), bsz, max_blocks, _ptr(freed_out), _ptr(lo_out), _stream(stream)))
+                            _ptr(tags), bsz, max_blocks, _ptr(freed_out), _host_ptr(lo_out), _stream(stream)))
 
 
 def refine(pool, pairs, new_blocks, block_table, tags, lo_in, stream=None):
     bsz, max_blocks = block_table.shape
     _check(lib().ekv_refine(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(new_blocks),
-                            _ptr(block_table), _ptr(tags), bsz, max_blocks, _ptr(lo_in), _stream(stream)))
+                            _ptr(block_table), _ptr(tags), bsz, max_blocks, _host_ptr(lo_in), _stream(stream)))
 
 
 def refine_staged(pool, pairs, new_blocks, block_table, tags, stream=None):
@@ -229,14 +244,14 @@ def demote_layers(pool, layer_kv, pairs, block_table, tags, freed_out, lo_out=No
     bsz, max_blocks = block_table.shape
     _check(lib().ekv_demote_layers(ctypes.byref(pool), _ptr(layer_kv), layer_kv.shape[0], pairs.shape[0],
                                    _ptr(pairs), _ptr(block_table), _ptr(tags), bsz, max_blocks, _ptr(freed_out),
-                                   _ptr(lo_out), _stream(stream)))
+                                   _host_ptr(lo_out), _stream(stream)))
 
 
 def refine_layers(pool, layer_kv, pairs, new_blocks, block_table, tags, lo_in, stream=None):
     bsz, max_blocks = block_table.shape
     _check(lib().ekv_refine_layers(ctypes.byref(pool), _ptr(layer_kv), layer_kv.shape[0], pairs.shape[0],
                                    _ptr(pairs), _ptr(new_blocks), _ptr(block_table), _ptr(tags), bsz, max_blocks,
-                                   _ptr(lo_in), _stream(stream)))
+                                   _host_ptr(lo_in), _stream(stream)))
 
 
 def check_transition(kind, pairs, block_table, tags, seq_lens, num_blocks, new_blocks=None, page=PAGE):

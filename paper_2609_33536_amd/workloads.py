@@ -143,9 +143,18 @@ def make_decode_case(seq_lens, num_q_heads, num_kv_heads, *, head_dim=HEAD_DIM,
 
 def make_prefill_case(prefix_lens, chunk_lens, num_q_heads, num_kv_heads, *,
                       head_dim=HEAD_DIM, page=PAGE, dtype="bf16", seed=0,
-                      base_fraction=0.0, placement="random", spare_blocks=0):
+                      base_fraction=0.0, placement="random", spare_blocks=0,
+                      aligned_keys=0, aligned_factor=4.0):
     """A pool holding each sequence's prefix, the new chunk's Q/K/V rows and
-    the slots the chunk's K/V are to be written to (after the prefix)."""
+    the slots the chunk's K/V are to be written to (after the prefix).
+
+    ``aligned_keys`` > 0 plants, per sequence with a chunk and a prefix of at
+    least 64 tokens, that many prefix keys in the second half of the prefix
+    whose K row (for one KV head) is ``aligned_factor`` times one chunk
+    query's row (a random row and a random head of that KV head's group),
+    rounded like every other value: that query's score jumps far above the
+    scores of the first keys, which a streaming softmax has to absorb
+    after it has already accumulated output."""
     prefix_lens = np.asarray(prefix_lens, dtype=np.int32)
     chunk_lens = np.asarray(chunk_lens, dtype=np.int32)
     total = prefix_lens + chunk_lens
@@ -163,7 +172,22 @@ def make_prefill_case(prefix_lens, chunk_lens, num_q_heads, num_kv_heads, *,
             slots[cu[s] + i] = int(case["block_table"][s, t // page]) * page + t % page
     # BASE pairs only inside the prefix (new KV stays TARGET)
     case["pairs"] = choose_pairs(rng, prefix_lens, base_fraction, placement, page)
-    case["q"] = to_words(rng.standard_normal((n, num_q_heads, head_dim), dtype=np.float32), query_dtype(dtype))
+    qf = rng.standard_normal((n, num_q_heads, head_dim), dtype=np.float32)
+    case["q"] = to_words(qf, query_dtype(dtype))
+    planted = []
+    group = num_q_heads // num_kv_heads
+    for s in range(len(total) if aligned_keys else 0):
+        if chunk_lens[s] == 0 or prefix_lens[s] < 64:
+            continue
+        for _ in range(aligned_keys):
+            t = int(rng.integers(prefix_lens[s] // 2, prefix_lens[s]))
+            row = int(cu[s] + rng.integers(0, chunk_lens[s]))
+            kvh = int(rng.integers(0, num_kv_heads))
+            head = kvh * group + int(rng.integers(0, group))
+            blk = int(case["block_table"][s, t // page])
+            case["pool"][blk, 0, kvh, t % page, :] = to_words(aligned_factor * qf[row, head], dtype)
+            planted.append((s, t, row, head))
+    case["aligned"] = np.array(planted, dtype=np.int64).reshape(-1, 4)
     case["k_new"] = to_words(rng.standard_normal((n, num_kv_heads, head_dim), dtype=np.float32), dtype)
     case["v_new"] = to_words(rng.standard_normal((n, num_kv_heads, head_dim), dtype=np.float32), dtype)
     case["cu_q"] = cu

@@ -226,3 +226,51 @@ def test_refinement_bytes_in_pinned_host_memory(dtype, num_layers):
         got = dev[layer].cpu().numpy().view(np.uint16 if dtype == "bf16" else np.uint8)
         assert np.array_equal(got, rp), layer
     assert np.array_equal(bt.cpu().numpy(), rbt) and np.array_equal(tags.cpu().numpy(), rtg)
+
+
+def test_refinement_bytes_in_pageable_memory_are_rejected():
+    """Refinement bytes in pageable host memory (a CPU tensor that is not
+    pinned) are EKV_ERR_INVALID for demote, refine and their multi-layer
+    forms, decided on the host before anything is enqueued: the pool, the
+    table and the tags keep their values, and the library stays usable."""
+    torch = require_gpu()
+    hkv = 2
+    c = workloads.make_decode_case([300, 640], 4 * hkv, hkv, seed=75, base_fraction=0.5, spare_blocks=20)
+    host_safety_check(c, c["pool"].shape)
+    dev = torch.from_numpy(c["pool"].view(np.int16).copy()).cuda()
+    pool = ekv.make_pool(dev, hkv, "bf16")
+    pairs = c["pairs"]
+    n = len(pairs)
+    block_bytes = 2 * hkv * PAGE * 128 * 2
+    bt = torch.from_numpy(c["block_table"].copy()).cuda()
+    tags = torch.from_numpy(c["tags"].copy()).cuda()
+    pairs_d = torch.from_numpy(pairs.copy()).cuda()
+    freed = torch.full((n,), -7, dtype=torch.int32, device="cuda")
+    layer_kv = torch.tensor([dev.data_ptr()], dtype=torch.int64, device="cuda")
+    pageable = torch.zeros((n, block_bytes), dtype=torch.uint8)          # CPU, not pinned
+    assert not pageable.is_pinned()
+    new_d = torch.from_numpy(np.asarray(c["free"][:n], dtype=np.int32)).cuda()
+    calls = [lambda: ekv.demote(pool, pairs_d, bt, tags, freed, pageable),
+             lambda: ekv.demote_layers(pool, layer_kv, pairs_d, bt, tags, freed, pageable),
+             lambda: ekv.refine(pool, pairs_d, new_d, bt, tags, pageable),
+             lambda: ekv.refine_layers(pool, layer_kv, pairs_d, new_d, bt, tags, pageable)]
+    for k, call in enumerate(calls):
+        print(f"pageable lo: call {k}", flush=True)
+        with pytest.raises(ekv.EkvError) as e:
+            call()
+        assert e.value.status == ekv.ERR_INVALID
+    torch.cuda.synchronize()
+    assert np.array_equal(dev.cpu().numpy().view(np.uint16), c["pool"])
+    assert np.array_equal(bt.cpu().numpy(), c["block_table"]) and np.array_equal(tags.cpu().numpy(), c["tags"])
+    assert (freed.cpu().numpy() == -7).all()
+    # device arguments given as CPU tensors are refused by the binding itself
+    with pytest.raises(ekv.EkvError):
+        ekv.demote(pool, pairs_d.cpu(), bt, tags, freed, None)
+    # the library is still usable: a device lo buffer works
+    lo = torch.empty((n, block_bytes), dtype=torch.uint8, device="cuda")
+    ekv.demote(pool, pairs_d, bt, tags, freed, lo)
+    torch.cuda.synchronize()
+    opool, obt, otg, ofreed, olo = otr.demote(c["pool"], c["block_table"], c["tags"], pairs, c["seq_lens"])
+    assert np.array_equal(dev.cpu().numpy().view(np.uint16), opool)
+    assert np.array_equal(lo.cpu().numpy().reshape(olo.shape), olo)
+    assert np.array_equal(freed.cpu().numpy(), ofreed)

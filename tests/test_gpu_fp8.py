@@ -12,6 +12,7 @@ import pytest
 from oracle import fp8 as ofp8
 from oracle import lowering as olow
 from paper_2609_33536_amd import ekv, kvpool, workloads
+from tests import softmax_rises
 from tests.gpu_util import check_attention, default_scale, host_safety_check, require_gpu, words_to_tensor
 
 pytestmark = pytest.mark.gpu
@@ -161,16 +162,23 @@ def _run_prefill(case, hq, hkv, *, use_boundaries=True, out_fp32=True, scale=Non
         opool, obt, otg, _, _ = ofp8.demote(opool, obt, otg, case["pairs"], case["seq_lens"])
     kv.relower()
     q = words_to_tensor(case["q"], torch, "fp16")
-    out = torch.full((q.shape[0], hq, 128), float("nan"), dtype=torch.float32 if out_fp32 else torch.float16,
-                     device="cuda")
+    flags = tuple(out_fp32) if isinstance(out_fp32, (tuple, list)) else (out_fp32,)
     max_q = int(np.diff(case["cu_q"]).max())
     print(f"prefill e5m2: B={len(case['seq_lens'])} Hq={hq} Hkv={hkv} rows={q.shape[0]} pairs={len(case['pairs'])} "
-          f"boundaries={use_boundaries} fp32={out_fp32}", flush=True)
-    ekv.attn_prefill(kv.pool, kv.batch(hq, use_boundaries=use_boundaries), q, torch.from_numpy(case["cu_q"]).cuda(),
-                     max_q, out, scale)
+          f"boundaries={use_boundaries} fp32={flags}", flush=True)
+    outs = []
+    for fp32 in flags:
+        out = torch.full((q.shape[0], hq, 128), float("nan"), dtype=torch.float32 if fp32 else torch.float16,
+                         device="cuda")
+        ekv.attn_prefill(kv.pool, kv.batch(hq, use_boundaries=use_boundaries), q,
+                         torch.from_numpy(case["cu_q"]).cuda(), max_q, out, scale)
+        outs.append(out)
     torch.cuda.synchronize()
     ref = ofp8.prefill(case["q"], case["cu_q"], opool, obt, otg, case["seq_lens"], scale)
-    return check_attention(out.float().cpu().numpy(), ref, out_fp32)
+    for fp32, out in zip(flags, outs):
+        res = check_attention(out.float().cpu().numpy(), ref, fp32)
+        print(f"  fp32={fp32}: max abs err {res[0]:.3e}", flush=True)
+    return res
 
 
 @pytest.mark.parametrize("fraction", [0.0, 0.5, 1.0])
@@ -191,7 +199,7 @@ def test_prefill_e5m2_structured_general_and_fp16_output():
     _run_prefill(c, 32, 8, out_fp32=False)
 
 
-@pytest.mark.parametrize("scale", [0.03, -0.1])
+@pytest.mark.parametrize("scale", [0.03, -0.1, 0.0, -0.0])
 def test_prefill_e5m2_empty_chunks_and_scales(scale):
     """Empty chunks, an empty sequence and single-token chunks in one batch,
     at other softmax scales (a negative one included)."""
@@ -253,4 +261,14 @@ def test_prefill_e5m2_8b_full_size():
     query / 8 KV heads; every output checked."""
     c = workloads.make_prefill_case([2048] * 16, [512] * 16, 32, 8, dtype="e5m2", seed=3, base_fraction=0.5,
                                     spare_blocks=2)
-    _run_prefill(c, 32, 8, out_fp32=False)
+    _run_prefill(c, 32, 8, out_fp32=(False, True))
+
+
+@pytest.mark.parametrize("name", ["aligned-e5m2", "scale1-e5m2-g1"])
+def test_prefill_e5m2_rescale_of_live_output(name):
+    """8-bit pools on inputs that make the kernel rescale accumulators that
+    already hold output (shown on the CPU by test_rescale_inputs.py)."""
+    case, hq, hkv, scale, dtype = softmax_rises.make(name)
+    assert dtype == "e5m2"
+    _run_prefill(case, hq, hkv, out_fp32=(True, False), scale=scale)
+    _run_prefill(case, hq, hkv, out_fp32=True, scale=scale, use_boundaries=False)

@@ -11,8 +11,10 @@ the merge order do not depend on timing)."""
 import numpy as np
 import pytest
 
+from oracle import attention as oatt
 from paper_2609_33536_amd import ekv, kvpool, workloads
-from tests.gpu_util import default_scale, require_gpu, words_to_tensor
+from tests import softmax_rises
+from tests.gpu_util import check_attention, default_scale, require_gpu, words_to_tensor
 
 pytestmark = pytest.mark.gpu
 
@@ -141,8 +143,9 @@ def test_concurrent_calls_on_two_streams():
         kv.relower()
         batch = kv.batch(16)
         runs.append((kv, batch, ekv.decode_workspace(kv.pool, batch), words_to_tensor(c["q"], torch, "bf16")))
+    # the prefill's planted keys make it rescale live accumulators
     p = workloads.make_prefill_case([100, 900, 50], [40, 77, 12], 16, 4, seed=72, base_fraction=0.5,
-                                    spare_blocks=4)
+                                    spare_blocks=4, aligned_keys=3)
     pkv = kvpool.PagedKV(p["pool"], p["block_table"], p["seq_lens"], p["free"], 4)
     pkv.append(torch.from_numpy(p["slots"]).cuda(), words_to_tensor(p["k_new"], torch, "bf16"),
                words_to_tensor(p["v_new"], torch, "bf16"))
@@ -167,6 +170,12 @@ def test_concurrent_calls_on_two_streams():
         launch(k, out, torch.cuda.current_stream())
         torch.cuda.synchronize()
         alone.append(out)
+    # the prefill run alone matches the oracle, and its inputs make the
+    # kernel rescale accumulators that already hold output
+    opool, obt, otg = softmax_rises.oracle_state(p, "bf16")
+    assert (softmax_rises.score_rises(p, opool, obt, otg, scale, "bf16") > 9.0).sum() >= 4
+    ref = oatt.prefill(p["q"], p["cu_q"], opool, obt, otg, p["seq_lens"], "bf16", scale)
+    check_attention(alone[2].cpu().numpy(), ref, True)
     streams = [torch.cuda.Stream() for _ in range(3)]
     for rep in range(3):
         outs = [torch.full(s, float("nan"), dtype=torch.float32, device="cuda") for s in shapes]

@@ -12,13 +12,19 @@ import pytest
 from oracle import attention as oatt
 from oracle import transitions as otr
 from paper_2609_33536_amd import ekv, kvpool, workloads
+from tests import softmax_rises
 from tests.gpu_util import check_attention, default_scale, host_safety_check, require_gpu, words_to_tensor
 
 pytestmark = pytest.mark.gpu
 
 
 def _run_prefill(case, hq, hkv, *, out_fp32=True, use_boundaries=True, scale=None):
+    """Runs the case on the GPU and checks it against the oracle.  out_fp32
+    may be a tuple of flags: the kernel then runs once per output type
+    against one oracle result.  Returns (max abs err, max rel err) of the
+    last run."""
     torch = require_gpu()
+    flags = tuple(out_fp32) if isinstance(out_fp32, (tuple, list)) else (out_fp32,)
     scale = default_scale() if scale is None else scale
     dtype = case["dtype"]
     host_safety_check(case, case["pool"].shape)
@@ -41,14 +47,20 @@ def _run_prefill(case, hq, hkv, *, out_fp32=True, use_boundaries=True, scale=Non
     kv.relower()
     q = words_to_tensor(case["q"], torch, dtype)
     cu = torch.from_numpy(case["cu_q"]).cuda()
-    out = torch.full((q.shape[0], hq, 128), float("nan"), dtype=torch.float32 if out_fp32 else q.dtype,
-                     device="cuda")
     batch = kv.batch(hq, use_boundaries=use_boundaries)
     max_q = int(np.diff(case["cu_q"]).max())
-    ekv.attn_prefill(kv.pool, batch, q, cu, max_q, out, scale)
+    outs = []
+    for fp32 in flags:
+        out = torch.full((q.shape[0], hq, 128), float("nan"), dtype=torch.float32 if fp32 else q.dtype,
+                         device="cuda")
+        ekv.attn_prefill(kv.pool, batch, q, cu, max_q, out, scale)
+        outs.append(out)
     torch.cuda.synchronize()
     ref = oatt.prefill(case["q"], case["cu_q"], opool, obt, otg, case["seq_lens"], dtype, scale)
-    return check_attention(out.float().cpu().numpy(), ref, out_fp32)
+    for fp32, out in zip(flags, outs):
+        res = check_attention(out.float().cpu().numpy(), ref, fp32)
+        print(f"  fp32={fp32}: max abs err {res[0]:.3e}", flush=True)
+    return res
 
 
 @pytest.mark.parametrize("fraction", [0.0, 0.5, 1.0])
@@ -79,7 +91,7 @@ def test_prefill_structured_and_general_agree(prefix, chunk, fraction):
     _run_prefill(c, 32, 8, use_boundaries=False)
 
 
-@pytest.mark.parametrize("scale", [0.03, -0.1])
+@pytest.mark.parametrize("scale", [0.03, -0.1, 0.0, -0.0])
 def test_prefill_empty_chunks_and_scales(scale):
     """A batch mixing empty chunks (a 300-token prefix with no new token), an
     empty sequence, single-token chunks and a first chunk with no prefix, at
@@ -95,5 +107,18 @@ def test_prefill_llama3_8b_chunk_full_size():
     512-token causal chunk), 32 query / 8 KV heads: every output checked."""
     c = workloads.make_prefill_case([2048] * 16, [512] * 16, 32, 8, seed=3, base_fraction=0.5,
                                     spare_blocks=2)
-    err, rel = _run_prefill(c, 32, 8, out_fp32=False)
-    print(f"prefill full size: max abs err {err:.3e}", flush=True)
+    err, rel = _run_prefill(c, 32, 8, out_fp32=(False, True))
+    print(f"prefill full size: max abs err {err:.3e} (fp32 output, strict 2e-3)", flush=True)
+
+
+@pytest.mark.parametrize("name", ["aligned-bf16", "aligned-fp16", "scale1-bf16-g16"])
+def test_prefill_rescale_of_live_output(name):
+    """Inputs whose later 32-key units rise far above the first unit's
+    scores (test_rescale_inputs.py shows it from the oracle's keys), so the
+    kernel rescales accumulators that already hold output; structured
+    (boundaries) and general (tags) lowering, fp32 output at the strict bound
+    and 16-bit output."""
+    case, hq, hkv, scale, dtype = softmax_rises.make(name)
+    assert dtype in ("bf16", "fp16")
+    _run_prefill(case, hq, hkv, out_fp32=(True, False), scale=scale)
+    _run_prefill(case, hq, hkv, out_fp32=True, scale=scale, use_boundaries=False)
