@@ -153,8 +153,14 @@ ekv_status ekv_lower(const uint8_t* h_tags, const int32_t* h_seq_lens, int32_t b
 
 /*
  * Bytes of device scratch that ekv_attn_decode needs for this pool and
- * batch: split-KV partial results plus one merge counter per (sequence,
- * KV head).  Returns 0 for unsupported shapes.
+ * batch: merge counters and the split-KV partial results of the (sequence,
+ * KV head)s that a launch cuts, two slots of G = num_q_heads / num_kv_heads
+ * partial rows per workgroup of the persistent grid.  The size depends on
+ * the group size and on the batch's work (number of sequences times its
+ * length bound) only up to the grid's cap of 4096 workgroups, not on the
+ * mode, the lengths themselves or the device: a workspace of this size
+ * serves every call whose batch needs no more, on any device.  At most
+ * 2 * 4096 * G * 520 + 32 KiB bytes.  Returns 0 for unsupported shapes.
  */
 size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch);
 
@@ -162,8 +168,10 @@ size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch);
  * Prepare a decode workspace for first use: fills ws_bytes bytes of ws
  * with zeros on the stream (a kernel, not a memset).  The merge counters
  * must read zero when a decode starts; every decode call leaves them at
- * zero, so this is needed once after allocation (or after ws was used for
- * anything else).  A zero-filled allocation needs no call.
+ * zero (they keep one place whatever the batch, so calls with different
+ * batches may share a workspace), so this is needed once after allocation
+ * (or after ws was used for anything else).  A zero-filled allocation
+ * needs no call.
  * Errors: EKV_ERR_INVALID (NULL ws with nonzero size, size not a multiple
  * of 4), EKV_ERR_HIP.
  */

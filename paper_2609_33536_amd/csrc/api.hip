@@ -92,28 +92,62 @@ int plan_min_chunk() {
   return 8;
 }
 
-// Workspace: [merge counters u32 B*Hkv | (m, l) f32 rows | o f32 rows], 256-B aligned parts.
-// A (sequence, KV head) of np pairs is cut into at most ceil(np / chunk) + 1
-// pieces, and chunk >= min_chunk.
+// LDS ring depth of the decode kernel: the deepest ring that still lets 4
+// workgroups (one per SIMD) share a CU's 160 KiB with their window buffers.
+// 8-bit pools holding BASE pairs: per-pair work outweighs the halved bytes,
+// so twice the waves per SIMD (a shallower ring) pay more than depth.
+int decode_slots(const ekv_pool* p, int group, bool elastic) {
+  int slots = group <= 4 ? 4 : (group == 8 ? 3 : 2);
+  if (p->dtype == EKV_DTYPE_E5M2 && elastic) slots = 2;
+  if (const char* env = getenv("EKV_DECODE_SLOTS")) slots = std::max(2, std::min(4, atoi(env)));
+  return slots;
+}
+
+// Workspace: [merge counters u32, 2 kMaxDecodeGrid | (m, l) f32 | o f32
+// rows], 256-B aligned parts; the last two hold two slots per workgroup of
+// the launch (G rows a slot), the counters two per possible workgroup.
+// The launch grid is the kernel's resident workgroups on the device, or
+// fewer for small work, and never more than kMaxDecodeGrid.  The size a
+// caller allocates (exact = false) bounds the grid by the work and that cap
+// only, so it needs no device and serves every mode of a batch shape; the
+// size a call needs (exact = true) uses the device's own grid, the larger
+// of the native and the elastic kernel's.
 struct DecodePlan {
-  int min_chunk, max_pieces;
+  int min_chunk, grid;      // grid of the call's own mode (exact plans)
   long long pairs_max;
   size_t ml_offset, o_offset, total;
 };
 
-DecodePlan plan_decode(const ekv_pool* p, const ekv_batch* b) {
-  DecodePlan d{};
+ekv_status plan_decode(const ekv_pool* p, const ekv_batch* b, int group, bool exact, DecodePlan* d) {
   const int nblk = std::max(1, max_seq_blocks(b));
   const int np_max = (nblk + 1) / 2;
-  d.min_chunk = plan_min_chunk();
-  d.max_pieces = (np_max + d.min_chunk - 1) / d.min_chunk + 1;
-  d.pairs_max = (long long)b->batch * p->num_kv_heads * np_max;
-  const size_t rows = (size_t)b->batch * b->num_q_heads * d.max_pieces;
+  d->min_chunk = plan_min_chunk();
+  d->pairs_max = (long long)b->batch * p->num_kv_heads * np_max;
+  if (d->pairs_max >= (1LL << 30)) return fail(EKV_ERR_UNSUPPORTED, "batch too large for one decode call");
+  const long long wanted = (d->pairs_max + d->min_chunk - 1) / d->min_chunk;
+  int grids[2] = {0, 0};
+  for (int elastic = 0; elastic < 2; ++elastic) {
+    if (!exact) {
+      grids[elastic] = (int)std::max<long long>(1, std::min<long long>(wanted, ekv::kMaxDecodeGrid));
+      continue;
+    }
+    ekv::DecodeArgs a{};
+    a.pairs_max = d->pairs_max;
+    a.min_chunk = d->min_chunk;
+    a.slots = decode_slots(p, group, elastic != 0);
+    const hipError_t e = ekv::decode_grid(a, p->dtype, group, elastic != 0, &grids[elastic]);
+    if (e != hipSuccess) return hip_status(e, "decode grid");
+  }
+  d->grid = grids[b->mode != EKV_MODE_NATIVE ? 1 : 0];
+  const size_t slots = 2 * (size_t)std::max(grids[0], grids[1]);
   auto align = [](size_t x) { return (x + 255) & ~(size_t)255; };
-  d.ml_offset = align((size_t)b->batch * p->num_kv_heads * sizeof(uint32_t));
-  d.o_offset = align(d.ml_offset + rows * 2 * sizeof(float));
-  d.total = d.o_offset + rows * ekv::kHeadDim * sizeof(float);
-  return d;
+  // The counters keep one place whatever the grid: a workspace reused by
+  // calls whose grids differ (other batch sizes) never finds partial rows
+  // of an earlier call where a later call expects zero counters.
+  d->ml_offset = align(2 * (size_t)ekv::kMaxDecodeGrid * sizeof(uint32_t));
+  d->o_offset = align(d->ml_offset + slots * group * 2 * sizeof(float));
+  d->total = d->o_offset + slots * group * ekv::kHeadDim * sizeof(float);
+  return EKV_OK;
 }
 
 float log2e_scale(float scale) { return scale * 1.4426950408889634f; }
@@ -207,6 +241,62 @@ ekv_status debug_check_list(const ekv_pool* pool, int kind, int n, const int32_t
   return debug_verdict(report, stream, call);
 }
 
+// One decode call on a workspace (the caller's, or the static scratch with
+// clear_counters: its merge counters are zeroed first by a fill kernel).
+ekv_status decode_call(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out, int32_t out_dtype,
+                       float scale, void* ws, size_t ws_bytes, bool clear_counters, hipStream_t stream,
+                       const char* who) {
+  ekv_status st = check_pool(pool);
+  if (st != EKV_OK) return st;
+  int group = 0;
+  if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
+  if (batch->batch == 0) return EKV_OK;
+  if (!q || !out) return fail(EKV_ERR_INVALID, "q and out are required");
+  const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
+  if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
+    return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
+  if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
+  DecodePlan plan{};
+  if (!clear_counters) {   // the caller's workspace: at least ekv_decode_workspace_bytes
+    if ((st = plan_decode(pool, batch, group, false, &plan)) != EKV_OK) return st;
+    if (!ws || ws_bytes < plan.total)
+      return fail(EKV_ERR_INVALID, "workspace of %zu bytes needed, %zu given", plan.total, ws_bytes);
+  }
+  if ((st = plan_decode(pool, batch, group, true, &plan)) != EKV_OK) return st;
+  if (plan.total > ws_bytes)   // (the static scratch: sized by the device's own grid)
+    return fail(EKV_ERR_UNSUPPORTED, "%s: needs %zu bytes of scratch, %zu available", who, plan.total, ws_bytes);
+  if (debug_mode() && (st = debug_check_batch(pool, batch, stream, who)) != EKV_OK) return st;
+  const bool elastic = batch->mode != EKV_MODE_NATIVE;
+  ekv::DecodeArgs a{};
+  a.pool = static_cast<const uint16_t*>(pool->kv);
+  a.q = static_cast<const uint16_t*>(q);
+  a.seq_lens = batch->seq_lens;
+  a.bt = batch->block_table;
+  a.tags = batch->tags;
+  a.bounds = elastic ? batch->boundaries : nullptr;
+  a.counters = static_cast<uint32_t*>(ws);
+  a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.ml_offset);
+  a.ws_o = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.o_offset);
+  a.out = out;
+  a.batch = batch->batch;
+  a.num_kv_heads = pool->num_kv_heads;
+  a.num_q_heads = batch->num_q_heads;
+  a.max_blocks = batch->max_blocks;
+  a.num_blocks = pool->num_blocks;
+  a.len_cap = max_seq_blocks(batch) * ekv::kPage;
+  if (batch->max_seq_len > 0) a.len_cap = std::min(a.len_cap, batch->max_seq_len);
+  a.min_chunk = plan.min_chunk;
+  a.pairs_max = plan.pairs_max;
+  a.grid = plan.grid;
+  a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
+  a.slots = decode_slots(pool, group, elastic);
+  a.scale_log2 = log2e_scale(scale);
+  if (clear_counters &&
+      (st = hip_status(ekv::launch_zero_u32(a.counters, 2 * (size_t)plan.grid, stream), "scratch clear")) != EKV_OK)
+    return st;
+  return hip_status(ekv::launch_decode(a, pool->dtype, group, elastic, stream), "decode launch");
+}
+
 }  // namespace
 
 extern "C" {
@@ -289,7 +379,9 @@ ekv_status ekv_lower(const uint8_t* h_tags, const int32_t* h_seq_lens, int32_t b
 size_t ekv_decode_workspace_bytes(const ekv_pool* pool, const ekv_batch* batch) {
   int group = 0;   // (no allocation or exception on this path)
   if (check_pool(pool) != EKV_OK || check_attention_batch(pool, batch, &group) != EKV_OK) return 0;
-  return plan_decode(pool, batch).total;
+  DecodePlan plan{};
+  if (plan_decode(pool, batch, group, false, &plan) != EKV_OK) return 0;
+  return plan.total;
 }
 
 ekv_status ekv_decode_workspace_init(void* ws, size_t ws_bytes, hipStream_t stream) {
@@ -305,53 +397,7 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
                            int32_t out_dtype, float scale, void* ws, size_t ws_bytes,
                            hipStream_t stream) {
   return ekv::guard("ekv_attn_decode", [&]() -> ekv_status {
-    ekv_status st = check_pool(pool);
-    if (st != EKV_OK) return st;
-    int group = 0;
-    if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
-    if (batch->batch == 0) return EKV_OK;
-    if (!q || !out) return fail(EKV_ERR_INVALID, "q and out are required");
-    const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
-    if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
-      return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
-    if (!std::isfinite(scale)) return fail(EKV_ERR_INVALID, "scale must be finite");
-    const DecodePlan plan = plan_decode(pool, batch);
-    if (!ws || ws_bytes < plan.total)
-      return fail(EKV_ERR_INVALID, "workspace of %zu bytes needed, %zu given", plan.total, ws_bytes);
-    if (plan.pairs_max >= (1LL << 30)) return fail(EKV_ERR_UNSUPPORTED, "batch too large for one decode call");
-    if (debug_mode() && (st = debug_check_batch(pool, batch, stream, "ekv_attn_decode")) != EKV_OK) return st;
-    ekv::DecodeArgs a{};
-    a.pool = static_cast<const uint16_t*>(pool->kv);
-    a.q = static_cast<const uint16_t*>(q);
-    a.seq_lens = batch->seq_lens;
-    a.bt = batch->block_table;
-    a.tags = batch->tags;
-    a.bounds = batch->mode == EKV_MODE_NATIVE ? nullptr : batch->boundaries;
-    a.counters = static_cast<uint32_t*>(ws);
-    a.ws_ml = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.ml_offset);
-    a.ws_o = reinterpret_cast<float*>(static_cast<char*>(ws) + plan.o_offset);
-    a.out = out;
-    a.batch = batch->batch;
-    a.num_kv_heads = pool->num_kv_heads;
-    a.num_q_heads = batch->num_q_heads;
-    a.max_blocks = batch->max_blocks;
-    a.num_blocks = pool->num_blocks;
-    a.len_cap = max_seq_blocks(batch) * ekv::kPage;
-    if (batch->max_seq_len > 0) a.len_cap = std::min(a.len_cap, batch->max_seq_len);
-    a.max_splits = plan.max_pieces;
-    a.min_chunk = plan.min_chunk;
-    a.pairs_max = plan.pairs_max;
-    a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
-    // LDS ring depth: the deepest ring that still lets 4 workgroups (one per
-    // SIMD) share a CU's 160 KiB with their window buffers.
-    a.slots = group <= 4 ? 4 : (group == 8 ? 3 : 2);
-    // 8-bit pools holding BASE pairs: per-pair work outweighs the halved bytes,
-    // so twice the waves per SIMD (a shallower ring) pay more than depth
-    if (pool->dtype == EKV_DTYPE_E5M2 && batch->mode != EKV_MODE_NATIVE) a.slots = 2;
-    if (const char* env = getenv("EKV_DECODE_SLOTS")) a.slots = std::max(2, std::min(4, atoi(env)));
-    a.scale_log2 = log2e_scale(scale);
-    return hip_status(ekv::launch_decode(a, pool->dtype, group, batch->mode != EKV_MODE_NATIVE, stream),
-                      "ekv_attn_decode launch");
+    return decode_call(pool, batch, q, out, out_dtype, scale, ws, ws_bytes, false, stream, "ekv_attn_decode");
   });
 }
 

@@ -48,12 +48,17 @@
 // (o, max, sum); the wave that finishes last -- found with a per-(sequence,
 // KV head) counter in the workspace -- merges them and writes the output,
 // then resets the counter to zero for the next call.
+#include <algorithm>
+#include <atomic>
+
 #include "attn_device.h"
 #include "common.h"
 #include "launch.h"
 
 namespace ekv {
 namespace {
+
+constexpr int kMaxDevices = 64;
 
 __device__ __forceinline__ void store_agent_f2(float* p, float a, float b) {
   const uint64_t v = (uint64_t)__float_as_uint(a) | ((uint64_t)__float_as_uint(b) << 32);
@@ -83,6 +88,19 @@ __device__ __forceinline__ float wave_sum(float x) {
   return x;
 }
 
+// Workspace slots of partials.  Workgroup w owns slots 2w and 2w + 1: the
+// piece of the (sequence, KV head) that contains its first pair goes to 2w,
+// the piece of a later (sequence, KV head) that contains its last pair to
+// 2w + 1 (the (sequence, KV head)s strictly inside its range are never cut).
+// Piece k of a cut (sequence, KV head) was made by workgroup w_first + k, so
+// its slot is 2 (w_first + k), plus one for k = 0 when the (sequence, KV
+// head) starts inside w_first's range (first_odd).  The merge counter of a
+// (sequence, KV head) lives at the slot of its piece 0.  A slot holds G
+// partial rows (one per query head of the group) and G (max, sum) pairs.
+__device__ __forceinline__ int piece_slot(int w_first, int first_odd, int k) {
+  return 2 * (w_first + k) + (k == 0 ? first_odd : 0);
+}
+
 // Merge the nsplit (<= 64) partials of the G heads of one (sequence, KV
 // head): out = sum_k w_k o_k / sum_k w_k l_k with w_k = exp2(m_k - max m).
 // Lane k holds split k's (max, sum); for the numerators lane (c, par) =
@@ -90,23 +108,24 @@ __device__ __forceinline__ float wave_sum(float x) {
 // parity par.  The (max, sum) loads and the first 16 row loads are issued
 // together, so a merge of up to 2 * kB splits costs one memory round trip.
 template <typename T, int G>
-__device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int lane) {
+__device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int w_first, int first_odd, int lane) {
   constexpr int kB = G >= 16 ? 1 : 16 / G;     // split pairs per batch
   const int c = lane & 31, par = lane >> 5;
   float2 mlk[G];
 #pragma unroll
   for (int h = 0; h < G; ++h)
-    mlk[h] = lane < nsplit ? load_agent_f2(a.ws_ml + 2 * ((head0 + h) * a.max_splits + lane))
+    mlk[h] = lane < nsplit ? load_agent_f2(a.ws_ml + 2 * ((size_t)piece_slot(w_first, first_odd, lane) * G + h))
                            : make_float2(-__builtin_inff(), 0.f);
   f32x4 v[G][kB];
   auto load_batch = [&](int k0) {
 #pragma unroll
     for (int h = 0; h < G; ++h) {
-      const float* o = a.ws_o + (head0 + h) * a.max_splits * kHeadDim + 4 * c;
+      const float* o = a.ws_o + (size_t)h * kHeadDim + 4 * c;
 #pragma unroll
       for (int b = 0; b < kB; ++b) {
         const int k = k0 + 2 * b + par;
-        v[h][b] = k < nsplit ? load_agent_f4(o + (size_t)k * kHeadDim) : f32x4{0.f, 0.f, 0.f, 0.f};
+        v[h][b] = k < nsplit ? load_agent_f4(o + (size_t)piece_slot(w_first, first_odd, k) * G * kHeadDim)
+                             : f32x4{0.f, 0.f, 0.f, 0.f};
       }
     }
   };
@@ -151,27 +170,28 @@ __device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int 
   }
 }
 
-// Any number of splits, one head at a time (long sequences only).
-template <typename T>
-__device__ void merge_head_serial(const DecodeArgs& a, size_t head, int nsplit, int lane) {
-  const float* ml = a.ws_ml + 2 * head * a.max_splits;
-  const float* o = a.ws_o + head * a.max_splits * kHeadDim + 2 * lane;
+// Any number of splits, one head (h of the group) at a time (long sequences only).
+template <typename T, int G>
+__device__ void merge_head_serial(const DecodeArgs& a, size_t head, int h, int nsplit, int w_first, int first_odd,
+                                  int lane) {
+  const float* ml = a.ws_ml + 2 * h;
+  const float* o = a.ws_o + (size_t)h * kHeadDim + 2 * lane;
   float mmax = -__builtin_inff();
   for (int k0 = 0; k0 < nsplit; k0 += 64)
-    if (k0 + lane < nsplit) mmax = fmaxf(mmax, load_agent_f2(ml + 2 * (k0 + lane)).x);
+    if (k0 + lane < nsplit) mmax = fmaxf(mmax, load_agent_f2(ml + 2 * (size_t)piece_slot(w_first, first_odd, k0 + lane) * G).x);
   mmax = wave_max(mmax);
   float den = 0.f, num0 = 0.f, num1 = 0.f;
   for (int k0 = 0; k0 < nsplit; k0 += 64) {
     float wk = 0.f;
     if (k0 + lane < nsplit) {
-      const float2 mlk = load_agent_f2(ml + 2 * (k0 + lane));
+      const float2 mlk = load_agent_f2(ml + 2 * (size_t)piece_slot(w_first, first_odd, k0 + lane) * G);
       wk = fast_exp2(mlk.x - mmax);
       den += wk * mlk.y;
     }
     const int kn = min(64, nsplit - k0);
     for (int k = 0; k < kn; ++k) {
       const float w = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk), k));
-      const float2 v = load_agent_f2(o + (size_t)(k0 + k) * kHeadDim);
+      const float2 v = load_agent_f2(o + (size_t)piece_slot(w_first, first_odd, k0 + k) * G * kHeadDim);
       num0 += w * v.x;
       num1 += w * v.y;
     }
@@ -672,7 +692,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   // partial pieces whose merge counter is bumped after the stream (at most 2)
   int pend_n = 0;
   size_t pend_head0[2] = {0, 0};
-  int pend_counter[2] = {0, 0}, pend_pieces[2] = {0, 0};
+  int pend_wfirst[2] = {0, 0}, pend_odd[2] = {0, 0}, pend_pieces[2] = {0, 0};
 
   auto finalize_piece = [&]() {
     if constexpr (kStack) stacked_sum<G>(st);
@@ -691,18 +711,20 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
                         f32x4{st.o[4][r], st.o[5][r], st.o[6][r], st.o[7][r]} * inv, a.out_fp32);
       }
     } else {
-      const int idx = (int)blockIdx.x - w_first;
+      // this workgroup's slot for the piece: 2w if the (sequence, KV head)
+      // contains its first pair, else 2w + 1
+      const size_t row = (size_t)(2 * (int)blockIdx.x + (first > start ? 1 : 0)) * G + n;
       if (n < G) {
-        const size_t slot = (head0 + n) * a.max_splits + idx;
-        float* dst = a.ws_o + slot * kHeadDim + 32 * g;
+        float* dst = a.ws_o + row * kHeadDim + 32 * g;
 #pragma unroll
         for (int r = 0; r < 4; ++r)
 #pragma unroll
           for (int j = 0; j < 8; j += 2) store_agent_f2(dst + 8 * r + j, st.o[j][r], st.o[j + 1][r]);
-        if (g == 0) store_agent_f2(a.ws_ml + 2 * slot, st.m, l);
+        if (g == 0) store_agent_f2(a.ws_ml + 2 * row, st.m, l);
       }
       pend_head0[pend_n] = head0;
-      pend_counter[pend_n] = ccur.s * hkv + ccur.kvh;
+      pend_wfirst[pend_n] = w_first;
+      pend_odd[pend_n] = first > w_first * chunk ? 1 : 0;
       pend_pieces[pend_n] = pieces;
       ++pend_n;
     }
@@ -874,60 +896,84 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   // both counters are bumped before either result is awaited
   uint32_t prev0 = 0u, prev1 = 0u;
   if (lane == 0) {
-    prev0 = __hip_atomic_fetch_add(a.counters + pend_counter[0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    prev0 = __hip_atomic_fetch_add(a.counters + piece_slot(pend_wfirst[0], pend_odd[0], 0), 1u, __ATOMIC_RELAXED,
+                                   __HIP_MEMORY_SCOPE_AGENT);
     if (pend_n > 1)
-      prev1 = __hip_atomic_fetch_add(a.counters + pend_counter[1], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      prev1 = __hip_atomic_fetch_add(a.counters + piece_slot(pend_wfirst[1], pend_odd[1], 0), 1u, __ATOMIC_RELAXED,
+                                     __HIP_MEMORY_SCOPE_AGENT);
   }
   for (int k = 0; k < pend_n; ++k) {
-    uint32_t* counter = a.counters + pend_counter[k];
+    uint32_t* counter = a.counters + piece_slot(pend_wfirst[k], pend_odd[k], 0);
     if (__builtin_amdgcn_readfirstlane(k == 0 ? prev0 : prev1) != (uint32_t)(pend_pieces[k] - 1)) continue;
     asm volatile("" ::: "memory");
     if (lane == 0) __hip_atomic_store(counter, 0u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (pend_pieces[k] <= 64) merge_splits<T, G>(a, pend_head0[k], pend_pieces[k], lane);
+    if (pend_pieces[k] <= 64) merge_splits<T, G>(a, pend_head0[k], pend_pieces[k], pend_wfirst[k], pend_odd[k], lane);
     else
-      for (int h = 0; h < G; ++h) merge_head_serial<T>(a, pend_head0[k] + h, pend_pieces[k], lane);
+      for (int h = 0; h < G; ++h)
+        merge_head_serial<T, G>(a, pend_head0[k] + h, h, pend_pieces[k], pend_wfirst[k], pend_odd[k], lane);
   }
 }
 
-// Workgroups that fit on the device at once for a kernel (one wave each).
+// Workgroups that fit on the device at once for a kernel (one wave each),
+// cached per device and kernel instance (occupancy does not change).
 template <typename K>
-int resident_groups(K kernel) {
-  int dev = 0, cus = 0, per_cu = 0;
-  if (hipGetDevice(&dev) != hipSuccess) return 0;
+int resident_groups(K kernel, std::atomic<int>* cache) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
+  int r = cache[dev].load(std::memory_order_relaxed);
+  if (r > 0) return r;
+  int cus = 0, per_cu = 0;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
   if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 64, 0) != hipSuccess) return 0;
-  return cus * per_cu;
+  r = cus * per_cu;
+  cache[dev].store(r, std::memory_order_relaxed);
+  return r;
 }
 
+// Launches the instance, or (grid_out != null) only reports the grid it
+// would use: the resident workgroups, or fewer when the work is small.
 template <typename T, int G, int NSLOT, bool F8>
-hipError_t launch_slots(const DecodeArgs& args, bool elastic, hipStream_t st) {
+hipError_t run_slots(const DecodeArgs& a, bool elastic, hipStream_t st, int* grid_out) {
+  static std::atomic<int> cache[2][kMaxDevices];
   auto kernel = elastic ? decode_kernel<T, G, true, NSLOT, F8> : decode_kernel<T, G, false, NSLOT, F8>;
-  DecodeArgs a = args;
-  const int resident = resident_groups(kernel);
-  if (resident <= 0) return hipErrorInvalidDeviceFunction;
-  const long long wanted = (a.pairs_max + a.min_chunk - 1) / a.min_chunk;
-  a.grid = (int)std::max<long long>(1, std::min<long long>(resident, wanted));
+  if (grid_out) {
+    const int resident = resident_groups(kernel, cache[elastic ? 1 : 0]);
+    if (resident <= 0) return hipErrorInvalidDeviceFunction;
+    const long long wanted = (a.pairs_max + a.min_chunk - 1) / a.min_chunk;
+    *grid_out = (int)std::max<long long>(1, std::min<long long>(std::min(resident, kMaxDecodeGrid), wanted));
+    return hipSuccess;
+  }
+  if (a.grid <= 0) return hipErrorInvalidValue;
   hipLaunchKernelGGL(kernel, dim3(a.grid), dim3(64), 0, st, a);
   return hipGetLastError();
 }
 
 template <typename T, int G, bool F8>
-hipError_t launch_typed(const DecodeArgs& a, bool elastic, hipStream_t st) {
+hipError_t run_typed(const DecodeArgs& a, bool elastic, hipStream_t st, int* grid_out) {
   switch (a.slots) {
-    case 2: return launch_slots<T, G, 2, F8>(a, elastic, st);
-    case 4: return launch_slots<T, G, 4, F8>(a, elastic, st);
-    default: return launch_slots<T, G, 3, F8>(a, elastic, st);
+    case 2: return run_slots<T, G, 2, F8>(a, elastic, st, grid_out);
+    case 4: return run_slots<T, G, 4, F8>(a, elastic, st, grid_out);
+    default: return run_slots<T, G, 3, F8>(a, elastic, st, grid_out);
   }
 }
 
 template <typename T, bool F8>
-hipError_t launch_group(const DecodeArgs& a, int group, bool elastic, hipStream_t st) {
+hipError_t run_group(const DecodeArgs& a, int group, bool elastic, hipStream_t st, int* grid_out) {
   switch (group) {
-    case 1: return launch_typed<T, 1, F8>(a, elastic, st);
-    case 2: return launch_typed<T, 2, F8>(a, elastic, st);
-    case 4: return launch_typed<T, 4, F8>(a, elastic, st);
-    case 8: return launch_typed<T, 8, F8>(a, elastic, st);
-    case 16: return launch_typed<T, 16, F8>(a, elastic, st);
+    case 1: return run_typed<T, 1, F8>(a, elastic, st, grid_out);
+    case 2: return run_typed<T, 2, F8>(a, elastic, st, grid_out);
+    case 4: return run_typed<T, 4, F8>(a, elastic, st, grid_out);
+    case 8: return run_typed<T, 8, F8>(a, elastic, st, grid_out);
+    case 16: return run_typed<T, 16, F8>(a, elastic, st, grid_out);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+hipError_t run_dtype(const DecodeArgs& a, int dtype, int group, bool elastic, hipStream_t st, int* grid_out) {
+  switch (dtype) {
+    case 0: return run_group<Bf16, false>(a, group, elastic, st, grid_out);
+    case 1: return run_group<Fp16, false>(a, group, elastic, st, grid_out);
+    case 3: return run_group<Fp16, true>(a, group, elastic, st, grid_out);   // E5M2 bytes, FP16 queries
     default: return hipErrorInvalidValue;
   }
 }
@@ -941,12 +987,11 @@ __global__ void fill_zero_kernel(uint32_t* p, size_t n) {
 
 hipError_t launch_decode(const DecodeArgs& a, int dtype, int group, bool elastic, hipStream_t st) {
   if (a.batch == 0) return hipSuccess;
-  switch (dtype) {
-    case 0: return launch_group<Bf16, false>(a, group, elastic, st);
-    case 1: return launch_group<Fp16, false>(a, group, elastic, st);
-    case 3: return launch_group<Fp16, true>(a, group, elastic, st);   // E5M2 bytes, FP16 queries
-    default: return hipErrorInvalidValue;
-  }
+  return run_dtype(a, dtype, group, elastic, st, nullptr);
+}
+
+hipError_t decode_grid(const DecodeArgs& a, int dtype, int group, bool elastic, int* grid) {
+  return run_dtype(a, dtype, group, elastic, nullptr, grid);
 }
 
 hipError_t launch_zero_u32(uint32_t* p, size_t n, hipStream_t st) {

@@ -14,24 +14,30 @@ struct DecodeArgs {
   const int32_t* bt;         // [B][max_blocks]
   const uint8_t* tags;       // [B][max_blocks] or null
   const int32_t* bounds;     // [B][2] or null
-  float* ws_o;               // [B][Hq][max_splits][128] partial outputs of cut (seq, KV head)s
-  float* ws_ml;              // [B][Hq][max_splits][2]   partial (max, sum)
-  uint32_t* counters;        // [B][Hkv] merge counters, zero between calls
+  float* ws_o;               // [2 grid][G][128] partial outputs, two slots per workgroup
+  float* ws_ml;              // [2 grid][G][2]   partial (max, sum)
+  uint32_t* counters;        // [2 grid] merge counters (at a cut (seq, KV head)'s piece-0 slot), zero between calls
   void* out;                 // [B][Hq][128]
   int32_t batch, num_kv_heads, num_q_heads, max_blocks;
   int32_t num_blocks;        // pool size: table entries are clamped into it
   int32_t len_cap;           // sequence lengths are clamped to this (max_seq_len)
-  int32_t max_splits;        // partial slots per query head (pieces of one (seq, KV head))
   int32_t min_chunk;         // fewest pairs a workgroup streams
-  int32_t grid;              // workgroups launched (set by the launcher)
+  int32_t grid;              // workgroups launched (decode_grid of the same arguments; the workspace has 2 grid slots)
   int64_t pairs_max;         // upper bound on the pairs of all (seq, KV head)s
   int32_t out_fp32;
   int32_t slots;             // LDS ring depth per wave (2..6)
   float scale_log2;          // softmax scale * log2(e)
 };
 
-// dtype: 0 bf16, 1 fp16.  elastic: false = native path (tags never read).
+// Most workgroups one decode launch uses (a cap on the resident grid).
+constexpr int kMaxDecodeGrid = 4096;
+
+// dtype: 0 bf16, 1 fp16, 3 8-bit.  elastic: false = native path (tags never read).
 hipError_t launch_decode(const DecodeArgs& a, int dtype, int group, bool elastic, hipStream_t st);
+// The grid launch_decode would use for these arguments (min_chunk, pairs_max
+// and slots must be set): the resident workgroups of the kernel instance,
+// or fewer for small work.
+hipError_t decode_grid(const DecodeArgs& a, int dtype, int group, bool elastic, int* grid);
 hipError_t launch_zero_u32(uint32_t* p, size_t n, hipStream_t st);
 
 struct TransitionArgs {

@@ -181,3 +181,30 @@ def test_workspace_reused_across_calls_and_init():
         ekv.attn_decode(kv.pool, batch, q, out, default_scale(), ws)
         torch.cuda.synchronize()
         check_attention(out.cpu().numpy(), ref, True)
+
+
+def test_one_workspace_for_batches_of_different_grids():
+    """A workspace sized for the largest batch serves smaller ones whose
+    launches use fewer workgroups (other slot layouts), and the large one
+    again after them: every call matches the oracle (the merge counters
+    keep one place whatever the grid)."""
+    torch = require_gpu()
+    cases = [workloads.make_decode_case(lens, 32, 8, seed=90 + k, base_fraction=0.5, spare_blocks=2)
+             for k, lens in enumerate(([3000, 100, 2048, 5000, 4000, 700], [40, 900], [3000, 100, 2048, 5000, 4000, 700]))]
+    runs = []
+    for c in cases:
+        kv = kvpool.PagedKV(c["pool"], c["block_table"], c["seq_lens"], c["free"], 8)
+        kv.demote(c["pairs"])
+        kv.relower()
+        opool, obt, otg, _, _ = otr.demote(c["pool"], c["block_table"], c["tags"], c["pairs"], c["seq_lens"])
+        runs.append((kv, oatt.decode(c["q"], opool, obt, otg, c["seq_lens"]), words_to_tensor(c["q"], torch, "bf16")))
+    need = [ekv.decode_workspace_bytes(kv.pool, kv.batch(32)) for kv, _, _ in runs]
+    assert need[1] < need[0]
+    ws = torch.full((max(need),), 0xAB, dtype=torch.uint8, device="cuda")
+    ekv.decode_workspace_init(ws)
+    for k, (kv, ref, q) in enumerate(runs + runs[1:2]):
+        out = torch.full((len(kv.mirror.seq_lens), 32, 128), float("nan"), dtype=torch.float32, device="cuda")
+        print(f"shared workspace: call {k} B={len(kv.mirror.seq_lens)}", flush=True)
+        ekv.attn_decode(kv.pool, kv.batch(32), q, out, default_scale(), ws)
+        torch.cuda.synchronize()
+        check_attention(out.cpu().numpy(), ref, True)
