@@ -125,8 +125,17 @@ __device__ __forceinline__ void scale_in_place(f32x16& v, float f) {
   for (int i = 0; i < 16; ++i) v[i] *= f;
 }
 
+// Workgroup barrier that also orders this wave's LDS accesses.  On gfx950
+// s_barrier does not wait for the wave's outstanding LDS operations, and
+// the compiler adds no wait before a bare s_barrier: an LDS write issued
+// before it (the widened 8-bit tiles) could land after another wave has
+// passed the barrier and read the old bytes, and an LDS read still in
+// flight could see a slot that the ring's next load has begun to refill.
+// s_waitcnt lgkmcnt(0) completes every LDS access of the wave first.  The
+// ring's direct-to-LDS loads are vector memory operations, waited for with
+// explicit counts before the barrier that publishes a slot.
 __device__ __forceinline__ void barrier() {
-  asm volatile("" ::: "memory");
+  asm volatile("s_waitcnt lgkmcnt(0)" ::: "memory");
   __builtin_amdgcn_s_barrier();
   asm volatile("" ::: "memory");
 }
