@@ -200,6 +200,25 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
                            hipStream_t stream);
 
 /*
+ * ekv_attn_decode without a caller workspace and without any allocation,
+ * for callers that cannot allocate device memory: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  The
+ * split-KV scratch is a static device array of 32 MiB inside the library
+ * (one per device, held until the process ends); its device address is
+ * looked up once per device on the first call there.  Each call first
+ * zeroes the scratch's merge counters with a fill kernel on the stream,
+ * then runs the same decode kernel as ekv_attn_decode (same results).  The
+ * call allocates nothing and never synchronises; the EKV_DEBUG checks are
+ * not run.  All calls on one device share the scratch: calls that may
+ * overlap on one device (other streams, other threads) race and must be
+ * ordered by the caller.  A batch whose launch needs more than 32 MiB of
+ * scratch (2 slots of G partial rows per workgroup, plus 32 KiB) returns
+ * EKV_ERR_UNSUPPORTED.  Other arguments and errors as ekv_attn_decode.
+ */
+ekv_status ekv_attn_decode_noalloc(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out,
+                                   int32_t out_dtype, float scale, hipStream_t stream);
+
+/*
  * Chunked-prefill attention (§3.2; App. A): sequence s contributes the new
  * rows q[cu_q[s] .. cu_q[s+1]) whose K/V have already been appended; row i
  * of the chunk sees keys 0 .. seq_lens[s] - n_s + i (causal, inclusive),

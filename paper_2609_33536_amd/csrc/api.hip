@@ -150,6 +150,31 @@ ekv_status plan_decode(const ekv_pool* p, const ekv_batch* b, int group, bool ex
   return EKV_OK;
 }
 
+// The no-allocation decode's scratch: one array per device (each GPU the
+// library runs on holds its own copy until the process ends).  Host code
+// never uses its name as an address: scratch_address() looks up the
+// device's address of the array once per device, with that device current.
+constexpr size_t kScratchBytes = size_t(32) << 20;
+constexpr int kScratchDevices = 64;
+static __device__ __align__(256) uint8_t scratch[kScratchBytes];
+
+ekv_status scratch_address(void** out) {
+  static std::mutex mu;
+  static void* addr[kScratchDevices] = {};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return hip_status(hipGetLastError(), "hipGetDevice");
+  if (dev < 0 || dev >= kScratchDevices) return fail(EKV_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kScratchDevices);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!addr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(scratch)");
+    addr[dev] = ptr;
+  }
+  *out = addr[dev];
+  return EKV_OK;
+}
+
 float log2e_scale(float scale) { return scale * 1.4426950408889634f; }
 
 // ---- device-side validation and the EKV_DEBUG mode ------------------------
@@ -241,8 +266,9 @@ ekv_status debug_check_list(const ekv_pool* pool, int kind, int n, const int32_t
   return debug_verdict(report, stream, call);
 }
 
-// One decode call on a workspace (the caller's, or the static scratch with
-// clear_counters: its merge counters are zeroed first by a fill kernel).
+// One decode call on a workspace: the caller's, or (clear_counters) the
+// static scratch, whose merge counters are zeroed first by a fill kernel
+// and which the EKV_DEBUG checks do not use (they allocate).
 ekv_status decode_call(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out, int32_t out_dtype,
                        float scale, void* ws, size_t ws_bytes, bool clear_counters, hipStream_t stream,
                        const char* who) {
@@ -265,7 +291,8 @@ ekv_status decode_call(const ekv_pool* pool, const ekv_batch* batch, const void*
   if ((st = plan_decode(pool, batch, group, true, &plan)) != EKV_OK) return st;
   if (plan.total > ws_bytes)   // (the static scratch: sized by the device's own grid)
     return fail(EKV_ERR_UNSUPPORTED, "%s: needs %zu bytes of scratch, %zu available", who, plan.total, ws_bytes);
-  if (debug_mode() && (st = debug_check_batch(pool, batch, stream, who)) != EKV_OK) return st;
+  // (the debug checks allocate their report buffer: not for the static scratch)
+  if (!clear_counters && debug_mode() && (st = debug_check_batch(pool, batch, stream, who)) != EKV_OK) return st;
   const bool elastic = batch->mode != EKV_MODE_NATIVE;
   ekv::DecodeArgs a{};
   a.pool = static_cast<const uint16_t*>(pool->kv);
@@ -398,6 +425,17 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
                            hipStream_t stream) {
   return ekv::guard("ekv_attn_decode", [&]() -> ekv_status {
     return decode_call(pool, batch, q, out, out_dtype, scale, ws, ws_bytes, false, stream, "ekv_attn_decode");
+  });
+}
+
+ekv_status ekv_attn_decode_noalloc(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out,
+                                   int32_t out_dtype, float scale, hipStream_t stream) {
+  return ekv::guard("ekv_attn_decode_noalloc", [&]() -> ekv_status {
+    void* ws = nullptr;
+    const ekv_status st = scratch_address(&ws);
+    if (st != EKV_OK) return st;
+    return decode_call(pool, batch, q, out, out_dtype, scale, ws, kScratchBytes, true, stream,
+                       "ekv_attn_decode_noalloc");
   });
 }
 

@@ -71,6 +71,7 @@ SIGNATURES = {
     "ekv_decode_workspace_bytes": (_U, [ctypes.POINTER(Pool), ctypes.POINTER(Batch)]),
     "ekv_decode_workspace_init": (_I, [_P, _U, _S]),
     "ekv_attn_decode": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _F, _P, _U, _S]),
+    "ekv_attn_decode_noalloc": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _F, _S]),
     "ekv_attn_prefill": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _I, _P, _I, _F, _S]),
     "ekv_append_kv": (_I, [ctypes.POINTER(Pool), _P, _P, _P, _I, _S]),
     "ekv_demote": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _I, _I, _P, _P, _S]),
@@ -196,6 +197,12 @@ def attn_decode(pool, batch, q, out, scale, ws, stream=None):
     _check(lib().ekv_attn_decode(ctypes.byref(pool), ctypes.byref(batch), _ptr(q), _ptr(out),
                                  dtype_code(out.dtype), scale, _ptr(ws), ws.numel() * ws.element_size(),
                                  _stream(stream)))
+
+
+def attn_decode_noalloc(pool, batch, q, out, scale, stream=None):
+    """Decode on the library's static scratch (no workspace, no allocation)."""
+    _check(lib().ekv_attn_decode_noalloc(ctypes.byref(pool), ctypes.byref(batch), _ptr(q), _ptr(out),
+                                         dtype_code(out.dtype), scale, _stream(stream)))
 
 
 def attn_prefill(pool, batch, q, cu_q, max_q_len, out, scale, stream=None):
