@@ -73,6 +73,10 @@ def parse():
                     help="only the elastic decode launches (for PMC byte counters of that kernel)")
     ap.add_argument("--prefill-only", action="store_true",
                     help="only the chunked-prefill launches (for PMC counters of that kernel)")
+    ap.add_argument("--pressure-only", action="store_true",
+                    help="only the pressure-transition mix (for PMC counters of demote / refine)")
+    ap.add_argument("--decode-70b-only", action="store_true",
+                    help="only the 70B-shaped decode layer (for PMC counters of that launch)")
     return ap.parse_args()
 
 
@@ -255,6 +259,15 @@ def main():
     stream = torch.cuda.current_stream()
     scale = 1.0 / math.sqrt(D)
 
+    if args.pressure_only:
+        print(json.dumps({"pressure_mix": pressure_mix(torch, ekv, kvpool, workloads, stream, scale,
+                                                       steps=max(1, args.steps))}))
+        return 0
+    if args.decode_70b_only:
+        print(json.dumps({"decode_70b": decode_70b(torch, ekv, kvpool, workloads, stream, scale,
+                                                   reps=max(1, args.steps))}))
+        return 0
+
     if args.prefill_only:
         pf = build_prefill(torch, kvpool, workloads)
         pf_batch = pf["kv"].batch(HQ)
@@ -420,6 +433,8 @@ def main():
     result["async_promotion"] = async_promotion_cost(torch, kvpool, tpool, cand, stream)
     print("[bench] multi-layer transitions", file=sys.stderr, flush=True)
     result["transitions_all_layers"] = transitions_all_layers(torch, ekv, stream)
+    print("[bench] pressure-transition mix", file=sys.stderr, flush=True)
+    result["pressure_mix"] = pressure_mix(torch, ekv, kvpool, workloads, stream, scale)
     if not args.no_cpu_baseline:
         print("[bench] cpu_baseline: float64 oracle on the sample", file=sys.stderr, flush=True)
         result["cpu_baseline"], result["parity"] = cpu_baseline(dec, outs, pf)
@@ -650,6 +665,98 @@ def transitions_all_layers(torch, ekv, stream, layers=32, pairs=TRANSITION_PAIRS
             "demote_ms": round(d_ms, 4), "demote_GB_per_s": round(moved / (d_ms * 1e-3) / 1e9, 1),
             "refine_ms": round(r_ms, 4), "refine_GB_per_s": round(moved / (r_ms * 1e-3) / 1e9, 1),
             "paper_sync_demotion_ms": 25.44}
+
+
+def pressure_mix(torch, ekv, kvpool, workloads, stream, scale, steps=20):
+    """The pressure-transition mix: an 8B-shaped pool of 200,000 blocks
+    (13.1 GB), 128 sequences with context uniform in [1024, 16384] (seed 4).
+    Each step demotes a random 10 % of the TARGET pairs (with their
+    refinement bytes, kept in device memory), then refines a random 5 % of
+    the BASE pairs (sampled after that demotion; new blocks from the free
+    FIFO), then decodes the whole batch.  Host planning and uploads are
+    outside the timed regions; each launch is timed with HIP events on the
+    launch stream.  Algorithmic bytes: 4 block-equivalents per demoted pair
+    (2 blocks read, the packed block and the low bytes written) and per
+    refined pair (packed block and low bytes read, 2 blocks written), plus
+    the lists and table updates; decode as for the 8B layer."""
+    nb, bsz, hq = 200_000, 128, 32
+    rng = np.random.default_rng(4)
+    seq_lens = workloads.seq_lens_uniform(rng, bsz, 1024, 16384)
+    used = sum(-(-int(l) // PAGE) for l in seq_lens)
+    case = workloads.make_decode_case_torch(seq_lens, hq, HKV, seed=4, spare_blocks=nb - used)
+    kv = kvpool.PagedKV(case["pool"], case["block_table"], seq_lens, case["free"], HKV)
+    del case["pool"]
+    q = case["q"]
+    out = torch.empty((bsz, hq, D), dtype=torch.bfloat16, device="cuda")
+    block_bytes = kv.block_bytes
+    full_pairs = [int(l) // (2 * PAGE) for l in seq_lens]
+    pair_s = np.concatenate([np.full(n, s, dtype=np.int32) for s, n in enumerate(full_pairs)])
+    pair_j = np.concatenate([np.arange(n, dtype=np.int32) for n in full_pairs])
+    lo_store = {}
+    srng = np.random.default_rng(44)
+    ws = None
+
+    def upload(a):
+        return torch.from_numpy(np.ascontiguousarray(a)).cuda()
+
+    def timed(fn):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        fn()
+        e1.record(stream)
+        e1.synchronize()
+        return e0.elapsed_time(e1)
+
+    rows = []
+    for step in range(steps):
+        tg = kv.mirror.tags[pair_s, 2 * pair_j]
+        tp = np.nonzero(tg == 0)[0]
+        nd = int(0.1 * len(tp))
+        dsel = np.sort(srng.choice(tp, nd, replace=False))
+        dp = np.stack([pair_s[dsel], pair_j[dsel]], axis=1).astype(np.int32)
+        host_freed = kv.mirror.plan_demote(dp)
+        pairs_d, freed = upload(dp), torch.empty(nd, dtype=torch.int32, device="cuda")
+        lo = torch.empty((nd, block_bytes), dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        d_ms = timed(lambda: ekv.demote(kv.pool, pairs_d, kv.bt, kv.tags, freed, lo))
+        kv.mirror.commit_freed(host_freed)
+        for i, k in enumerate(dsel.tolist()):
+            lo_store[k] = (lo, i)
+        tg = kv.mirror.tags[pair_s, 2 * pair_j]
+        bp = np.nonzero(tg == 1)[0]
+        nr = int(0.05 * len(bp))
+        rsel = np.sort(srng.choice(bp, nr, replace=False))
+        rp = np.stack([pair_s[rsel], pair_j[rsel]], axis=1).astype(np.int32)
+        new = kv.mirror.plan_refine(rp)
+        lo_in = torch.stack([lo_store[k][0][lo_store[k][1]] for k in rsel.tolist()])
+        for k in rsel.tolist():
+            del lo_store[k]
+        rpairs_d, new_d = upload(rp), upload(new)
+        torch.cuda.synchronize()
+        r_ms = timed(lambda: ekv.refine(kv.pool, rpairs_d, new_d, kv.bt, kv.tags, lo_in))
+        mode = kv.relower()
+        batch = kv.batch(hq)
+        if ws is None:
+            ws = torch.zeros(ekv.decode_workspace_bytes(kv.pool, batch), dtype=torch.uint8, device="cuda")
+        torch.cuda.synchronize()
+        c_ms = timed(lambda: ekv.attn_decode(kv.pool, batch, q, out, scale, ws))
+        dbytes = nd * (4 * block_bytes + 8 + 8 + 2 + 4)
+        rbytes = nr * (4 * block_bytes + 8 + 4 + 4 + 2)
+        cbytes = decode_bytes(seq_lens, kv.mirror.tags, hq, HKV, mode)
+        rows.append({"step": step, "demoted_pairs": nd, "refined_pairs": nr,
+                     "base_block_fraction": round(float(kv.mirror.tags[pair_s, 2 * pair_j].mean()), 4),
+                     "mode": ["native", "structured", "general"][mode],
+                     "demote_ms": round(d_ms, 4), "demote_GB_per_s": round(dbytes / (d_ms * 1e-3) / 1e9, 1),
+                     "refine_ms": round(r_ms, 4), "refine_GB_per_s": round(rbytes / (r_ms * 1e-3) / 1e9, 1),
+                     "decode_ms": round(c_ms, 4), "decode_GB_per_s": round(cbytes / (c_ms * 1e-3) / 1e9, 1)})
+    del kv, lo_store, ws
+    torch.cuda.empty_cache()
+    med = {k: round(float(np.median([r[k] for r in rows])), 1)
+           for k in ("demote_GB_per_s", "refine_GB_per_s", "decode_GB_per_s")}
+    return {"workload": f"{nb} blocks (13.1 GB), {bsz} sequences with context uniform[1024,16384] seed 4, "
+                        f"{hq}/{HKV} heads; per step: demote 10% of TARGET pairs (with refinement bytes), "
+                        "refine 5% of BASE pairs, decode the batch",
+            "steps": steps, "median": med, "per_step": rows}
 
 
 def controller_cost(ekv, mirror, reps=200):
