@@ -38,11 +38,19 @@ __device__ __forceinline__ DmaOffsets dma_offsets(int lane) {
 
 typedef __attribute__((address_space(3))) void* lds_ptr;
 
+// Cache policy of the K/V tile loads of decode: non-temporal.  Decode reads
+// every K/V byte of a launch exactly once, so keeping the lines in the
+// caches only displaces other data; with the non-temporal bit the
+// direct-to-LDS stream of random 8 KiB tiles reads 6.9 TB/s on MI355X,
+// against 6.2 TB/s with the default policy.  (Prefill re-reads each tile
+// for every query tile of its sequence and keeps the default.)
+constexpr int kStreamOnce = 2;   // the NT bit of the load's cache-policy operand
+
 __device__ __forceinline__ void dma_tile(const char* src, const uint32_t (&off)[4], char* dst) {
 #pragma unroll
   for (int r = 0; r < 4; ++r)
     __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off[r]),
-                                     (lds_ptr)(dst + 1024 * r), 16, 0, 0);
+                                     (lds_ptr)(dst + 1024 * r), 16, 0, kStreamOnce);
 }
 
 struct SplitState {

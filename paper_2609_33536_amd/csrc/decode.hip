@@ -262,7 +262,7 @@ __device__ __forceinline__ void wait_vm4(int n) {
 __device__ __forceinline__ void dma_nibbles(const char* tile, const uint32_t (&nib)[2], char* dst) {
 #pragma unroll
   for (int r = 0; r < 2; ++r)
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile + nib[r]), (lds_ptr)(dst + 1024 * r), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile + nib[r]), (lds_ptr)(dst + 1024 * r), 16, 0, kStreamOnce);
 }
 
 // A TARGET pair's tile: loads 0, 1 (member 0) from tile0, 2, 3 (member 1) from tile1.
@@ -271,7 +271,7 @@ __device__ __forceinline__ void dma_pair_bytes(const char* tile0, const char* ti
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
     const char* src = r < 2 ? tile0 + off[r] : tile1 + (off[r] - kTileBytes / 2);
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src), (lds_ptr)(dst + 1024 * r), 16, 0, 0);
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src), (lds_ptr)(dst + 1024 * r), 16, 0, kStreamOnce);
   }
 }
 
@@ -280,7 +280,7 @@ __device__ __forceinline__ void dma_member0_bytes(const char* tile0, const uint3
 #pragma unroll
   for (int r = 0; r < 2; ++r)
     __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile0 + off[r]), (lds_ptr)(dst + 1024 * r), 16, 0,
-                                     0);
+                                     kStreamOnce);
 }
 
 // 4 bytes of nibbles (element 2k low, 2k+1 high in byte k) -> 8 element
