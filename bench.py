@@ -77,6 +77,9 @@ def parse():
                     help="only the pressure-transition mix (for PMC counters of demote / refine)")
     ap.add_argument("--decode-70b-only", action="store_true",
                     help="only the 70B-shaped decode layer (for PMC counters of that launch)")
+    ap.add_argument("--timeline", action="store_true",
+                    help="per-launch time budget of the 8B decode layer from the instrumented library "
+                         "(built by python -m paper_2609_33536_amd.build --timeline)")
     return ap.parse_args()
 
 
@@ -254,11 +257,18 @@ def main():
         return 0
     from __graft_entry__ import _ensure_built
     from paper_2609_33536_amd import ekv, kvpool, workloads
-    _ensure_built()
+    if args.timeline:
+        from paper_2609_33536_amd import build as _build
+        ekv.LIB_PATH = _build.TIMELINE_LIB   # the instrumented variant, never the default
+    else:
+        _ensure_built()
     torch.cuda.set_device(0)
     stream = torch.cuda.current_stream()
     scale = 1.0 / math.sqrt(D)
 
+    if args.timeline:
+        print(json.dumps(decode_timeline(torch, ekv, kvpool, workloads, stream, scale)))
+        return 0
     if args.pressure_only:
         print(json.dumps({"pressure_mix": pressure_mix(torch, ekv, kvpool, workloads, stream, scale,
                                                        steps=max(1, args.steps))}))
@@ -464,6 +474,63 @@ def native_dispatch(torch, ekv, kv, q, out, scale, stream, reps=30):
     med = {k: float(np.median([a.elapsed_time(b) for a, b in v])) for k, v in times.items()}
     return {"native_ms": round(med["native"], 5), "elastic_forced_ms": round(med["elastic"], 5),
             "ratio": round(med["native"] / med["elastic"], 4), "acceptance": "ratio <= 1.02"}
+
+
+def decode_timeline(torch, ekv, kvpool, workloads, stream, scale, reps=5):
+    """Where the time of one 8B decode launch goes, per BASE fraction, from
+    the instrumented library's per-workgroup timestamps (100 MHz constant
+    clock, relative to the first workgroup's start): workgroup start skew,
+    first K/V slot after start, end of each workgroup's stream, end of its
+    merges, and the mean stream end per XCD; next to the launch's HIP-event
+    time.  Median over `reps` launches of each statistic."""
+    import ctypes
+    lib = ekv.lib()
+    lib.ekv_timeline_read.argtypes = [ctypes.c_void_p, ctypes.c_int]
+    dec = build_decode(torch, kvpool, workloads, 2, 2)
+    q = dec["q"]
+    out = torch.empty((B, HQ, D), dtype=torch.bfloat16, device="cuda")
+    res = []
+    for k, kv in enumerate(dec["pools"]):
+        b = kv.batch(HQ)
+        ws = ekv.decode_workspace(kv.pool, b)
+        rows = []
+        for rep in range(reps + 2):
+            lib.ekv_timeline_clear()
+            torch.cuda.synchronize()
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            ekv.attn_decode(kv.pool, b, q, out, scale, ws)
+            e1.record(stream)
+            torch.cuda.synchronize()
+            host = np.zeros(8 * 8192, dtype=np.uint64)
+            lib.ekv_timeline_read(host.ctypes.data, host.size)
+            t = host.reshape(-1, 8).astype(np.int64)
+            t = t[t[:, 7] == 1]
+            t0 = t[:, 0].min()
+            start, first, stream_end, end = ((t[:, c] - t0) / 100.0 for c in range(4))
+            xcc = t[:, 6] & 0xF
+            merged = t[:, 5] > 0
+            if rep >= 2:
+                rows.append({"event_us": e0.elapsed_time(e1) * 1e3, "workgroups": len(t),
+                             "start_skew_us": float(start.max()),
+                             "first_slot_after_start_us": float(np.median(first - start)),
+                             "first_slot_after_start_max_us": float((first - start).max()),
+                             "stream_end_p50_us": float(np.median(stream_end)),
+                             "stream_end_p90_us": float(np.percentile(stream_end, 90)),
+                             "stream_end_max_us": float(stream_end.max()),
+                             "end_max_us": float(end.max()),
+                             "merge_us_p50": float(np.median((end - stream_end)[merged])) if merged.any() else 0.0,
+                             "merge_us_max": float((end - stream_end)[merged].max()) if merged.any() else 0.0,
+                             "xcd_mean_stream_end_us": [float(stream_end[xcc == x].mean()) for x in range(8)]})
+        med = {key: (round(float(np.median([r[key] for r in rows])), 1) if not isinstance(rows[0][key], list)
+                     else [round(float(np.median([r[key][x] for r in rows])), 1) for x in range(8)])
+               for key in rows[0]}
+        med["outside_workgroups_us"] = round(med["event_us"] - med["end_max_us"], 1)
+        res.append({"base_fraction": FRACTIONS[k], "mode": ["native", "structured", "general"][dec["modes"][k]],
+                    "algorithmic_bytes": decode_bytes(dec["seq_lens"], kv.mirror.tags, HQ, HKV, dec["modes"][k]),
+                    **med})
+        del ws
+    return {"decode_timeline": res, "library": "libekv_timeline.so (timestamps in the decode kernel)"}
 
 
 def decode_70b(torch, ekv, kvpool, workloads, stream, scale, reps=20):

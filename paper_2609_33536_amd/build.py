@@ -1,7 +1,9 @@
 """Build libekv.so (HIP, gfx950) in-tree with hipcc.
 
 Every call compiles all sources; objects go to ``_build/`` and the shared
-library next to this file.  Usage: ``python -m paper_2609_33536_amd.build``.
+library next to this file.  Usage: ``python -m paper_2609_33536_amd.build``
+(``--timeline``: the instrumented libekv_timeline.so for the per-launch time
+budget of the decode kernel, next to libekv.so).
 """
 
 import os
@@ -15,6 +17,7 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(HERE, "libekv.so")
+TIMELINE_LIB = os.path.join(HERE, "libekv_timeline.so")
 SOURCES = ["api.hip", "control.hip", "decode.hip", "prefill.hip", "transition.hip", "validate.hip"]
 ARCH = "gfx950"
 
@@ -36,13 +39,19 @@ def hipcc():
     return path
 
 
-def build(verbose=False, extra_flags=()):
-    os.makedirs(BUILD, exist_ok=True)
+def build(verbose=False, extra_flags=(), timeline=False):
+    """Compile every source and link LIB; with timeline=True the instrumented
+    variant libekv_timeline.so instead (decode workgroups record timestamps,
+    see EKV_TIMELINE in decode.hip; for measurement only)."""
+    build_dir = os.path.join(BUILD, "timeline") if timeline else BUILD
+    lib = TIMELINE_LIB if timeline else LIB
+    extra_flags = tuple(extra_flags) + (("-DEKV_TIMELINE",) if timeline else ())
+    os.makedirs(build_dir, exist_ok=True)
     cc = hipcc()
     procs = []
     objs = []
     for src in SOURCES:
-        obj = os.path.join(BUILD, src.replace(".hip", ".o"))
+        obj = os.path.join(build_dir, src.replace(".hip", ".o"))
         objs.append(obj)
         cmd = [cc, *FLAGS, *extra_flags, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
@@ -59,14 +68,14 @@ def build(verbose=False, extra_flags=()):
             print(out)
     if failed:
         raise RuntimeError(f"hipcc failed for {failed}")
-    tmp = LIB + ".tmp"
+    tmp = lib + ".tmp"
     cmd = [cc, f"--offload-arch={ARCH}", "-shared", "-fPIC", "-o", tmp, *objs]
     if verbose:
         print(" ".join(cmd), flush=True)
     subprocess.run(cmd, check=True)
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":
-    print(build(verbose="-v" in sys.argv))
+    print(build(verbose="-v" in sys.argv, timeline="--timeline" in sys.argv))

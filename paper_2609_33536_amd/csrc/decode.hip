@@ -55,6 +55,24 @@
 #include "common.h"
 #include "launch.h"
 
+#ifdef EKV_TIMELINE
+// Instrumented build only (libekv_timeline.so): per-workgroup timestamps of
+// the last decode launch -- start, first K/V slot ready, end of the stream,
+// end of the merges (100 MHz constant clock) -- and the workgroup's XCD,
+// for the per-launch time budget.  Not compiled into libekv.so.
+__device__ uint64_t g_timeline[8 * 8192];
+extern "C" int ekv_timeline_read(uint64_t* host, int n) {
+  return (int)hipMemcpyFromSymbol(host, HIP_SYMBOL(g_timeline), sizeof(uint64_t) * n, 0, hipMemcpyDeviceToHost);
+}
+extern "C" int ekv_timeline_clear(void) {
+  static uint64_t zeros[8 * 8192];
+  return (int)hipMemcpyToSymbol(HIP_SYMBOL(g_timeline), zeros, sizeof(zeros), 0, hipMemcpyHostToDevice);
+}
+#define EKV_TL(...) __VA_ARGS__
+#else
+#define EKV_TL(...)
+#endif
+
 namespace ekv {
 namespace {
 
@@ -385,6 +403,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   const int g = lane >> 4;
   const int hkv = a.num_kv_heads;
   const int B = a.batch;
+  EKV_TL(const uint64_t tl_start = __builtin_amdgcn_s_memrealtime(); uint64_t tl_first = 0; uint64_t tl_stream = 0;)
 
   // ---- the range of this workgroup -------------------------------------
   const int len0 = lane < B ? clamp_len(a.seq_lens[lane], a.len_cap) : 0;   // kept: sequences 0..63
@@ -749,6 +768,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       const bool lone = !base && cb + 1 >= ccur.b1;
       c_ops += (base || lone) ? 4 : 8;
       wait_vm4(ops - c_ops);
+      EKV_TL(if (!tl_first) tl_first = __builtin_amdgcn_s_memrealtime();)
       const char* ring0 = &sm.ring[0][0];
       const char* kb = ring0 + kUnit * cslot;
       const char* vb = ring0 + kUnit * (cslot + 1 == 2 * NSLOT ? 0 : cslot + 1);
@@ -801,6 +821,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     } else {
     c_ops += 8;
     wait_vm<NSLOT - 1>(ops - c_ops);
+    EKV_TL(if (!tl_first) tl_first = __builtin_amdgcn_s_memrealtime();)
     const char* sb = sm.ring[cslot];
     if (block_is_base(cmode, ctag, ccur.b0, cb)) {
       // one packed pair: member 0 = logical block cb, member 1 = cb + 1
@@ -889,9 +910,22 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     cb = ccur.b0;
   }
   (void)piece_j0;
+  EKV_TL(tl_stream = __builtin_amdgcn_s_memrealtime();
+         auto tl_write = [&]() {
+           if (lane == 0 && blockIdx.x < 8192) {
+             uint64_t* r = g_timeline + 8 * blockIdx.x;
+             r[0] = tl_start; r[1] = tl_first; r[2] = tl_stream; r[3] = __builtin_amdgcn_s_memrealtime();
+             r[4] = (uint64_t)(end - start); r[5] = (uint64_t)pend_n;
+             r[6] = (uint64_t)__builtin_amdgcn_s_getreg(30740);   // XCC_ID (hwreg 20, bits 0..15)
+             r[7] = 1;
+           }
+         };)
 
   // ---- merges ----------------------------------------------------------
-  if (pend_n == 0) return;
+  if (pend_n == 0) {
+    EKV_TL(tl_write();)
+    return;
+  }
   asm volatile("s_waitcnt vmcnt(0)" ::: "memory");   // partials have landed before they are counted
   // both counters are bumped before either result is awaited
   uint32_t prev0 = 0u, prev1 = 0u;
@@ -912,6 +946,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       for (int h = 0; h < G; ++h)
         merge_head_serial<T, G>(a, pend_head0[k] + h, h, pend_pieces[k], pend_wfirst[k], pend_odd[k], lane);
   }
+  EKV_TL(tl_write();)
 }
 
 // Workgroups that fit on the device at once for a kernel (one wave each),
