@@ -46,10 +46,19 @@ typedef __attribute__((address_space(3))) void* lds_ptr;
 // for every query tile of its sequence and keeps the default.)
 constexpr int kStreamOnce = 2;   // the NT bit of the load's cache-policy operand
 
+// A lane's 32-bit offset, made opaque at the load: without it the compiler
+// hoists the offset's widening to 64 bits out of the loop, and each load then
+// needs a 64-bit vector add for its address; with it the load takes the
+// scalar-base form (64-bit base in scalar registers + 32-bit lane offset).
+__device__ __forceinline__ uint32_t lane_offset(uint32_t off) {
+  asm volatile("" : "+v"(off));
+  return off;
+}
+
 __device__ __forceinline__ void dma_tile(const char* src, const uint32_t (&off)[4], char* dst) {
 #pragma unroll
   for (int r = 0; r < 4; ++r)
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + off[r]),
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(src + lane_offset(off[r])),
                                      (lds_ptr)(dst + 1024 * r), 16, 0, kStreamOnce);
 }
 
@@ -124,8 +133,45 @@ __device__ __forceinline__ void v_operands(const u32x4 (&v)[NG][4], u32x2 (&vop)
     for (int j = 0; j < 8; ++j) vop[q][j] = v_operand<BASE>(v[q], j);
 }
 
+// The A operands of the column-stacked PV product: operand j holds the
+// lane's 4 tokens of group 0 and then those of group 1 (zero for NG = 1),
+// built in place, so that no register moves sit between the permutes and
+// the products.
+template <bool BASE, int NG>
+__device__ __forceinline__ void v_operands_stacked(const u32x4 (&v)[NG][4], u32x4 (&vop)[8]) {
+#pragma unroll
+  for (int j = 0; j < 8; ++j) {
+    const u32x2 a0 = v_operand<BASE>(v[0], j);
+    const u32x2 a1 = NG == 2 ? v_operand<BASE>(v[NG - 1], j) : u32x2{0u, 0u};
+    vop[j] = u32x4{a0.x, a0.y, a1.x, a1.y};
+  }
+}
+
+// Two probabilities -> one packed word for the column-stacked product: the
+// 16-bit heads rne(p) for k = 0 (head columns), the 16-bit remainders
+// rne(p - rne(p)) for k = 1 (remainder columns).  p - rne(p) is exact in
+// fp32, so one fused multiply-add per value selects what is rounded.
+template <typename T>
+__device__ __forceinline__ uint32_t split_stacked(float p0, float p1, float k);
+typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
+typedef float f32x2v __attribute__((ext_vector_type(2)));
+template <>
+__device__ __forceinline__ uint32_t split_stacked<Bf16>(float p0, float p1, float k) {
+  const uint32_t h = __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2v{p0, p1}, bf16x2v));
+  const f32x2v v = {__builtin_fmaf(-k, __uint_as_float(h << 16), p0),
+                    __builtin_fmaf(-k, __uint_as_float(h & 0xffff0000u), p1)};
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(v, bf16x2v));
+}
+template <>
+__device__ __forceinline__ uint32_t split_stacked<Fp16>(float p0, float p1, float k) {
+  const _Float16 h0 = (_Float16)p0, h1 = (_Float16)p1;
+  const _Float16 w0 = (_Float16)__builtin_fmaf(-k, (float)h0, p0), w1 = (_Float16)__builtin_fmaf(-k, (float)h1, p1);
+  return (uint32_t)__builtin_bit_cast(uint16_t, w0) | ((uint32_t)__builtin_bit_cast(uint16_t, w1) << 16);
+}
+
 // Online-softmax update of one query column set for NG 16-token groups of
-// one slot, followed by O += V^T P^T.  Token p of group q (p = tok0 + 16q
+// one slot, followed by O += V^T P^T.  c = |scale| log2(e) >= 0: a negative
+// scale is applied by negating the query (exact) instead.  Token p of group q (p = tok0 + 16q
 // + 4g + i for this lane) counts only if p < lim (lim: this lane's column
 // limit); `mask` says whether any token of the slot can fail that test.
 // The reference max only moves (and O, l are rescaled) when some column's
@@ -134,12 +180,12 @@ __device__ __forceinline__ void v_operands(const u32x4 (&v)[NG][4], u32x2 (&vop)
 // against the duplicated V operand.
 template <typename T, int NG>
 __device__ __forceinline__ void softmax_pv(SplitState& st, const f32x4 (&s)[NG], const u32x2 (&vop)[NG][8],
-                                           int tok0, int lim, bool mask, float scale_log2, int g) {
+                                           int tok0, int lim, bool mask, float c, int g) {
   float sc[NG][4];
 #pragma unroll
   for (int q = 0; q < NG; ++q)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) sc[q][i] = s[q][i] * scale_log2;
+    for (int i = 0; i < 4; ++i) sc[q][i] = s[q][i] * c;
   if (mask) {
 #pragma unroll
     for (int q = 0; q < NG; ++q)
@@ -189,27 +235,32 @@ __device__ __forceinline__ void softmax_pv(SplitState& st, const f32x4 (&s)[NG],
 // other half zero).  Columns n < G accumulate V^T times the 16-bit head of P,
 // columns G <= n < 2G the 16-bit remainder; stacked_sum() adds the two
 // column sets at the end.  So P still carries ~16 significant bits, and V
-// is neither duplicated nor multiplied twice.
+// is neither duplicated nor multiplied twice.  Scores enter the softmax as
+// s * c (log2 units, c >= 0): a step without masked tokens folds c into the
+// max and the exponent's fused multiply-add; a masked step scales first and
+// then sets masked tokens to -inf, so that c = 0 never multiplies an infinity.
 template <typename T, int NG, int G>
-__device__ __forceinline__ void softmax_pv_stacked(SplitState& st, const f32x4 (&s)[NG], const u32x2 (&vop)[NG][8],
-                                                   int tok0, int lim, bool mask, float scale_log2, int g, int n) {
+__device__ __forceinline__ void softmax_pv_stacked(SplitState& st, const f32x4 (&s)[NG], const u32x4 (&vop)[8],
+                                                   int tok0, int lim, bool mask, float c, int g, int n) {
   static_assert(2 * G <= 16, "two column sets must fit the 16 MFMA columns");
   float sc[NG][4];
-#pragma unroll
-  for (int q = 0; q < NG; ++q)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) sc[q][i] = s[q][i] * scale_log2;
+  float cc = c;
   if (mask) {
 #pragma unroll
     for (int q = 0; q < NG; ++q)
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
-        if (tok0 + q * kPage + 4 * g + i >= lim) sc[q][i] = -__builtin_inff();
+      for (int i = 0; i < 4; ++i) sc[q][i] = tok0 + q * kPage + 4 * g + i >= lim ? -__builtin_inff() : s[q][i] * c;
+    cc = 1.0f;
+  } else {
+#pragma unroll
+    for (int q = 0; q < NG; ++q)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) sc[q][i] = s[q][i];
   }
   float mx = fmaxf(fmaxf(sc[0][0], sc[0][1]), fmaxf(sc[0][2], sc[0][3]));
 #pragma unroll
   for (int q = 1; q < NG; ++q) mx = fmaxf(mx, fmaxf(fmaxf(sc[q][0], sc[q][1]), fmaxf(sc[q][2], sc[q][3])));
-  mx = head_max(mx);
+  mx = head_max(mx) * cc;
   if (__builtin_amdgcn_ballot_w64(mx > st.m + 8.0f)) {
     const float m_new = fmaxf(st.m, mx);
     const float alpha = fast_exp2(st.m - m_new);
@@ -218,33 +269,54 @@ __device__ __forceinline__ void softmax_pv_stacked(SplitState& st, const f32x4 (
     for (int j = 0; j < 8; ++j) st.o[j] *= alpha;
     st.m = m_new;
   }
-  const bool lo_cols = n >= G;
+  const float k = n >= G ? 1.0f : 0.0f;   // remainder columns
   uint32_t pw[2][2] = {{0u, 0u}, {0u, 0u}};
 #pragma unroll
   for (int q = 0; q < NG; ++q) {
     float p[4];
 #pragma unroll
-    for (int i = 0; i < 4; ++i) p[i] = fast_exp2(sc[q][i] - st.m);
+    for (int i = 0; i < 4; ++i) p[i] = fast_exp2(__builtin_fmaf(sc[q][i], cc, -st.m));
     st.l += (p[0] + p[1]) + (p[2] + p[3]);
-    uint16_t w[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      float back;
-      const uint16_t hi = Mma<T>::round(p[i], &back);
-      float dummy;
-      const uint16_t lo = Mma<T>::round(p[i] - back, &dummy);
-      w[i] = lo_cols ? lo : hi;
-    }
-    pw[q][0] = (uint32_t)w[0] | ((uint32_t)w[1] << 16);
-    pw[q][1] = (uint32_t)w[2] | ((uint32_t)w[3] << 16);
+    pw[q][0] = split_stacked<T>(p[0], p[1], k);
+    pw[q][1] = split_stacked<T>(p[2], p[3], k);
   }
   const u32x4 pb = {pw[0][0], pw[0][1], pw[1][0], pw[1][1]};
 #pragma unroll
-  for (int j = 0; j < 8; ++j) {
-    const u32x2 a0 = vop[0][j];
-    const u32x2 a1 = NG == 2 ? vop[NG - 1][j] : u32x2{0u, 0u};
-    st.o[j] = Mma<T>::qk(u32x4{a0.x, a0.y, a1.x, a1.y}, pb, st.o[j]);
+  for (int j = 0; j < 8; ++j) st.o[j] = Mma<T>::qk(vop[j], pb, st.o[j]);
+}
+
+// PV operands of one 32-token step: column-stacked (S, groups of at most 8
+// heads) or per 16-token group.  One softmax / PV call per step, whatever
+// the kind of the step's blocks, keeps the accumulators in one place: with
+// a call per kind, the compiler gave each its own output registers and
+// copied all 32 accumulator registers back at the top of every step.
+template <bool S>
+struct PvOps {
+  u32x4 v[8];
+};
+template <>
+struct PvOps<false> {
+  u32x2 v[2][8];
+};
+
+// NG = 1: the second group's operands are zero (its tokens are masked).
+template <bool BASE, int NG, bool S>
+__device__ __forceinline__ void pv_operands(const u32x4 (&v)[NG][4], PvOps<S>& o) {
+  if constexpr (S) {
+    v_operands_stacked<BASE, NG>(v, o.v);
+  } else {
+#pragma unroll
+    for (int q = 0; q < 2; ++q)
+#pragma unroll
+      for (int j = 0; j < 8; ++j) o.v[q][j] = q < NG ? v_operand<BASE>(v[q < NG ? q : 0], j) : u32x2{0u, 0u};
   }
+}
+
+template <typename T, int G, bool S>
+__device__ __forceinline__ void pv_step(SplitState& st, const f32x4 (&s)[2], const PvOps<S>& o, int tok0, int lim,
+                                        bool mask, float c, int g, int n) {
+  if constexpr (S) softmax_pv_stacked<T, 2, G>(st, s, o.v, tok0, lim, mask, c, g, n);
+  else softmax_pv<T, 2>(st, s, o.v, tok0, lim, mask, c, g);
 }
 
 // After column-stacked accumulation: column n (< G) gets its remainder

@@ -241,29 +241,26 @@ __device__ __forceinline__ void wait_vm(int n) {
   }
 }
 
-// As wait_vm, in steps of 4 (slots of the 8-bit format cost 4 or 8 loads).
+// As wait_vm, in steps of 4 (units of the 8-bit format cost 4 loads), as
+// one assembly block: a chain of scalar compares where the first level L
+// with n >= L waits for vmcnt <= L (never above n).  Written as a C switch
+// over its 16 levels, the compiler's control-flow structurizer made it a
+// long run of scalar instructions and taken branches on every step, which
+// the 8-bit elastic path (bound by instruction issue) paid for: 3 % at
+// BASE fraction 1.  n is at most 4 (units in the ring - 1) + the window's
+// loads, below 36 for rings of up to 4 slots.
+#define EKV_WAIT_LEVEL(lbl, cnt)                                         \
+  "s_cmp_lt_i32 %0, " #cnt "\n\t"                                        \
+  "s_cbranch_scc1 " #lbl "f\n\t"                                         \
+  "s_waitcnt vmcnt(" #cnt ")\n\t"                                        \
+  "s_branch 9f\n" #lbl ":\n\t"
 __device__ __forceinline__ void wait_vm4(int n) {
-  n = __builtin_amdgcn_readfirstlane(n);   // wave-uniform: scalar branches below
-  if (n >= 63) return;
-  switch (n >> 2) {
-    case 0: asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); break;
-    case 1: asm volatile("s_waitcnt vmcnt(4)" ::: "memory"); break;
-    case 2: asm volatile("s_waitcnt vmcnt(8)" ::: "memory"); break;
-    case 3: asm volatile("s_waitcnt vmcnt(12)" ::: "memory"); break;
-    case 4: asm volatile("s_waitcnt vmcnt(16)" ::: "memory"); break;
-    case 5: asm volatile("s_waitcnt vmcnt(20)" ::: "memory"); break;
-    case 6: asm volatile("s_waitcnt vmcnt(24)" ::: "memory"); break;
-    case 7: asm volatile("s_waitcnt vmcnt(28)" ::: "memory"); break;
-    case 8: asm volatile("s_waitcnt vmcnt(32)" ::: "memory"); break;
-    case 9: asm volatile("s_waitcnt vmcnt(36)" ::: "memory"); break;
-    case 10: asm volatile("s_waitcnt vmcnt(40)" ::: "memory"); break;
-    case 11: asm volatile("s_waitcnt vmcnt(44)" ::: "memory"); break;
-    case 12: asm volatile("s_waitcnt vmcnt(48)" ::: "memory"); break;
-    case 13: asm volatile("s_waitcnt vmcnt(52)" ::: "memory"); break;
-    case 14: asm volatile("s_waitcnt vmcnt(56)" ::: "memory"); break;
-    default: asm volatile("s_waitcnt vmcnt(60)" ::: "memory"); break;
-  }
+  n = __builtin_amdgcn_readfirstlane(n);
+  asm volatile(EKV_WAIT_LEVEL(1, 32) EKV_WAIT_LEVEL(2, 28) EKV_WAIT_LEVEL(3, 24) EKV_WAIT_LEVEL(4, 20)
+               EKV_WAIT_LEVEL(5, 16) EKV_WAIT_LEVEL(6, 12) EKV_WAIT_LEVEL(7, 8) EKV_WAIT_LEVEL(8, 4)
+               "s_waitcnt vmcnt(0)\n9:" ::"s"(n) : "memory", "scc");
 }
+#undef EKV_WAIT_LEVEL
 
 // ---- 8-bit TARGET / 4-bit BASE slots -------------------------------------
 // The ring is cut into 4 KiB units.  A TARGET pair takes two: its K and its
@@ -280,7 +277,8 @@ __device__ __forceinline__ void wait_vm4(int n) {
 __device__ __forceinline__ void dma_nibbles(const char* tile, const uint32_t (&nib)[2], char* dst) {
 #pragma unroll
   for (int r = 0; r < 2; ++r)
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile + nib[r]), (lds_ptr)(dst + 1024 * r), 16, 0, kStreamOnce);
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile + lane_offset(nib[r])), (lds_ptr)(dst + 1024 * r), 16,
+                                     0, kStreamOnce);
 }
 
 // A TARGET pair's tile: loads 0, 1 (member 0) from tile0, 2, 3 (member 1) from tile1.
@@ -288,7 +286,7 @@ __device__ __forceinline__ void dma_pair_bytes(const char* tile0, const char* ti
                                                char* dst) {
 #pragma unroll
   for (int r = 0; r < 4; ++r) {
-    const char* src = r < 2 ? tile0 + off[r] : tile1 + (off[r] - kTileBytes / 2);
+    const char* src = r < 2 ? tile0 + lane_offset(off[r]) : tile1 + lane_offset(off[r] - kTileBytes / 2);
     __builtin_amdgcn_global_load_lds(static_cast<const void*>(src), (lds_ptr)(dst + 1024 * r), 16, 0, kStreamOnce);
   }
 }
@@ -297,8 +295,8 @@ __device__ __forceinline__ void dma_pair_bytes(const char* tile0, const char* ti
 __device__ __forceinline__ void dma_member0_bytes(const char* tile0, const uint32_t (&off)[4], char* dst) {
 #pragma unroll
   for (int r = 0; r < 2; ++r)
-    __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile0 + off[r]), (lds_ptr)(dst + 1024 * r), 16, 0,
-                                     kStreamOnce);
+    __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile0 + lane_offset(off[r])), (lds_ptr)(dst + 1024 * r), 16,
+                                     0, kStreamOnce);
 }
 
 // 4 bytes of nibbles (element 2k low, 2k+1 high in byte k) -> 8 element
@@ -687,12 +685,17 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   int c_ops = ops_prologue;     // instructions issued up to and including the slot being consumed
   int ctag = 0;
   ModeInfo cmode = window_mode(sm.win[0], ctag);
+  // The softmax takes c = |scale| log2(e); a negative scale negates the
+  // query instead (a sign flip of each 16-bit word, exact).
+  const float c_scale = fabsf(a.scale_log2);
+  const uint32_t q_sign = a.scale_log2 < 0.f ? 0x80008000u : 0u;
   u32x4 qop[4];
   auto load_q = [&](const char* wb) {
 #pragma unroll
     for (int k = 0; k < 4; ++k)
-      qop[k] = (n < kQCols) ? *reinterpret_cast<const u32x4*>(wb + kWinQ + (n % G) * 2 * kHeadDim + 16 * (4 * g + k))
-                            : u32x4{0u, 0u, 0u, 0u};
+      qop[k] = (n < kQCols)
+                   ? (*reinterpret_cast<const u32x4*>(wb + kWinQ + (n % G) * 2 * kHeadDim + 16 * (4 * g + k)) ^ q_sign)
+                   : u32x4{0u, 0u, 0u, 0u};
   };
   load_q(sm.win[0]);
   int cb = ccur.b0;
@@ -773,10 +776,11 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       const char* kb = ring0 + kUnit * cslot;
       const char* vb = ring0 + kUnit * (cslot + 1 == 2 * NSLOT ? 0 : cslot + 1);
       f32x4 sc[2];
-      u32x2 vop[2][8];
+      PvOps<kStack> pvo;
       if (base) {
         // nibbles straight to 16-bit operand words (a BASE pair is two full
         // blocks: no tail to clear)
+        NibPlanes pv[2][4];
 #pragma unroll
         for (int m = 0; m < 2; ++m) {
           const char* mb = kb + m * (kTileBytes / 4);
@@ -785,11 +789,18 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
 #pragma unroll
           for (int q = 0; q < 4; ++q) kw[q] = nib_words(kn[q]);
           sc[m] = qk_scores<T, false>(kw, qop);
-          NibPlanes pv[4];
 #pragma unroll
-          for (int i = 0; i < 4; ++i) pv[i] = nib_planes(*reinterpret_cast<const uint32_t*>(mb + kTileBytes / 2 + rv4[i]));
+          for (int i = 0; i < 4; ++i)
+            pv[m][i] = nib_planes(*reinterpret_cast<const uint32_t*>(mb + kTileBytes / 2 + rv4[i]));
+        }
 #pragma unroll
-          for (int j = 0; j < 8; ++j) vop[m][j] = nib_v_operand(pv, j);
+        for (int j = 0; j < 8; ++j) {
+          const u32x2 a0 = nib_v_operand(pv[0], j), a1 = nib_v_operand(pv[1], j);
+          if constexpr (kStack) pvo.v[j] = u32x4{a0.x, a0.y, a1.x, a1.y};
+          else {
+            pvo.v[0][j] = a0;
+            pvo.v[1][j] = a1;
+          }
         }
       } else {
         u32x4 k[2][4], v[2][4];
@@ -808,11 +819,10 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
           sc[m] = qk_scores<T, true>(k[m], qop);
         }
         zero_tail_v<2>(v, cb * kPage, ccur.len, g);
-        v_operands<true, 2>(v, vop);
+        pv_operands<true, 2>(v, pvo);
       }
       const bool tail = cb * kPage + 2 * kPage > ccur.len;
-      if constexpr (kStack) softmax_pv_stacked<T, 2, G>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g, n);
-      else softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
+      pv_step<T, G>(st, sc, pvo, cb * kPage, ccur.len, tail, c_scale, g, n);
       cb += lone ? 1 : 2;
       const int units = base ? 1 : 2;
       n_consumed += units;
@@ -823,10 +833,16 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     wait_vm<NSLOT - 1>(ops - c_ops);
     EKV_TL(if (!tl_first) tl_first = __builtin_amdgcn_s_memrealtime();)
     const char* sb = sm.ring[cslot];
+    // Each kind of step leaves its scores and PV operands here; one softmax
+    // and PV call follows for all of them.  A step of one TARGET block (the
+    // lone last block, or any block with a ring of fewer than 4 slots) masks
+    // the empty second group through lim.
+    f32x4 sc[2];
+    PvOps<kStack> pvo;
+    int step_blocks = 2, step_slots = 1;
     if (block_is_base(cmode, ctag, ccur.b0, cb)) {
       // one packed pair: member 0 = logical block cb, member 1 = cb + 1
       u32x4 k[2][4], v[2][4];
-      f32x4 sc[2];
 #pragma unroll
       for (int m = 0; m < 2; ++m) {
         const char* mb = sb + m * (kTileBytes / 2);
@@ -840,13 +856,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
         for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mb + rv_b[i]);
         sc[m] = qk_scores<T, true>(k[m], qop);
       }
-      u32x2 vop[2][8];
-      v_operands<true, 2>(v, vop);
-      if constexpr (kStack) softmax_pv_stacked<T, 2, G>(st, sc, vop, cb * kPage, ccur.len, false, a.scale_log2, g, n);
-      else softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, false, a.scale_log2, g);
-      cb += 2;
-      ++n_consumed;
-      cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
+      pv_operands<true, 2>(v, pvo);
     } else if (NSLOT >= 4 && cb + 1 < ccur.b1) {
       // two TARGET blocks (the two members of a pair, in consecutive slots):
       // one softmax step over 32 tokens, two independent QK chains
@@ -865,33 +875,30 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
         v[0][i] = *reinterpret_cast<const u32x4*>(sb + rv_t[i]);
         v[1][i] = *reinterpret_cast<const u32x4*>(sb2 + rv_t[i]);
       }
-      const f32x4 sc[2] = {qk_scores<T, false>(k[0], qop), qk_scores<T, false>(k[1], qop)};
-      const bool tail = cb * kPage + 2 * kPage > ccur.len;
+      sc[0] = qk_scores<T, false>(k[0], qop);
+      sc[1] = qk_scores<T, false>(k[1], qop);
       zero_tail_v<2>(v, cb * kPage, ccur.len, g);
-      u32x2 vop[2][8];
-      v_operands<false, 2>(v, vop);
-      if constexpr (kStack) softmax_pv_stacked<T, 2, G>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g, n);
-      else softmax_pv<T, 2>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
-      cb += 2;
-      n_consumed += 2;
-      cslot = cslot2 + 1 == NSLOT ? 0 : cslot2 + 1;
+      pv_operands<false, 2>(v, pvo);
+      step_slots = 2;
     } else {
       u32x4 k[4], v[1][4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) k[q] = *reinterpret_cast<const u32x4*>(sb + rk_t[q]);
 #pragma unroll
       for (int i = 0; i < 4; ++i) v[0][i] = *reinterpret_cast<const u32x4*>(sb + rv_t[i]);
-      const f32x4 sc[1] = {qk_scores<T, false>(k, qop)};
-      const bool tail = cb * kPage + kPage > ccur.len;
+      sc[0] = qk_scores<T, false>(k, qop);
+      sc[1] = f32x4{0.f, 0.f, 0.f, 0.f};
       zero_tail_v<1>(v, cb * kPage, ccur.len, g);
-      u32x2 vop[1][8];
-      v_operands<false, 1>(v, vop);
-      if constexpr (kStack) softmax_pv_stacked<T, 1, G>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g, n);
-      else softmax_pv<T, 1>(st, sc, vop, cb * kPage, ccur.len, tail, a.scale_log2, g);
-      cb += 1;
-      ++n_consumed;
-      cslot = cslot + 1 == NSLOT ? 0 : cslot + 1;
+      pv_operands<false, 1>(v, pvo);
+      step_blocks = 1;
     }
+    const int lim = step_blocks == 1 ? min(ccur.len, cb * kPage + kPage) : ccur.len;
+    const bool mask = step_blocks == 1 || cb * kPage + 2 * kPage > ccur.len;
+    pv_step<T, G>(st, sc, pvo, cb * kPage, lim, mask, c_scale, g, n);
+    cb += step_blocks;
+    n_consumed += step_slots;
+    cslot += step_slots;
+    if (cslot >= NSLOT) cslot -= NSLOT;
     }   // 16-bit TARGET
     if (cb < ccur.b1) continue;
     // window finished

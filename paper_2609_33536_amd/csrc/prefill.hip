@@ -67,8 +67,6 @@ template <> struct Mma32<Fp16> {
 // upper half of the fp32 word (truncation), one byte permute for the pair.
 template <typename T>
 __device__ __forceinline__ void split_p(float p0, float p1, uint32_t& hi, uint32_t& lo);
-typedef __bf16 bf16x2v __attribute__((ext_vector_type(2)));
-typedef float f32x2v __attribute__((ext_vector_type(2)));
 
 template <>
 __device__ __forceinline__ void split_p<Bf16>(float p0, float p1, uint32_t& hi, uint32_t& lo) {
