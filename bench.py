@@ -143,6 +143,16 @@ def reduce_pmc(directory):
                 vals.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]) * 1024.0)
         return vals
 
+    def in_dispatch_order(run, counter, key):
+        """Bytes of the dispatches whose kernel name contains key, in launch order."""
+        path = os.path.join(directory, f"{run}_{counter}", "run_counter_collection.csv")
+        rows = []
+        with open(path) as f:
+            for r in csv.DictReader(f):
+                if key in r["Kernel_Name"]:
+                    rows.append((int(r["Dispatch_Id"]), float(r["Counter_Value"]) * 1024.0))
+        return [v for _, v in sorted(rows)]
+
     def log_json(run, key):
         with open(os.path.join(directory, f"{run}.log")) as f:
             for line in f:
@@ -156,22 +166,28 @@ def reduce_pmc(directory):
     for counter in ("FETCH_SIZE", "WRITE_SIZE"):
         c = [v for k, vs in per_kernel("pmc_copy", counter).items() if "copyBuffer" in k for v in vs]
         scale[counter] = copy["copy_calibration_bytes"] / (sum(c) / len(c))
-        d = [v for k, vs in per_kernel("pmc_dec", counter).items() if "decode_kernel" in k for v in vs]
+        d = in_dispatch_order("pmc_dec", counter, "decode_kernel")
         nf = len(dec["base_fractions"])
         rounds = len(d) // nf
         assert rounds * nf == len(d), (counter, len(d), nf)
         # launches rotate over the fractions; skip the first round (cold)
         per_launch[counter] = [float(np.mean(d[nf + i::nf])) * scale[counter] for i in range(nf)]
     hbm = [f + w for f, w in zip(per_launch["FETCH_SIZE"], per_launch["WRITE_SIZE"])]
+    # the roofline's kernel is the elastic one; the native launch (fraction 0) is listed beside it
+    el = [i for i, k in enumerate(dec["kernels"]) if k == "elastic"]
     out = {"source_digest": source_digest(),
-           "kernel": "decode_kernel<Bf16, 4, true, 4, false>",
-           "base_fractions": dec["base_fractions"],
+           "kernel": "decode_kernel<Bf16, 4, true, 4, false, false>",
+           "base_fractions": dec["base_fractions"], "kernels": dec["kernels"],
            "fetch_scale": round(scale["FETCH_SIZE"], 5), "write_scale": round(scale["WRITE_SIZE"], 5),
            "fetch_bytes": [round(v) for v in per_launch["FETCH_SIZE"]],
            "write_bytes": [round(v) for v in per_launch["WRITE_SIZE"]],
            "algorithmic_bytes": dec["bytes_per_launch"],
-           "hbm_bytes_per_launch": round(float(np.mean(hbm))),
-           "algorithmic_bytes_per_launch": round(float(np.mean(dec["bytes_per_launch"])))}
+           "hbm_bytes_per_launch": round(float(np.mean([hbm[i] for i in el]))),
+           "algorithmic_bytes_per_launch": round(float(np.mean([dec["bytes_per_launch"][i] for i in el])))}
+    if "native" in dec["kernels"]:
+        i = dec["kernels"].index("native")
+        out["native"] = {"hbm_bytes_per_launch": round(hbm[i]), "algorithmic_bytes_per_launch": dec["bytes_per_launch"][i],
+                         "hbm_over_algorithmic": round(hbm[i] / dec["bytes_per_launch"][i], 4)}
     out["hbm_over_algorithmic"] = round(out["hbm_bytes_per_launch"] / out["algorithmic_bytes_per_launch"], 4)
     with open(TRAFFIC_FILE, "w") as f:
         json.dump(out, f, indent=1)
@@ -296,15 +312,16 @@ def main():
     ws = torch.zeros(max(ekv.decode_workspace_bytes(kv.pool, bt) for kv, bt in zip(pools, batches)),
                      dtype=torch.uint8, device="cuda")
 
-    if args.decode_only:
+    if args.decode_only:   # (counter runs: every fraction in rotation, the native launch included)
         for _ in range(args.warmup + args.steps):
-            for k in ELASTIC:
+            for k in range(len(FRACTIONS)):
                 ekv.attn_decode(pools[k].pool, batches[k], q, outs[k], scale, ws)
         torch.cuda.synchronize()
         print(json.dumps({"decode_only_rounds": args.warmup + args.steps,
-                          "base_fractions": [FRACTIONS[k] for k in ELASTIC],
+                          "base_fractions": list(FRACTIONS),
+                          "kernels": ["elastic" if k in ELASTIC else "native" for k in range(len(FRACTIONS))],
                           "bytes_per_launch": [decode_bytes(seq_lens, pools[k].mirror.tags, HQ, HKV,
-                                                            dec["modes"][k]) for k in ELASTIC]}))
+                                                            dec["modes"][k]) for k in range(len(FRACTIONS))]}))
         return 0
 
     print("[bench] building the prefill workload", file=sys.stderr, flush=True)
@@ -423,7 +440,7 @@ def main():
         "roofline": {"bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
                      "frac": round(achieved / HBM_PEAK_GBS, 4),
                      "traffic": (traffic["hbm_bytes_per_launch"] if traffic else None),
-                     "kernel": "decode_kernel<Bf16, 4, true, 4, false> (ekv_attn_decode, 16-bit elastic path)",
+                     "kernel": "decode_kernel<Bf16, 4, true, 4, false, false> (ekv_attn_decode, 16-bit elastic path)",
                      "algorithmic_bytes_per_launch": round(sum(decode_bytes_f[k] for k in ELASTIC) / len(ELASTIC)),
                      "avg_launch_ms": round(sum(el_ms) / len(el_ms), 5)},
     }
@@ -432,6 +449,7 @@ def main():
             "mean over the f=0.25/0.5/1 launches of PMC FETCH_SIZE and WRITE_SIZE, each scaled by "
             "what it reads for a 1 GiB device copy")
     result["native_dispatch"] = native_dispatch(torch, ekv, pools[FRACTIONS.index(0.0)], q, outs[0], scale, stream)
+    result["decode_append"] = decode_append(torch, ekv, pools[FRACTIONS.index(0.5)], q, scale, stream)
     print("[bench] 70B-shaped decode layer", file=sys.stderr, flush=True)
     result["decode_70b"] = decode_70b(torch, ekv, kvpool, workloads, stream, scale)
     result["controller"] = controller_cost(ekv, tpool.mirror)
@@ -474,6 +492,43 @@ def native_dispatch(torch, ekv, kv, q, out, scale, stream, reps=30):
     med = {k: float(np.median([a.elapsed_time(b) for a, b in v])) for k, v in times.items()}
     return {"native_ms": round(med["native"], 5), "elastic_forced_ms": round(med["elastic"], 5),
             "ratio": round(med["native"] / med["elastic"], 4), "acceptance": "ratio <= 1.02"}
+
+
+def decode_append(torch, ekv, kv, q, scale, stream, reps=30):
+    """Append each sequence's newest token and decode, on the 8B layer at BASE
+    fraction 0.5: ekv_append_kv then ekv_attn_decode, against the one launch
+    of ekv_attn_decode_append (alternating; median event times around each).
+    Both write the same rows, so the pool's contents do not change between
+    repetitions."""
+    gen = torch.Generator(device="cuda")
+    gen.manual_seed(SEED + 11)
+    k_new = torch.randn((B, HKV, D), generator=gen, device="cuda").to(torch.bfloat16)
+    v_new = torch.randn((B, HKV, D), generator=gen, device="cuda").to(torch.bfloat16)
+    lens = kv.mirror.seq_lens
+    slots = torch.tensor([int(kv.mirror.bt[s, (int(l) - 1) // PAGE]) * PAGE + (int(l) - 1) % PAGE
+                          for s, l in enumerate(lens)], dtype=torch.int32, device="cuda")
+    batch = kv.batch(HQ)
+    ws = ekv.decode_workspace(kv.pool, batch)
+    out = torch.empty((B, HQ, D), dtype=torch.bfloat16, device="cuda")
+    two, one = [], []
+    for r in range(reps + 3):
+        for fused in (False, True):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record(stream)
+            if fused:
+                ekv.attn_decode_append(kv.pool, batch, q, k_new, v_new, out, scale, ws)
+            else:
+                ekv.append_kv(kv.pool, slots, k_new, v_new)
+                ekv.attn_decode(kv.pool, batch, q, out, scale, ws)
+            e1.record(stream)
+            e1.synchronize()
+            if r >= 3:
+                (one if fused else two).append(e0.elapsed_time(e1))
+    return {"workload": "8B decode layer at BASE fraction 0.5 (general), newest token of each of the 64 "
+                        "sequences appended",
+            "append_then_decode_ms": round(float(np.median(two)), 5),
+            "fused_ms": round(float(np.median(one)), 5),
+            "saved_ms": round(float(np.median(two)) - float(np.median(one)), 5)}
 
 
 def decode_timeline(torch, ekv, kvpool, workloads, stream, scale, reps=5):

@@ -200,6 +200,26 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
                            hipStream_t stream);
 
 /*
+ * Append, then decode, in one launch (§3.2: a decoded token's new K/V
+ * enter in TARGET form, and the step's attention reads them).  The same
+ * result, output and pool, as ekv_append_kv of each sequence's newest token
+ * followed by ekv_attn_decode: for every s with seq_lens[s] >= 1, the token
+ * at position p = seq_lens[s] - 1 takes k_new[s] / v_new[s], written to
+ * block block_table[s][p / page_size], offset p % page_size, and the
+ * attention over seq_lens[s] tokens reads these rows.  (seq_lens counts the
+ * new token.)  The block of p must be TARGET, as for ekv_append_kv; a
+ * sequence whose block of p is BASE is neither written nor patched (its
+ * decode reads the pool as it is).
+ *   k_new, v_new  device [batch][num_kv_heads][head_dim], pool dtype (bytes
+ *                 for an 8-bit pool); read only
+ * Other arguments as ekv_attn_decode; the pool is written.
+ * Errors: as ekv_attn_decode (also EKV_ERR_INVALID for NULL k_new / v_new).
+ */
+ekv_status ekv_attn_decode_append(const ekv_pool* pool, const ekv_batch* batch, const void* q,
+                                  const void* k_new, const void* v_new, void* out, int32_t out_dtype,
+                                  float scale, void* ws, size_t ws_bytes, hipStream_t stream);
+
+/*
  * ekv_attn_decode without a caller workspace and without any allocation,
  * for callers that cannot allocate device memory: code under HIP graph
  * capture, tight serving loops, harnesses that forbid allocation.  The

@@ -271,13 +271,14 @@ ekv_status debug_check_list(const ekv_pool* pool, int kind, int n, const int32_t
 // and which the EKV_DEBUG checks do not use (they allocate).
 ekv_status decode_call(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out, int32_t out_dtype,
                        float scale, void* ws, size_t ws_bytes, bool clear_counters, hipStream_t stream,
-                       const char* who) {
+                       const char* who, const void* k_new = nullptr, const void* v_new = nullptr) {
   ekv_status st = check_pool(pool);
   if (st != EKV_OK) return st;
   int group = 0;
   if ((st = check_attention_batch(pool, batch, &group)) != EKV_OK) return st;
   if (batch->batch == 0) return EKV_OK;
   if (!q || !out) return fail(EKV_ERR_INVALID, "q and out are required");
+  if ((k_new == nullptr) != (v_new == nullptr)) return fail(EKV_ERR_INVALID, "%s: k_new and v_new go together", who);
   const int q_dtype = pool->dtype == EKV_DTYPE_E5M2 ? EKV_DTYPE_FP16 : pool->dtype;   // 8-bit pools: FP16 queries
   if (out_dtype != q_dtype && out_dtype != EKV_DTYPE_FP32)
     return fail(EKV_ERR_INVALID, "out_dtype must be the query dtype or fp32");
@@ -318,6 +319,9 @@ ekv_status decode_call(const ekv_pool* pool, const ekv_batch* batch, const void*
   a.out_fp32 = out_dtype == EKV_DTYPE_FP32;
   a.slots = decode_slots(pool, group, elastic);
   a.scale_log2 = log2e_scale(scale);
+  a.k_new = k_new;
+  a.v_new = v_new;
+  a.pool_out = k_new ? pool->kv : nullptr;
   if (clear_counters &&
       (st = hip_status(ekv::launch_zero_u32(a.counters, 2 * (size_t)plan.grid, stream), "scratch clear")) != EKV_OK)
     return st;
@@ -425,6 +429,16 @@ ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const v
                            hipStream_t stream) {
   return ekv::guard("ekv_attn_decode", [&]() -> ekv_status {
     return decode_call(pool, batch, q, out, out_dtype, scale, ws, ws_bytes, false, stream, "ekv_attn_decode");
+  });
+}
+
+ekv_status ekv_attn_decode_append(const ekv_pool* pool, const ekv_batch* batch, const void* q, const void* k_new,
+                                  const void* v_new, void* out, int32_t out_dtype, float scale, void* ws,
+                                  size_t ws_bytes, hipStream_t stream) {
+  return ekv::guard("ekv_attn_decode_append", [&]() -> ekv_status {
+    if (!k_new || !v_new) return fail(EKV_ERR_INVALID, "ekv_attn_decode_append: k_new and v_new are required");
+    return decode_call(pool, batch, q, out, out_dtype, scale, ws, ws_bytes, false, stream, "ekv_attn_decode_append",
+                       k_new, v_new);
   });
 }
 

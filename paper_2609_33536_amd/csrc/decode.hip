@@ -389,7 +389,7 @@ struct alignas(16) DecodeSmem {
 // written out directly; one cut by range ends leaves one partial per piece,
 // and the last piece to arrive merges them (after its stream has ended).
 // ---------------------------------------------------------------------------
-template <typename T, int G, bool ELASTIC, int NSLOT, bool F8>
+template <typename T, int G, bool ELASTIC, int NSLOT, bool F8, bool FUSED>
 __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   __shared__ DecodeSmem<G, ELASTIC, NSLOT> sm;
   // query groups of at most 8 heads hold each head in two MFMA columns
@@ -553,6 +553,44 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
                            : (blk >= m.base_lo && blk < m.base_hi);
   };
 
+  // ---- fused append ------------------------------------------------------
+  // The newest token of a sequence (position len - 1) takes its K / V rows
+  // from k_new / v_new.  Its block is TARGET (a caller's invariant; a BASE
+  // block is left as it is).  The issue side follows that block's tile loads
+  // with two loads of the new rows into the same slot, at the token's row:
+  // loads return in order, so they overwrite the pool's old row there.  The
+  // consume side, which owns the block's (sequence, KV head) tile in this
+  // launch, writes the rows from LDS to the pool.  One row is 2 x 128 words
+  // (16 lanes x 16 B) or, for 8-bit pools, 2 x 128 bytes (8 lanes x 16 B).
+  constexpr bool fused = FUSED;   // (a separate instance: the plain decode keeps none of this code)
+  constexpr int kRowBytes = F8 ? kHeadDim : 2 * kHeadDim;
+  constexpr int kRowLanes = kRowBytes / 16;
+  auto patched = [&](int len, int blk, bool base) -> bool { return fused && !base && blk == (len - 1) / kPage; };
+  // chunk of the row that lane i moves: the one the slot's swizzle puts at i
+  auto row_chunk = [&](int t) -> int { return F8 ? (lane ^ tau(t)) : (lane ^ t); };
+  auto dma_new_row = [&](int s, int kvh, int t, char* k_row, char* v_row) {
+    if (lane < kRowLanes) {
+      const size_t off = ((size_t)s * hkv + kvh) * kRowBytes + 16 * row_chunk(t);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(static_cast<const char*>(a.k_new) + off), (lds_ptr)k_row,
+                                       16, 0, 0);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(static_cast<const char*>(a.v_new) + off), (lds_ptr)v_row,
+                                       16, 0, 0);
+    }
+    ops += 2;
+  };
+  // the rows, from the slot (k_row, v_row: their LDS addresses) to the pool
+  auto store_new_row = [&](int phys, int kvh, int t, const char* k_row, const char* v_row) {
+    if (lane < kRowLanes) {
+      const u32x4 kr = *reinterpret_cast<const u32x4*>(k_row + 16 * lane);
+      const u32x4 vr = *reinterpret_cast<const u32x4*>(v_row + 16 * lane);
+      constexpr size_t kTileP = F8 ? kTileBytes / 2 : kTileBytes;
+      char* dst = static_cast<char*>(a.pool_out) + (size_t)phys * 2 * hkv * kTileP + (size_t)kvh * kTileP +
+                  (size_t)t * kRowBytes + 16 * row_chunk(t);
+      *reinterpret_cast<u32x4*>(dst) = kr;
+      *reinterpret_cast<u32x4*>(dst + (size_t)hkv * kTileP) = vr;
+    }
+  };
+
   // per-lane LDS read offsets inside a slot (see the swizzle above)
   uint32_t rk_t[4], rv_t[4], rk_b[2], rv_b[4];
 #pragma unroll
@@ -641,23 +679,31 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
         ops += 4;
         ib += 2;
         units = 1;
-      } else if (ib + 1 < icur.b1) {
-        // a whole TARGET pair: member m's rows from its own block, in the
-        // layout of a 16-bit packed BASE pair (bytes, member-major)
-        int phys1 = __builtin_amdgcn_readlane(bt_lane, ib + 1 - icur.b0);
-        phys1 = (unsigned)phys1 < (unsigned)a.num_blocks ? phys1 : 0;
-        const char* src1 = reinterpret_cast<const char*>(a.pool) + (size_t)phys1 * block_bytes +
-                           (size_t)icur.kvh * kTile;
-        dma_pair_bytes(src, src1, dma.base, dk);
-        dma_pair_bytes(src + v_off, src1 + v_off, dma.base, dv);
-        ops += 8;
-        ib += 2;
       } else {
-        // the sequence's last block, alone: member 0 only
-        dma_member0_bytes(src, dma.base, dk);
-        dma_member0_bytes(src + v_off, dma.base, dv);
-        ops += 4;
-        ib += 1;
+        const bool pair = ib + 1 < icur.b1;
+        if (pair) {
+          // a whole TARGET pair: member m's rows from its own block, in the
+          // layout of a 16-bit packed BASE pair (bytes, member-major)
+          int phys1 = __builtin_amdgcn_readlane(bt_lane, ib + 1 - icur.b0);
+          phys1 = (unsigned)phys1 < (unsigned)a.num_blocks ? phys1 : 0;
+          const char* src1 = reinterpret_cast<const char*>(a.pool) + (size_t)phys1 * block_bytes +
+                             (size_t)icur.kvh * kTile;
+          dma_pair_bytes(src, src1, dma.base, dk);
+          dma_pair_bytes(src + v_off, src1 + v_off, dma.base, dv);
+          ops += 8;
+        } else {
+          // the sequence's last block, alone: member 0 only
+          dma_member0_bytes(src, dma.base, dk);
+          dma_member0_bytes(src + v_off, dma.base, dv);
+          ops += 4;
+        }
+        for (int m = 0; m < (pair ? 2 : 1); ++m)
+          if (patched(icur.len, ib + m, false)) {
+            const int t = (icur.len - 1) % kPage;
+            dma_new_row(icur.s, icur.kvh, t, dk + m * (kTileBytes / 2) + t * kRowBytes,
+                        dv + m * (kTileBytes / 2) + t * kRowBytes);
+          }
+        ib += pair ? 2 : 1;
       }
       islot += units;
       if (islot >= 2 * NSLOT) islot -= 2 * NSLOT;
@@ -671,6 +717,10 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
         dma_tile(src + v_off, dma.tgt, dst + kTileBytes);
       }
       ops += 8;
+      if (patched(icur.len, ib, base)) {
+        const int t = (icur.len - 1) % kPage;
+        dma_new_row(icur.s, icur.kvh, t, dst + t * kRowBytes, dst + kTileBytes + t * kRowBytes);
+      }
       ib += base ? 2 : 1;
       islot = islot + 1 == NSLOT ? 0 : islot + 1;
       ++n_issued;
@@ -698,6 +748,13 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
                    : u32x4{0u, 0u, 0u, 0u};
   };
   load_q(sm.win[0]);
+  // physical block of block blk of the consume side's window (for the fused
+  // append's write to the pool)
+  auto window_block = [&](int blk) -> int {
+    const int e = *reinterpret_cast<const int*>(sm.win[cw_idx % (NSLOT + 1)] + kWinBt + 4 * (blk - ccur.b0));
+    const int phys = __builtin_amdgcn_readfirstlane(e);
+    return (unsigned)phys < (unsigned)a.num_blocks ? phys : 0;
+  };
   int cb = ccur.b0;
   int cslot = 0;
   int piece_j0 = ccur.j0;
@@ -770,11 +827,21 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       const bool base = block_is_base(cmode, ctag, ccur.b0, cb);
       const bool lone = !base && cb + 1 >= ccur.b1;
       c_ops += (base || lone) ? 4 : 8;
+      int new_member = -1;   // fused append: the member holding the newest token
+      if (!base)
+        for (int m = 0; m < (lone ? 1 : 2); ++m)
+          if (patched(ccur.len, cb + m, false)) new_member = m;
+      if (new_member >= 0) c_ops += 2;
       wait_vm4(ops - c_ops);
       EKV_TL(if (!tl_first) tl_first = __builtin_amdgcn_s_memrealtime();)
       const char* ring0 = &sm.ring[0][0];
       const char* kb = ring0 + kUnit * cslot;
       const char* vb = ring0 + kUnit * (cslot + 1 == 2 * NSLOT ? 0 : cslot + 1);
+      if (new_member >= 0) {
+        const int t = (ccur.len - 1) % kPage;
+        const int mo = new_member * (kTileBytes / 2) + t * kRowBytes;
+        store_new_row(window_block(cb + new_member), ccur.kvh, t, kb + mo, vb + mo);
+      }
       f32x4 sc[2];
       PvOps<kStack> pvo;
       if (base) {
@@ -830,9 +897,14 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       if (cslot >= 2 * NSLOT) cslot -= 2 * NSLOT;
     } else {
     c_ops += 8;
+    const bool base0 = block_is_base(cmode, ctag, ccur.b0, cb);
+    const bool new0 = patched(ccur.len, cb, base0);   // fused append: the newest token is in block cb
+    if (new0) c_ops += 2;
     wait_vm<NSLOT - 1>(ops - c_ops);
     EKV_TL(if (!tl_first) tl_first = __builtin_amdgcn_s_memrealtime();)
     const char* sb = sm.ring[cslot];
+    const int t_new = (ccur.len - 1) % kPage;
+    if (new0) store_new_row(window_block(cb), ccur.kvh, t_new, sb + t_new * kRowBytes, sb + kTileBytes + t_new * kRowBytes);
     // Each kind of step leaves its scores and PV operands here; one softmax
     // and PV call follows for all of them.  A step of one TARGET block (the
     // lone last block, or any block with a ring of fewer than 4 slots) masks
@@ -840,7 +912,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     f32x4 sc[2];
     PvOps<kStack> pvo;
     int step_blocks = 2, step_slots = 1;
-    if (block_is_base(cmode, ctag, ccur.b0, cb)) {
+    if (base0) {
       // one packed pair: member 0 = logical block cb, member 1 = cb + 1
       u32x4 k[2][4], v[2][4];
 #pragma unroll
@@ -862,8 +934,13 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       // one softmax step over 32 tokens, two independent QK chains
       const int cslot2 = cslot + 1 == NSLOT ? 0 : cslot + 1;
       c_ops += 8;
+      const bool new1 = patched(ccur.len, cb + 1, false);
+      if (new1) c_ops += 2;
       wait_vm<NSLOT - 2>(ops - c_ops);
       const char* sb2 = sm.ring[cslot2];
+      if (new1)
+        store_new_row(window_block(cb + 1), ccur.kvh, t_new, sb2 + t_new * kRowBytes,
+                      sb2 + kTileBytes + t_new * kRowBytes);
       u32x4 k[2][4], v[2][4];
 #pragma unroll
       for (int q = 0; q < 4; ++q) {
@@ -977,8 +1054,8 @@ int resident_groups(K kernel, std::atomic<int>* cache) {
 template <typename T, int G, int NSLOT, bool F8>
 hipError_t run_slots(const DecodeArgs& a, bool elastic, hipStream_t st, int* grid_out) {
   static std::atomic<int> cache[2][kMaxDevices];
-  auto kernel = elastic ? decode_kernel<T, G, true, NSLOT, F8> : decode_kernel<T, G, false, NSLOT, F8>;
-  if (grid_out) {
+  auto kernel = elastic ? decode_kernel<T, G, true, NSLOT, F8, false> : decode_kernel<T, G, false, NSLOT, F8, false>;
+  if (grid_out) {   // (the grid of the plain decode; the fused instance has the same registers and LDS)
     const int resident = resident_groups(kernel, cache[elastic ? 1 : 0]);
     if (resident <= 0) return hipErrorInvalidDeviceFunction;
     const long long wanted = (a.pairs_max + a.min_chunk - 1) / a.min_chunk;
@@ -986,6 +1063,8 @@ hipError_t run_slots(const DecodeArgs& a, bool elastic, hipStream_t st, int* gri
     return hipSuccess;
   }
   if (a.grid <= 0) return hipErrorInvalidValue;
+  if (a.k_new)
+    kernel = elastic ? decode_kernel<T, G, true, NSLOT, F8, true> : decode_kernel<T, G, false, NSLOT, F8, true>;
   hipLaunchKernelGGL(kernel, dim3(a.grid), dim3(64), 0, st, a);
   return hipGetLastError();
 }

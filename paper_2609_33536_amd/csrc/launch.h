@@ -27,6 +27,13 @@ struct DecodeArgs {
   int32_t out_fp32;
   int32_t slots;             // LDS ring depth per wave (2..6)
   float scale_log2;          // softmax scale * log2(e)
+  // Fused append (null otherwise): the K / V rows of each sequence's newest
+  // token (position seq_lens[s] - 1), [B][Hkv][128] in the pool's element
+  // type, replace that token's rows where decode reads them and are written
+  // to the pool (pool_out: the same pool, writable).
+  const void* k_new;
+  const void* v_new;
+  void* pool_out;
 };
 
 // Most workgroups one decode launch uses (a cap on the resident grid).

@@ -71,6 +71,8 @@ SIGNATURES = {
     "ekv_decode_workspace_bytes": (_U, [ctypes.POINTER(Pool), ctypes.POINTER(Batch)]),
     "ekv_decode_workspace_init": (_I, [_P, _U, _S]),
     "ekv_attn_decode": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _F, _P, _U, _S]),
+    "ekv_attn_decode_append": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _P, _P, _I, _F, _P,
+                                    ctypes.c_size_t, _S]),
     "ekv_attn_decode_noalloc": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _F, _S]),
     "ekv_attn_prefill": (_I, [ctypes.POINTER(Pool), ctypes.POINTER(Batch), _P, _P, _I, _I, _P, _I, _F, _S]),
     "ekv_append_kv": (_I, [ctypes.POINTER(Pool), _P, _P, _P, _I, _S]),
@@ -197,6 +199,13 @@ def attn_decode(pool, batch, q, out, scale, ws, stream=None):
     _check(lib().ekv_attn_decode(ctypes.byref(pool), ctypes.byref(batch), _ptr(q), _ptr(out),
                                  dtype_code(out.dtype), scale, _ptr(ws), ws.numel() * ws.element_size(),
                                  _stream(stream)))
+
+
+def attn_decode_append(pool, batch, q, k_new, v_new, out, scale, ws, stream=None):
+    """Append each sequence's newest token (k_new / v_new [B][Hkv][D]) and decode, in one launch."""
+    _check(lib().ekv_attn_decode_append(ctypes.byref(pool), ctypes.byref(batch), _ptr(q), _ptr(k_new), _ptr(v_new),
+                                        _ptr(out), dtype_code(out.dtype), scale, _ptr(ws),
+                                        ws.numel() * ws.element_size(), _stream(stream)))
 
 
 def attn_decode_noalloc(pool, batch, q, out, scale, stream=None):
