@@ -156,6 +156,11 @@ void arguments() {
          "decode small workspace", 0);
   expect(ekv_attn_decode(nullptr, &batch, host, host, 0, 1.f, host, need, nullptr) == EKV_ERR_INVALID, "decode NULL", 0);
   expect(ekv_attn_decode(&pool, &batch, host, host, 0, NAN, host, need, nullptr) == EKV_ERR_INVALID, "decode scale", 0);
+  expect(ekv_attn_decode_append(&pool, &batch, host, nullptr, host, host, 0, 1.f, host, need, nullptr) == EKV_ERR_INVALID,
+         "decode_append without k_new", 0);
+  expect(ekv_attn_decode_append(&pool, &batch, host, host, host, host, 0, 1.f, host, need - 1, nullptr) ==
+             EKV_ERR_INVALID,
+         "decode_append small workspace", 0);
   ekv_pool bad = pool;
   bad.head_dim = 64;
   expect(ekv_attn_prefill(&bad, &batch, host, lens, 1, 1, host, 0, 1.f, nullptr) == EKV_ERR_UNSUPPORTED, "prefill dim", 0);
