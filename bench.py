@@ -75,6 +75,8 @@ def parse():
                     help="only the chunked-prefill launches (for PMC counters of that kernel)")
     ap.add_argument("--pressure-only", action="store_true",
                     help="only the pressure-transition mix (for PMC counters of demote / refine)")
+    ap.add_argument("--decode-8bit-only", action="store_true",
+                    help="only the 8-bit TARGET / 4-bit BASE decode leg (for counter runs)")
     ap.add_argument("--decode-70b-only", action="store_true",
                     help="only the 70B-shaped decode layer (for PMC counters of that launch)")
     ap.add_argument("--timeline", action="store_true",
@@ -288,6 +290,11 @@ def main():
     if args.pressure_only:
         print(json.dumps({"pressure_mix": pressure_mix(torch, ekv, kvpool, workloads, stream, scale,
                                                        steps=max(1, args.steps))}))
+        return 0
+    if args.decode_8bit_only:
+        lens = workloads.seq_lens_uniform(np.random.default_rng(SEED), B, 2048, 8192)
+        print(json.dumps({"decode_8bit": decode_8bit(torch, ekv, kvpool, workloads, stream, lens, scale,
+                                                     reps=max(1, args.steps))}))
         return 0
     if args.decode_70b_only:
         print(json.dumps({"decode_70b": decode_70b(torch, ekv, kvpool, workloads, stream, scale,
