@@ -37,9 +37,9 @@
  *     never synchronises; errors detected on the host are returned before
  *     anything is enqueued; a launch failure returns EKV_ERR_HIP.
  *   - The library allocates no device memory.  Scratch space is passed in
- *     by the caller (see ekv_decode_workspace_bytes).  The one exception
- *     is the EKV_DEBUG=1 mode of ekv_validate_batch, which also
- *     synchronises.
+ *     by the caller (see ekv_decode_workspace_bytes), or is a static array
+ *     inside the library (ekv_attn_decode_noalloc; the EKV_DEBUG report).
+ *     The EKV_DEBUG=1 mode (below) synchronises.
  *   - Host-side checks cover shapes and pointers.  Checks that need the
  *     contents of device arrays (a tag that differs inside a pair, an
  *     already-BASE pair in a demotion list) are done by the ekv_check_*
@@ -401,8 +401,9 @@ ekv_status ekv_check_transition(int32_t kind, const int32_t* h_pairs, int32_t n,
  * With EKV_DEBUG=1 in the environment, ekv_attn_decode, ekv_attn_prefill
  * and every transition call run these checks first, synchronise the stream,
  * and return EKV_ERR_INVALID (naming the first violation) without
- * enqueuing anything else.  That mode allocates one report buffer per
- * device on first use and is meant for debugging only.
+ * enqueuing anything else.  That mode reports into a static 48-byte device
+ * array of the library (one per device; calls in this mode from several
+ * host threads on one device race on it) and is meant for debugging only.
  */
 enum {
   EKV_VIOL_SEQ_LEN = 0,       /* seq_lens[s] < 0, or beyond max_blocks*page_size or max_seq_len */

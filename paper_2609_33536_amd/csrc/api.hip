@@ -211,21 +211,26 @@ hipError_t enqueue_validate_batch(const ekv_pool* pool, const ekv_batch* batch, 
   return ekv::launch_validate_batch(a, stream);
 }
 
-// The report buffer of the debug mode: one per device, allocated on first use.
+// The report buffer of the debug mode: a static device array (one per
+// device, looked up like the scratch above), so that the debug mode
+// allocates nothing either.  Debug-mode calls synchronise before they read
+// it; calls that overlap on one device from several host threads race on it.
+static __device__ __align__(16) int32_t debug_report[2 * EKV_VIOL_COUNT];
+
 ekv_status debug_report_buffer(int32_t** out) {
   static std::mutex mu;
-  static std::vector<int32_t*> buffers;
+  static void* addr[kScratchDevices] = {};
   int dev = 0;
   if (hipGetDevice(&dev) != hipSuccess) return hip_status(hipGetLastError(), "hipGetDevice");
+  if (dev < 0 || dev >= kScratchDevices) return fail(EKV_ERR_UNSUPPORTED, "device %d: at most %d devices", dev, kScratchDevices);
   std::lock_guard<std::mutex> lock(mu);
-  if ((int)buffers.size() <= dev) buffers.resize(dev + 1, nullptr);
-  if (!buffers[dev]) {
-    void* p = nullptr;
-    const hipError_t e = hipMalloc(&p, 2 * EKV_VIOL_COUNT * sizeof(int32_t));
-    if (e != hipSuccess) return hip_status(e, "EKV_DEBUG report buffer");
-    buffers[dev] = static_cast<int32_t*>(p);
+  if (!addr[dev]) {
+    void* ptr = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&ptr, HIP_SYMBOL(debug_report));
+    if (e != hipSuccess) return hip_status(e, "hipGetSymbolAddress(debug_report)");
+    addr[dev] = ptr;
   }
-  *out = buffers[dev];
+  *out = static_cast<int32_t*>(addr[dev]);
   return EKV_OK;
 }
 
@@ -267,8 +272,9 @@ ekv_status debug_check_list(const ekv_pool* pool, int kind, int n, const int32_t
 }
 
 // One decode call on a workspace: the caller's, or (clear_counters) the
-// static scratch, whose merge counters are zeroed first by a fill kernel
-// and which the EKV_DEBUG checks do not use (they allocate).
+// static scratch, whose merge counters are zeroed first by a fill kernel;
+// that call runs no EKV_DEBUG checks (they synchronise the stream, which
+// its callers -- graph capture among them -- cannot have).
 ekv_status decode_call(const ekv_pool* pool, const ekv_batch* batch, const void* q, void* out, int32_t out_dtype,
                        float scale, void* ws, size_t ws_bytes, bool clear_counters, hipStream_t stream,
                        const char* who, const void* k_new = nullptr, const void* v_new = nullptr) {
@@ -292,7 +298,7 @@ ekv_status decode_call(const ekv_pool* pool, const ekv_batch* batch, const void*
   if ((st = plan_decode(pool, batch, group, true, &plan)) != EKV_OK) return st;
   if (plan.total > ws_bytes)   // (the static scratch: sized by the device's own grid)
     return fail(EKV_ERR_UNSUPPORTED, "%s: needs %zu bytes of scratch, %zu available", who, plan.total, ws_bytes);
-  // (the debug checks allocate their report buffer: not for the static scratch)
+  // (the debug checks synchronise: not for the no-allocation call)
   if (!clear_counters && debug_mode() && (st = debug_check_batch(pool, batch, stream, who)) != EKV_OK) return st;
   const bool elastic = batch->mode != EKV_MODE_NATIVE;
   ekv::DecodeArgs a{};
