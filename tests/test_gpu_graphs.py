@@ -84,6 +84,62 @@ def test_decode_and_prefill_replay_from_a_graph():
         assert torch.isfinite(got).all() and torch.isfinite(pgot).all()
 
 
+def test_decode_append_replays_from_a_graph():
+    """The fused append + decode captured once and replayed with new query
+    and new K/V rows: every replay equals the eager call, output and pool
+    (the newest tokens' rows in the pool are those of the replay)."""
+    torch = require_gpu()
+    rng = np.random.default_rng(65)
+    c = workloads.make_decode_case([300, 1500, 64, 2047, 17], 16, 4, seed=65, base_fraction=0.5,
+                                   spare_blocks=4)
+    lens = c["seq_lens"]
+    pairs = c["pairs"]
+    pairs = pairs[pairs[:, 1] != (lens[pairs[:, 0]] - 1) // 32]   # the newest token's pair stays TARGET
+    kv = kvpool.PagedKV(c["pool"], c["block_table"], lens, c["free"], 4)
+    kv.demote(pairs)
+    kv.commit()
+    kv.relower()
+    batch = kv.batch(16)
+    ws = ekv.decode_workspace(kv.pool, batch)
+    q = words_to_tensor(c["q"], torch, "bf16").clone()
+    kn = torch.zeros((5, 4, 128), dtype=torch.bfloat16, device="cuda")
+    vn = torch.zeros_like(kn)
+    out = torch.empty((5, 16, 128), dtype=torch.float32, device="cuda")
+    scale = default_scale()
+
+    def step():
+        ekv.attn_decode_append(kv.pool, batch, q, kn, vn, out, scale, ws)
+
+    side = torch.cuda.Stream()
+    side.wait_stream(torch.cuda.current_stream())
+    with torch.cuda.stream(side):
+        step()
+    torch.cuda.current_stream().wait_stream(side)
+    torch.cuda.synchronize()
+    graph = torch.cuda.CUDAGraph()
+    print("graph: capturing decode_append", flush=True)
+    with torch.cuda.graph(graph):
+        step()
+    torch.cuda.synchronize()
+    new = lambda shape: words_to_tensor(workloads.to_words(rng.standard_normal(shape, dtype=np.float32), "bf16"),
+                                        torch, "bf16")
+    for replay in range(4):
+        q.copy_(new(q.shape))
+        kn.copy_(new(kn.shape))
+        vn.copy_(new(vn.shape))
+        torch.cuda.synchronize()
+        print(f"graph: replay {replay}", flush=True)
+        graph.replay()
+        torch.cuda.synchronize()
+        got, pool_got = out.clone(), kv.kv.clone()
+        out.fill_(float("nan"))
+        step()
+        torch.cuda.synchronize()
+        assert torch.equal(got, out), f"replay {replay} differs from the eager call"
+        assert torch.equal(pool_got, kv.kv), f"replay {replay} left another pool"
+        assert torch.isfinite(got).all()
+
+
 def test_demote_refine_round_trip_replays_from_a_graph():
     """A demotion and the refinement that undoes it (its freed blocks as the
     new blocks, its refinement bytes as the input) in one graph: the
