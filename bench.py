@@ -120,6 +120,15 @@ def source_digest():
     return h.hexdigest()[:16]
 
 
+def busy_queue(torch, stream, cycles=1 << 18):
+    """Keep the GPU busy (a spin of ~0.1 ms) while the host enqueues the
+    launches that follow: a leg that synchronises after every launch would
+    otherwise record its start event into an idle queue, and the event time
+    would include the host's call overhead as well as the GPU's work."""
+    with torch.cuda.stream(stream):
+        torch.cuda._sleep(cycles)
+
+
 def measured_traffic():
     """HBM bytes per f=0.5 decode launch from the committed PMC summary, if it
     was taken from the current decode source."""
@@ -521,6 +530,7 @@ def decode_append(torch, ekv, kv, q, scale, stream, reps=30):
     for r in range(reps + 3):
         for fused in (False, True):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            busy_queue(torch, stream)
             e0.record(stream)
             if fused:
                 ekv.attn_decode_append(kv.pool, batch, q, k_new, v_new, out, scale, ws)
@@ -655,6 +665,7 @@ def decode_8bit(torch, ekv, kvpool, workloads, stream, seq_lens, scale, reps=20)
         times = []
         for r in range(reps + 3):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            busy_queue(torch, stream)
             e0.record(stream)
             ekv.attn_decode(kv.pool, batch, q, out, scale, ws)
             e1.record(stream)
@@ -703,6 +714,7 @@ def prefill_8bit(torch, ekv, kvpool, workloads, stream, scale, reps=20):
     times = []
     for r in range(reps + 3):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        busy_queue(torch, stream)
         e0.record(stream)
         ekv.attn_prefill(kv.pool, batch, q, cu, PF_CHUNK, out, scale)
         e1.record(stream)
@@ -804,7 +816,7 @@ def pressure_mix(torch, ekv, kvpool, workloads, stream, scale, steps=20):
     the BASE pairs (sampled after that demotion; new blocks from the free
     FIFO), then decodes the whole batch.  Host planning and uploads are
     outside the timed regions; each launch is timed with HIP events on the
-    launch stream.  Algorithmic bytes: 4 block-equivalents per demoted pair
+    launch stream, queued behind a short GPU spin (busy_queue).  Algorithmic bytes: 4 block-equivalents per demoted pair
     (2 blocks read, the packed block and the low bytes written) and per
     refined pair (packed block and low bytes read, 2 blocks written), plus
     the lists and table updates; decode as for the 8B layer."""
@@ -830,6 +842,7 @@ def pressure_mix(torch, ekv, kvpool, workloads, stream, scale, steps=20):
 
     def timed(fn):
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        busy_queue(torch, stream)
         e0.record(stream)
         fn()
         e1.record(stream)
