@@ -748,13 +748,20 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
                    : u32x4{0u, 0u, 0u, 0u};
   };
   load_q(sm.win[0]);
-  // physical block of block blk of the consume side's window (for the fused
-  // append's write to the pool)
-  auto window_block = [&](int blk) -> int {
-    const int e = *reinterpret_cast<const int*>(sm.win[cw_idx % (NSLOT + 1)] + kWinBt + 4 * (blk - ccur.b0));
-    const int phys = __builtin_amdgcn_readfirstlane(e);
+  // Fused append: the physical block of the newest token's block when it
+  // lies in the consume side's window, read when the side enters the window
+  // (like its tags and queries).  A window's buffer can be refilled for a
+  // later window while the consume side still works in it (the 8-bit ring
+  // holds units of three windows, one per buffer, when windows are one unit
+  // long), so nothing is read from it after entry.
+  auto newest_block = [&](const char* wb) -> int {
+    if constexpr (!fused) return 0;
+    const int nb = (ccur.len - 1) / kPage;
+    if (nb < ccur.b0 || nb >= ccur.b1) return 0;
+    const int phys = __builtin_amdgcn_readfirstlane(*reinterpret_cast<const int*>(wb + kWinBt + 4 * (nb - ccur.b0)));
     return (unsigned)phys < (unsigned)a.num_blocks ? phys : 0;
   };
+  int c_new_phys = newest_block(sm.win[0]);
   int cb = ccur.b0;
   int cslot = 0;
   int piece_j0 = ccur.j0;
@@ -840,7 +847,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       if (new_member >= 0) {
         const int t = (ccur.len - 1) % kPage;
         const int mo = new_member * (kTileBytes / 2) + t * kRowBytes;
-        store_new_row(window_block(cb + new_member), ccur.kvh, t, kb + mo, vb + mo);
+        store_new_row(c_new_phys, ccur.kvh, t, kb + mo, vb + mo);
       }
       f32x4 sc[2];
       PvOps<kStack> pvo;
@@ -904,7 +911,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     EKV_TL(if (!tl_first) tl_first = __builtin_amdgcn_s_memrealtime();)
     const char* sb = sm.ring[cslot];
     const int t_new = (ccur.len - 1) % kPage;
-    if (new0) store_new_row(window_block(cb), ccur.kvh, t_new, sb + t_new * kRowBytes, sb + kTileBytes + t_new * kRowBytes);
+    if (new0) store_new_row(c_new_phys, ccur.kvh, t_new, sb + t_new * kRowBytes, sb + kTileBytes + t_new * kRowBytes);
     // Each kind of step leaves its scores and PV operands here; one softmax
     // and PV call follows for all of them.  A step of one TARGET block (the
     // lone last block, or any block with a ring of fewer than 4 slots) masks
@@ -939,7 +946,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       wait_vm<NSLOT - 2>(ops - c_ops);
       const char* sb2 = sm.ring[cslot2];
       if (new1)
-        store_new_row(window_block(cb + 1), ccur.kvh, t_new, sb2 + t_new * kRowBytes,
+        store_new_row(c_new_phys, ccur.kvh, t_new, sb2 + t_new * kRowBytes,
                       sb2 + kTileBytes + t_new * kRowBytes);
       u32x4 k[2][4], v[2][4];
 #pragma unroll
@@ -987,6 +994,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     const char* wb = sm.win[cw_idx % (NSLOT + 1)];
     cmode = window_mode(wb, ctag);
     load_q(wb);
+    c_new_phys = newest_block(wb);
     if (ccur.piece_start) {
       reset();
       piece_j0 = ccur.j0;

@@ -137,6 +137,17 @@ def test_decode_append_newest_token_in_a_cut_sequence(dtype, min_chunk):
     _run([300, 1024, 77, 2000, 33], 4, dtype, 0.5, min_chunk=min_chunk, hkv=8, seed=61)
 
 
+@pytest.mark.parametrize("dtype", ["e5m2", "bf16"])
+def test_decode_append_many_one_block_sequences(dtype):
+    """96 sequences of 1..16 tokens: every window is one lone block holding
+    the newest token, so the issue side runs windows ahead of the consume
+    side as far as the ring allows (for the 8-bit ring, into the buffer of
+    the window being consumed); the newest token's block must still be
+    written where the table says."""
+    lens = [1 + (7 * i) % 16 for i in range(96)]
+    _run(lens, 4, dtype, 0.0, seed=90)
+
+
 def test_decode_append_leaves_a_base_tail_block_alone():
     """Lengths that are multiples of 32 with every eligible pair BASE: the
     newest token's block is BASE, so nothing is written and the decode reads
