@@ -6,13 +6,13 @@ configuration the benchmark uses.
   {0, 0.25, 0.5, 1} with random pairs.
 * Llama-3-70B-shaped decode layer: 256 sequences of 4096 tokens, 64/8 heads,
   the oldest half of every sequence's pairs BASE (structured), and the same
-  batch forced down the general path.
+  batch forced down the general path; every sequence checked.
 * Pressure-transition mix: a 200,000-block pool (13.1 GB), 128 sequences with
   context uniform in [1024, 16384]; every step demotes a random 10 % of the
   TARGET pairs, refines a random 5 % of the BASE pairs back, and decodes.
 
-Attention is checked on every sequence of the 8B layer (bf16 and fp32
-output) and on sampled sequences of the larger workloads, which the float64
+Attention is checked on every sequence of the 8B and 70B layers (bf16 and
+fp32 output) and on 8 sampled sequences per step of the pressure mix, which the float64
 oracle computes one by one from its own copy of the inputs (it never sees GPU results); the
 transitions and all bookkeeping are checked bit for bit.  To keep the oracle
 affordable on a multi-GB pool the harness hands it only the blocks a
@@ -90,7 +90,7 @@ def test_decode_llama3_8b_full_size_every_sequence(fraction):
     print(f"  max abs err on {len(sample)} sequences: bf16 out {err:.3e}, fp32 out {err32:.3e}", flush=True)
 
 
-def test_decode_llama3_70b_full_size_sampled_structured_and_general():
+def test_decode_llama3_70b_full_size_structured_and_general():
     torch = require_gpu()
     seq_lens = np.full(256, 4096, dtype=np.int32)
     case = workloads.make_decode_case_torch(seq_lens, 64, 8, seed=2, spare_blocks=64)
@@ -109,10 +109,14 @@ def test_decode_llama3_70b_full_size_sampled_structured_and_general():
     # same pairs, same work partition: the two paths differ only in how a
     # pair's mode is looked up, so the outputs agree bit for bit
     assert torch.equal(out_s, out_g)
+    # attention of every sequence against the oracle, bf16 and fp32 output
+    every = list(range(256))
+    ref = _oracle_on_sample(case["pool"], case["block_table"], seq_lens, pairs, every, _host_q(case["q"]))
+    err, _ = check_attention(out_s.float().cpu().numpy(), ref, out_fp32=False)
+    out32 = _decode(kv, case["q"], 64, out_fp32=True)
+    err32, _ = check_attention(out32.cpu().numpy(), ref, out_fp32=True)
+    print(f"  max abs err on all 256 sequences: bf16 out {err:.3e}, fp32 out {err32:.3e}", flush=True)
     sample = [0, 1, 100, 201, 255]
-    ref = _oracle_on_sample(case["pool"], case["block_table"], seq_lens, pairs, sample, _host_q(case["q"]))
-    err, _ = check_attention(out_s[sample].float().cpu().numpy(), ref, out_fp32=False)
-    print(f"  max abs err on {len(sample)} sequences: {err:.3e}", flush=True)
     # the demoted pool, block table and tags of the sampled sequences
     host_in, sbt, slens = workloads.extract_sequences(case["pool"], case["block_table"], seq_lens, sample)
     rows = {s: r for r, s in enumerate(sample)}
@@ -194,7 +198,7 @@ def test_pressure_transition_mix_200k_blocks():
         omode, obounds = olow.lower(otg, seq_lens, PAGE)
         assert mode == omode and np.array_equal(kv.bounds.cpu().numpy(), obounds)
         out = _decode(kv, case["q"], hq)
-        sample = sorted(srng.choice(bsz, 3, replace=False).tolist())
+        sample = sorted(srng.choice(bsz, 8, replace=False).tolist())
         ref = oatt.decode(q_host[sample], host_pool, obt[sample], otg[sample], seq_lens[sample])
         err, _ = check_attention(out[sample].float().cpu().numpy(), ref, out_fp32=False)
         assert np.isfinite(out.float().cpu().numpy()).all()
