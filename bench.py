@@ -441,6 +441,7 @@ def main():
                     "ms": round(dec_ms[k], 5),
                     "GB_per_s": round(decode_bytes_f[k] / (dec_ms[k] * 1e-3) / 1e9, 1),
                     "tokens_per_s": round(B / (dec_ms[k] * 1e-3), 1),
+                    "kv_tokens_per_s": round(float(np.sum(seq_lens)) / (dec_ms[k] * 1e-3), 1),
                     "realized_base_block_fraction": round(
                         float(sum(pools[k].mirror.tags[s, :-(-int(l) // PAGE)].sum()
                                   for s, l in enumerate(seq_lens))
@@ -636,7 +637,8 @@ def decode_70b(torch, ekv, kvpool, workloads, stream, scale, reps=20):
         nbytes = decode_bytes(seq_lens, kv.mirror.tags, hq, HKV, 2 if name == "general" else mode)
         res[name] = {"ms": round(ms, 5), "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
                      "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4), "bytes": nbytes,
-                     "tokens_per_s": round(bsz / (ms * 1e-3), 1)}
+                     "tokens_per_s": round(bsz / (ms * 1e-3), 1),
+                     "kv_tokens_per_s": round(float(np.sum(seq_lens)) / (ms * 1e-3), 1)}
         del ws
     del kv, case
     torch.cuda.empty_cache()
@@ -685,7 +687,8 @@ def decode_8bit(torch, ekv, kvpool, workloads, stream, seq_lens, scale, reps=20)
         nbytes += 2 * B * HQ * D * 2 + blocks * 4 + (blocks if mode == 2 else 0) + B * 4
         res.append({"base_fraction": f, "mode": ["native", "structured", "general"][mode], "ms": round(ms, 5),
                     "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1), "hbm_frac": round(nbytes / (ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
-                    "tokens_per_s": round(B / (ms * 1e-3), 1), "bytes": nbytes})
+                    "tokens_per_s": round(B / (ms * 1e-3), 1),
+                    "kv_tokens_per_s": round(float(np.sum(seq_lens)) / (ms * 1e-3), 1), "bytes": nbytes})
         del kv, ws
     del base
     torch.cuda.empty_cache()
@@ -889,7 +892,9 @@ def pressure_mix(torch, ekv, kvpool, workloads, stream, scale, steps=20):
                      "base_block_fraction": round(float(kv.mirror.tags[pair_s, 2 * pair_j].mean()), 4),
                      "mode": ["native", "structured", "general"][mode],
                      "demote_ms": round(d_ms, 4), "demote_GB_per_s": round(dbytes / (d_ms * 1e-3) / 1e9, 1),
+                     "demote_pairs_per_s": round(nd / (d_ms * 1e-3), 1),
                      "refine_ms": round(r_ms, 4), "refine_GB_per_s": round(rbytes / (r_ms * 1e-3) / 1e9, 1),
+                     "refine_pairs_per_s": round(nr / (r_ms * 1e-3), 1),
                      "decode_ms": round(c_ms, 4), "decode_GB_per_s": round(cbytes / (c_ms * 1e-3) / 1e9, 1)})
     del kv, lo_store, ws
     torch.cuda.empty_cache()
