@@ -137,10 +137,12 @@ def test_dtypes_and_outputs(dtype, out_fp32):
     _run(c, 16, 4, out_fp32=out_fp32)
 
 
-@pytest.mark.parametrize("scale", [0.02, 0.3, -0.088])
+@pytest.mark.parametrize("scale", [0.02, 0.3, -0.088, 0.0, -0.0])
 def test_decode_softmax_scales(scale):
     """Other softmax scales, a negative one included (the kernels apply its
-    sign to Q): structured and general paths."""
+    sign to Q), and zero of either sign (uniform attention: a zero scale
+    must never multiply a masked score's infinity): structured and general
+    paths."""
     c = workloads.make_decode_case([33, 700, 64, 1500], 16, 4, seed=44, base_fraction=0.5, spare_blocks=4)
     _run(c, 16, 4, scale=scale)
     _run(c, 16, 4, scale=scale, use_boundaries=False)
@@ -208,3 +210,19 @@ def test_one_workspace_for_batches_of_different_grids():
         ekv.attn_decode(kv.pool, kv.batch(32), q, out, default_scale(), ws)
         torch.cuda.synchronize()
         check_attention(out.cpu().numpy(), ref, True)
+
+
+@pytest.mark.parametrize("dtype", ["bf16", "e5m2"])
+def test_decode_batch_of_700_short_sequences(dtype):
+    """More sequences than one wave's lanes and than one pass of the range
+    scan (700 > 512): lengths 0..96, half the eligible pairs BASE, so the
+    work walker reloads its window of lengths every 64 sequences and skips
+    empty ones, and most (sequence, KV head)s are cut between workgroups."""
+    rng = np.random.default_rng(77)
+    lens = rng.integers(0, 97, size=700).tolist()
+    c = workloads.make_decode_case(lens, 8, 2, seed=78, base_fraction=0.5, spare_blocks=4, dtype=dtype)
+    if dtype == "e5m2":
+        from tests import test_gpu_fp8
+        test_gpu_fp8._run_decode(c, 8, 2)
+    else:
+        _run(c, 8, 2)

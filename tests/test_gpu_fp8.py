@@ -23,8 +23,9 @@ def _bytes_tensor(a, torch):
     return torch.from_numpy(np.ascontiguousarray(a, dtype=np.uint8)).cuda()
 
 
-def _run_decode(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None):
+def _run_decode(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode=None, scale=None):
     torch = require_gpu()
+    scale = default_scale() if scale is None else scale
     host_safety_check(case, case["pool"].shape)
     kv = kvpool.PagedKV(case["pool"], case["block_table"], case["seq_lens"], case["free"], hkv, "e5m2")
     opool, obt, otg = case["pool"], case["block_table"], case["tags"]
@@ -48,10 +49,20 @@ def _run_decode(case, hq, hkv, *, out_fp32=True, use_boundaries=True, force_mode
     batch = kv.batch(hq, mode=mode, use_boundaries=use_boundaries)
     ws = ekv.decode_workspace(kv.pool, batch)
     print(f"decode e5m2: B={bsz} Hq={hq} Hkv={hkv} mode={mode} fp32={out_fp32}", flush=True)
-    ekv.attn_decode(kv.pool, batch, q, out, default_scale(), ws)
+    ekv.attn_decode(kv.pool, batch, q, out, scale, ws)
     torch.cuda.synchronize()
-    ref = ofp8.decode(case["q"], opool, obt, otg, case["seq_lens"])
+    ref = ofp8.decode(case["q"], opool, obt, otg, case["seq_lens"], scale)
     return check_attention(out.float().cpu().numpy(), ref, out_fp32)
+
+
+@pytest.mark.parametrize("scale", [0.03, -0.1, 0.0, -0.0])
+def test_decode_e5m2_softmax_scales(scale):
+    """Other softmax scales on the 8-bit pool: negative (applied as the
+    query's sign) and zero of either sign; structured and general paths."""
+    c = workloads.make_decode_case([33, 700, 64, 1500], 16, 4, dtype="e5m2", seed=45, base_fraction=0.5,
+                                   spare_blocks=4)
+    _run_decode(c, 16, 4, scale=scale)
+    _run_decode(c, 16, 4, scale=scale, use_boundaries=False)
 
 
 @pytest.mark.parametrize("fraction", [0.0, 0.5, 1.0])
