@@ -355,11 +355,18 @@ __device__ __forceinline__ int clamp_len(int len, int cap) { return len < 0 ? 0 
 
 __device__ __forceinline__ int pairs_of(int len) { return ((len + kPage - 1) / kPage + 1) >> 1; }
 
-constexpr int kWinPairs = 32;                      // a window: at most 32 pairs = 64 blocks
-// Window buffer in LDS: block-table entries, tags (one dword each),
-// the sequence's boundaries, then the G query rows of the KV head.
-constexpr int kWinBt = 0, kWinTags = 256, kWinBounds = 512, kWinQ = 528;
-template <int G> constexpr int win_bytes() { return kWinQ + G * 2 * kHeadDim; }
+// Window geometry: a window covers at most kPairs pairs (2 kPairs blocks),
+// and its buffer in LDS holds the block-table entries, the tags (one dword
+// each), the sequence's boundaries, then the G query rows of the KV head.
+// The 8-bit two-slot ring uses half-size windows: its workgroup then needs
+// 20,272 B of LDS instead of 21,040 B at G = 4, so 8 instead of 7 fit a CU
+// (its BASE path is bound by latency, and the eighth wave shortens it).
+template <bool SMALL>
+struct WinGeo {
+  static constexpr int kPairs = SMALL ? 16 : 32;
+  static constexpr int kBt = 0, kTags = 8 * kPairs, kBounds = 16 * kPairs, kQ = 16 * kPairs + 16;
+};
+template <int G, bool SMALL> constexpr int win_bytes() { return WinGeo<SMALL>::kQ + G * 2 * kHeadDim; }
 
 // Position in the flattened (sequence, KV head, pair) space.
 struct Walker {
@@ -375,10 +382,10 @@ struct Window {
   bool piece_start, piece_end;
 };
 
-template <int G, bool ELASTIC, int NSLOT>
+template <int G, bool ELASTIC, int NSLOT, bool SMALL>
 struct alignas(16) DecodeSmem {
   char ring[NSLOT][kSlotBytes];
-  char win[NSLOT + 1][win_bytes<G>()];
+  char win[NSLOT + 1][win_bytes<G, SMALL>()];
 };
 
 // ---------------------------------------------------------------------------
@@ -391,7 +398,11 @@ struct alignas(16) DecodeSmem {
 // ---------------------------------------------------------------------------
 template <typename T, int G, bool ELASTIC, int NSLOT, bool F8, bool FUSED>
 __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
-  __shared__ DecodeSmem<G, ELASTIC, NSLOT> sm;
+  constexpr bool kSmallWin = F8 && NSLOT == 2;
+  using Geo = WinGeo<kSmallWin>;
+  constexpr int kWinPairs = Geo::kPairs, kWinBt = Geo::kBt, kWinTags = Geo::kTags, kWinBounds = Geo::kBounds,
+                kWinQ = Geo::kQ;
+  __shared__ DecodeSmem<G, ELASTIC, NSLOT, kSmallWin> sm;
   // query groups of at most 8 heads hold each head in two MFMA columns
   // (n and n + G): P's 16-bit head and remainder accumulate side by side
   constexpr bool kStack = 2 * G <= 16;
