@@ -389,11 +389,13 @@ struct alignas(16) DecodeSmem {
 };
 
 // ---------------------------------------------------------------------------
-// Decode kernel: workgroup w streams pairs [w*chunk, (w+1)*chunk) of the
-// flattened (sequence, KV head, pair) space, where chunk = ceil(T / grid)
-// (at least a.min_chunk) and T counts every pair of every (sequence, KV
-// head).  A (sequence, KV head) that lies wholly inside one range is
-// written out directly; one cut by range ends leaves one partial per piece,
+// Decode kernel: workgroup w streams a range of pairs of the flattened
+// (sequence, KV head, pair) space, [w*chunk, (w+1)*chunk) where chunk =
+// ceil(T / grid) (at least a.min_chunk) and T counts every pair of every
+// (sequence, KV head); with a.heavy > 0 the first a.heavy ranges are
+// a.heavy_permille / 1000 times the mean and the others share the rest.
+// A (sequence, KV head) that lies wholly inside one range is written out
+// directly; one cut by range ends leaves one partial per piece,
 // and the last piece to arrive merges them (after its stream has ended).
 // ---------------------------------------------------------------------------
 template <typename T, int G, bool ELASTIC, int NSLOT, bool F8, bool FUSED>
@@ -440,10 +442,26 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       }
     }
   }
-  const int chunk = max(a.min_chunk, (T_all + (int)gridDim.x - 1) / (int)gridDim.x);
-  const int start = (int)blockIdx.x * chunk;
-  if (start >= T_all) return;
-  const int end = min(T_all, start + chunk);
+  // Ranges: `heavy` leading workgroups stream r_heavy pairs each, the others r_light
+  // (equal ranges when heavy is 0 or the work is at the minimum range).
+  const int grid = (int)gridDim.x;
+  int r_heavy = max(a.min_chunk, (T_all + grid - 1) / grid), r_light = r_heavy, heavy = 0;
+  if (a.heavy > 0 && a.heavy < grid && (T_all + grid - 1) / grid > a.min_chunk) {
+    heavy = a.heavy;
+    r_heavy = max(1, (int)(((long long)T_all * a.heavy_permille + 1000LL * grid - 1) / (1000LL * grid)));
+    const long long rest = (long long)T_all - (long long)heavy * r_heavy;
+    r_light = rest > 0 ? (int)((rest + (grid - heavy) - 1) / (grid - heavy)) : 1;
+  }
+  const long long heavy_end = (long long)heavy * r_heavy;
+  auto range_start = [&](int w) -> long long {
+    return w < heavy ? (long long)w * r_heavy : heavy_end + (long long)(w - heavy) * r_light;
+  };
+  auto range_of = [&](int pos) -> int {   // the workgroup whose range holds pair pos
+    return pos < heavy_end ? pos / r_heavy : heavy + (int)((pos - heavy_end) / r_light);
+  };
+  if (range_start((int)blockIdx.x) >= T_all) return;
+  const int start = (int)range_start((int)blockIdx.x);
+  const int end = (int)min((long long)T_all, range_start((int)blockIdx.x + 1));
 
   Walker w0;
   {
@@ -519,17 +537,23 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     char* wb = sm.win[slot];
     const int nb = x.b1 - x.b0;
     const size_t row = (size_t)x.s * a.max_blocks + x.b0;
+    // (scalar base + 32-bit lane offset: no 64-bit per-lane address stays
+    // live across the stream for these once-per-window loads)
     if (lane < nb)
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.bt + row + lane), (lds_ptr)(wb + kWinBt), 4, 0, 0);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(reinterpret_cast<const char*>(a.bt + row) + lane_offset(4 * lane)),
+                                       (lds_ptr)(wb + kWinBt), 4, 0, 0);
     if (have_tags && lane < nb)
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.tags + row + lane), (lds_ptr)(wb + kWinTags), 1, 0, 0);
+      __builtin_amdgcn_global_load_lds(static_cast<const void*>(reinterpret_cast<const char*>(a.tags + row) + lane_offset(lane)),
+                                       (lds_ptr)(wb + kWinTags), 1, 0, 0);
     if (have_bounds && lane < 2)
-      __builtin_amdgcn_global_load_lds(static_cast<const void*>(a.bounds + 2 * x.s + lane), (lds_ptr)(wb + kWinBounds), 4, 0, 0);
+      __builtin_amdgcn_global_load_lds(
+          static_cast<const void*>(reinterpret_cast<const char*>(a.bounds + 2 * x.s) + lane_offset(4 * lane)),
+          (lds_ptr)(wb + kWinBounds), 4, 0, 0);
     const char* qsrc = reinterpret_cast<const char*>(a.q) + ((size_t)x.s * a.num_q_heads + (size_t)x.kvh * G) * 2 * kHeadDim;
 #pragma unroll
     for (int r = 0; r < kQInstr; ++r)
       if (64 * r + lane < G * 16)
-        __builtin_amdgcn_global_load_lds(static_cast<const void*>(qsrc + 16 * (64 * r + lane)),
+        __builtin_amdgcn_global_load_lds(static_cast<const void*>(qsrc + lane_offset(16 * (64 * r + lane))),
                                          (lds_ptr)(wb + kWinQ + 1024 * r), 16, 0, 0);
     ops += win_ops;
   };
@@ -658,22 +682,25 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   bool issue_done = false;
   int n_issued = 0, n_consumed = 0;   // ring slots
 
-  auto issue_slot = [&]() {
-    if (ib >= icur.b1) {   // enter the next window (its metadata was requested one window ago)
-      icur = inext;
-      ++iw_idx;
-      const int ws = iw_idx % (NSLOT + 1);
-      wait_vm<NSLOT - 1>(ops - ops_inext);
-      bt_lane = *reinterpret_cast<const int*>(sm.win[ws] + kWinBt + 4 * lane);
-      imode = window_mode(sm.win[ws], itag);
-      i_has_next = iwk.g < end;
-      if (i_has_next) {
-        inext = next_window(iwk);
-        dma_window(inext, (iw_idx + 1) % (NSLOT + 1));
-        ops_inext = ops;
-      }
-      ib = icur.b0;
+  // enter the next window (its metadata was requested one window ago)
+  auto enter_issue_window = [&]() {
+    icur = inext;
+    ++iw_idx;
+    const int ws = iw_idx % (NSLOT + 1);
+    wait_vm<NSLOT - 1>(ops - ops_inext);
+    bt_lane = *reinterpret_cast<const int*>(sm.win[ws] + kWinBt + 4 * lane);
+    imode = window_mode(sm.win[ws], itag);
+    i_has_next = iwk.g < end;
+    if (i_has_next) {
+      inext = next_window(iwk);
+      dma_window(inext, (iw_idx + 1) % (NSLOT + 1));
+      ops_inext = ops;
     }
+    ib = icur.b0;
+  };
+
+  auto issue_slot = [&]() {
+    if (ib >= icur.b1) enter_issue_window();
     const bool base = block_is_base(imode, itag, icur.b0, ib);
     int phys = __builtin_amdgcn_readlane(bt_lane, ib - icur.b0);
     phys = (unsigned)phys < (unsigned)a.num_blocks ? phys : 0;   // never leave the pool
@@ -796,7 +823,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     const float l = head_sum(st.l);
     const size_t head0 = (size_t)ccur.s * a.num_q_heads + (size_t)ccur.kvh * G;
     const int first = ccur.seq_base + ccur.kvh * ccur.np;
-    const int w_first = first / chunk, w_last = (first + ccur.np - 1) / chunk;
+    const int w_first = range_of(first), w_last = range_of(first + ccur.np - 1);
     const int pieces = w_last - w_first + 1;
     if (pieces == 1) {
       if (n < G) {
@@ -821,7 +848,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
       }
       pend_head0[pend_n] = head0;
       pend_wfirst[pend_n] = w_first;
-      pend_odd[pend_n] = first > w_first * chunk ? 1 : 0;
+      pend_odd[pend_n] = first > range_start(w_first) ? 1 : 0;
       pend_pieces[pend_n] = pieces;
       ++pend_n;
     }
@@ -888,7 +915,9 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
           }
         }
       } else {
-        u32x4 k[2][4], v[2][4];
+        // (only .xy of each V operand is loaded: the byte path reads no
+        // more, and zero .zw lets the tail clearing below fold to nothing there)
+        u32x4 k[2][4], v[2][4] = {};
 #pragma unroll
         for (int m = 0; m < 2; ++m) {
           const char* mb = kb + m * (kTileBytes / 2);
@@ -1019,7 +1048,8 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
              uint64_t* r = g_timeline + 8 * blockIdx.x;
              r[0] = tl_start; r[1] = tl_first; r[2] = tl_stream; r[3] = __builtin_amdgcn_s_memrealtime();
              r[4] = (uint64_t)(end - start); r[5] = (uint64_t)pend_n;
-             r[6] = (uint64_t)__builtin_amdgcn_s_getreg(30740);   // XCC_ID (hwreg 20, bits 0..15)
+             // XCC_ID (hwreg 20, bits 0..15); HW_ID (hwreg 4: wave slot, SIMD, CU, SH, SE) in bits 32..63
+             r[6] = (uint64_t)__builtin_amdgcn_s_getreg(30740) | ((uint64_t)__builtin_amdgcn_s_getreg(63492) << 32);
              r[7] = 1;
            }
          };)
@@ -1052,20 +1082,45 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   EKV_TL(tl_write();)
 }
 
-// Workgroups that fit on the device at once for a kernel (one wave each),
-// cached per device and kernel instance (occupancy does not change).
-template <typename K>
-int resident_groups(K kernel, std::atomic<int>* cache) {
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return 0;
-  int r = cache[dev].load(std::memory_order_relaxed);
-  if (r > 0) return r;
+// Workgroups that fit on the device at once for a kernel (one wave each):
+// compute units and workgroups per compute unit, cached per device and
+// kernel instance (occupancy does not change).
+struct Residency {
   int cus = 0, per_cu = 0;
-  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return 0;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 64, 0) != hipSuccess) return 0;
-  r = cus * per_cu;
-  cache[dev].store(r, std::memory_order_relaxed);
+  int total() const { return cus * per_cu; }
+};
+template <typename K>
+Residency residency(K kernel, std::atomic<int>* cache) {
+  Residency r;
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return r;
+  const int packed = cache[dev].load(std::memory_order_relaxed);
+  if (packed > 0) {
+    r.cus = packed >> 8;
+    r.per_cu = packed & 255;
+    return r;
+  }
+  int cus = 0, per_cu = 0;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) return r;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, kernel, 64, 0) != hipSuccess) return r;
+  if (cus <= 0 || per_cu <= 0 || per_cu > 255) return r;
+  r.cus = cus;
+  r.per_cu = per_cu;
+  cache[dev].store((cus << 8) | per_cu, std::memory_order_relaxed);
   return r;
+}
+
+// Range weighting for instances that hold two waves on every SIMD: the
+// first 4 x CUs workgroups of a full grid each take a SIMD's first slot and
+// are issued ahead of the second-slot waves, which then stream more slowly;
+// with equal ranges the second-slot waves finished ~25 % later (8-bit pool,
+// BASE fraction 1).  So the first-slot workgroups take ranges of
+// kHeavyPermille / 1000 times the mean and the others share the rest
+// (EKV_HEAVY_PERMILLE overrides; 1000 gives equal ranges).
+constexpr int kHeavyPermille = 1200;
+int heavy_permille() {
+  if (const char* env = getenv("EKV_HEAVY_PERMILLE")) return std::max(1000, std::min(1900, atoi(env)));
+  return kHeavyPermille;
 }
 
 // Launches the instance, or (grid_out != null) only reports the grid it
@@ -1074,9 +1129,10 @@ template <typename T, int G, int NSLOT, bool F8>
 hipError_t run_slots(const DecodeArgs& a, bool elastic, hipStream_t st, int* grid_out) {
   static std::atomic<int> cache[2][kMaxDevices];
   auto kernel = elastic ? decode_kernel<T, G, true, NSLOT, F8, false> : decode_kernel<T, G, false, NSLOT, F8, false>;
+  const Residency res = residency(kernel, cache[elastic ? 1 : 0]);
+  if (res.total() <= 0) return hipErrorInvalidDeviceFunction;
   if (grid_out) {   // (the grid of the plain decode; the fused instance has the same registers and LDS)
-    const int resident = resident_groups(kernel, cache[elastic ? 1 : 0]);
-    if (resident <= 0) return hipErrorInvalidDeviceFunction;
+    const int resident = res.total();
     const long long wanted = (a.pairs_max + a.min_chunk - 1) / a.min_chunk;
     *grid_out = (int)std::max<long long>(1, std::min<long long>(std::min(resident, kMaxDecodeGrid), wanted));
     return hipSuccess;
@@ -1084,7 +1140,14 @@ hipError_t run_slots(const DecodeArgs& a, bool elastic, hipStream_t st, int* gri
   if (a.grid <= 0) return hipErrorInvalidValue;
   if (a.k_new)
     kernel = elastic ? decode_kernel<T, G, true, NSLOT, F8, true> : decode_kernel<T, G, false, NSLOT, F8, true>;
-  hipLaunchKernelGGL(kernel, dim3(a.grid), dim3(64), 0, st, a);
+  DecodeArgs b = a;
+  b.heavy = 0;
+  b.heavy_permille = 1000;
+  if (res.per_cu == 8 && a.grid == res.total()) {
+    b.heavy = 4 * res.cus;
+    b.heavy_permille = heavy_permille();
+  }
+  hipLaunchKernelGGL(kernel, dim3(b.grid), dim3(64), 0, st, b);
   return hipGetLastError();
 }
 

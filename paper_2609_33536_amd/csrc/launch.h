@@ -25,7 +25,9 @@ struct DecodeArgs {
   int32_t grid;              // workgroups launched (decode_grid of the same arguments; the workspace has 2 grid slots)
   int64_t pairs_max;         // upper bound on the pairs of all (seq, KV head)s
   int32_t out_fp32;
-  int32_t slots;             // LDS ring depth per wave (2..6)
+  int32_t slots;             // LDS ring depth per wave (2..4)
+  int32_t heavy;             // leading workgroups with longer ranges (set by the launcher)
+  int32_t heavy_permille;    // their range length over the mean, x 1000
   float scale_log2;          // softmax scale * log2(e)
   // Fused append (null otherwise): the K / V rows of each sequence's newest
   // token (position seq_lens[s] - 1), [B][Hkv][128] in the pool's element

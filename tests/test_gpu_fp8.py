@@ -266,6 +266,40 @@ def test_decode_e5m2_8b_full_size_every_sequence(fraction):
         print(f"  {out_dtype}: max abs err {err:.3e} on {len(sample)} sequences", flush=True)
 
 
+@pytest.mark.parametrize("permille", [1000, 1900])
+@pytest.mark.parametrize("fraction", [0.5, 1.0])
+def test_decode_e5m2_8b_weighted_ranges(fraction, permille, monkeypatch):
+    """The full-size 8-bit layer fills the grid (two waves per SIMD), so the
+    launcher gives the first-slot workgroups longer ranges.  At equal ranges
+    (1000) and at the largest weight (1900: the other ranges shrink to a few
+    pairs, so (sequence, KV head)s are cut into more pieces) every sequence
+    still matches the oracle (FP32 output)."""
+    torch = require_gpu()
+    seq_lens = workloads.seq_lens_uniform(np.random.default_rng(1), 64, 2048, 8192)
+    case = workloads.make_decode_case_torch(seq_lens, 32, 8, seed=6, outlier_channels=10, spare_blocks=64,
+                                            dtype="e5m2")
+    pairs = workloads.choose_pairs(np.random.default_rng(2100 + int(2 * fraction)), seq_lens, fraction, "random")
+    kv = kvpool.PagedKV(case["pool"].clone(), case["block_table"], seq_lens, case["free"], 8, "e5m2")
+    kv.demote(pairs, emit_lo=False)
+    kv.commit()
+    kv.relower()
+    batch = kv.batch(32)
+    ws = ekv.decode_workspace(kv.pool, batch)
+    monkeypatch.setenv("EKV_HEAVY_PERMILLE", str(permille))
+    print(f"8-bit weighted ranges: f={fraction} permille={permille} pairs={len(pairs)}", flush=True)
+    out = torch.full((64, 32, 128), float("nan"), dtype=torch.float32, device="cuda")
+    ekv.attn_decode(kv.pool, batch, case["q"], out, default_scale(), ws)
+    torch.cuda.synchronize()
+    sample = list(range(64))
+    host, sbt, slens = workloads.extract_sequences(case["pool"], case["block_table"], seq_lens, sample)
+    tg = np.zeros(sbt.shape, dtype=np.uint8)
+    host, sbt, tg, _, _ = ofp8.demote(host, sbt, tg, pairs, slens)
+    q_words = case["q"].view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = ofp8.decode(q_words, host, sbt, tg, slens)
+    err, _ = check_attention(out.cpu().numpy(), ref, True)
+    print(f"  max abs err {err:.3e} on 64 sequences", flush=True)
+
+
 def test_prefill_e5m2_8b_full_size():
     """The chunked-prefill workload over an 8-bit pool as the benchmark runs
     it: 16 x (2048-token prefix, half its pairs BASE, + 512-token chunk), 32
