@@ -549,13 +549,63 @@ def decode_append(torch, ekv, kv, q, scale, stream, reps=30):
             "saved_ms": round(float(np.median(two)) - float(np.median(one)), 5)}
 
 
+def _timeline_stats(torch, lib, launch, stream, reps, first_slot):
+    """Median over `reps` launches of the per-workgroup timeline statistics
+    (after two warm-up launches); first_slot: workgroups below this index
+    hold the first wave slot of their SIMD (0: no split reported)."""
+    rows = []
+    for rep in range(reps + 2):
+        lib.ekv_timeline_clear()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record(stream)
+        launch()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        host = np.zeros(8 * 8192, dtype=np.uint64)
+        lib.ekv_timeline_read(host.ctypes.data, host.size)
+        t = host.reshape(-1, 8).astype(np.int64)
+        idx = np.nonzero(t[:, 7] == 1)[0]   # record w belongs to workgroup w
+        t = t[idx]
+        t0 = t[:, 0].min()
+        start, first, stream_end, end = ((t[:, c] - t0) / 100.0 for c in range(4))
+        xcc = t[:, 6] & 0xF
+        merged = t[:, 5] > 0
+        if rep >= 2:
+            r = {"event_us": e0.elapsed_time(e1) * 1e3, "workgroups": len(t),
+                 "start_skew_us": float(start.max()),
+                 "first_slot_after_start_us": float(np.median(first - start)),
+                 "first_slot_after_start_max_us": float((first - start).max()),
+                 "stream_end_p50_us": float(np.median(stream_end)),
+                 "stream_end_p90_us": float(np.percentile(stream_end, 90)),
+                 "stream_end_max_us": float(stream_end.max()),
+                 "end_max_us": float(end.max()),
+                 "merge_us_p50": float(np.median((end - stream_end)[merged])) if merged.any() else 0.0,
+                 "merge_us_max": float((end - stream_end)[merged].max()) if merged.any() else 0.0,
+                 "xcd_mean_stream_end_us": [float(stream_end[xcc == x].mean()) for x in range(8)]}
+            if first_slot:
+                lo = idx < first_slot
+                r["stream_end_p50_first_slot_us"] = float(np.median(stream_end[lo]))
+                r["stream_end_p50_second_slot_us"] = float(np.median(stream_end[~lo]))
+                r["pairs_first_slot"] = int(np.median(t[lo, 4]))
+                r["pairs_second_slot"] = int(np.median(t[~lo, 4]))
+            rows.append(r)
+    med = {key: (round(float(np.median([r[key] for r in rows])), 1) if not isinstance(rows[0][key], list)
+                 else [round(float(np.median([r[key][x] for r in rows])), 1) for x in range(8)])
+           for key in rows[0]}
+    med["outside_workgroups_us"] = round(med["event_us"] - med["end_max_us"], 1)
+    return med
+
+
 def decode_timeline(torch, ekv, kvpool, workloads, stream, scale, reps=5):
     """Where the time of one 8B decode launch goes, per BASE fraction, from
     the instrumented library's per-workgroup timestamps (100 MHz constant
     clock, relative to the first workgroup's start): workgroup start skew,
     first K/V slot after start, end of each workgroup's stream, end of its
     merges, and the mean stream end per XCD; next to the launch's HIP-event
-    time.  Median over `reps` launches of each statistic."""
+    time.  Median over `reps` launches of each statistic.  Also the same
+    layer over an 8-bit pool at BASE fraction 0.5 and 1 (two waves per
+    SIMD: the stream ends of the first-slot and second-slot workgroups)."""
     import ctypes
     lib = ekv.lib()
     lib.ekv_timeline_read.argtypes = [ctypes.c_void_p, ctypes.c_int]
@@ -566,44 +616,34 @@ def decode_timeline(torch, ekv, kvpool, workloads, stream, scale, reps=5):
     for k, kv in enumerate(dec["pools"]):
         b = kv.batch(HQ)
         ws = ekv.decode_workspace(kv.pool, b)
-        rows = []
-        for rep in range(reps + 2):
-            lib.ekv_timeline_clear()
-            torch.cuda.synchronize()
-            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            e0.record(stream)
-            ekv.attn_decode(kv.pool, b, q, out, scale, ws)
-            e1.record(stream)
-            torch.cuda.synchronize()
-            host = np.zeros(8 * 8192, dtype=np.uint64)
-            lib.ekv_timeline_read(host.ctypes.data, host.size)
-            t = host.reshape(-1, 8).astype(np.int64)
-            t = t[t[:, 7] == 1]
-            t0 = t[:, 0].min()
-            start, first, stream_end, end = ((t[:, c] - t0) / 100.0 for c in range(4))
-            xcc = t[:, 6] & 0xF
-            merged = t[:, 5] > 0
-            if rep >= 2:
-                rows.append({"event_us": e0.elapsed_time(e1) * 1e3, "workgroups": len(t),
-                             "start_skew_us": float(start.max()),
-                             "first_slot_after_start_us": float(np.median(first - start)),
-                             "first_slot_after_start_max_us": float((first - start).max()),
-                             "stream_end_p50_us": float(np.median(stream_end)),
-                             "stream_end_p90_us": float(np.percentile(stream_end, 90)),
-                             "stream_end_max_us": float(stream_end.max()),
-                             "end_max_us": float(end.max()),
-                             "merge_us_p50": float(np.median((end - stream_end)[merged])) if merged.any() else 0.0,
-                             "merge_us_max": float((end - stream_end)[merged].max()) if merged.any() else 0.0,
-                             "xcd_mean_stream_end_us": [float(stream_end[xcc == x].mean()) for x in range(8)]})
-        med = {key: (round(float(np.median([r[key] for r in rows])), 1) if not isinstance(rows[0][key], list)
-                     else [round(float(np.median([r[key][x] for r in rows])), 1) for x in range(8)])
-               for key in rows[0]}
-        med["outside_workgroups_us"] = round(med["event_us"] - med["end_max_us"], 1)
+        med = _timeline_stats(torch, lib, lambda: ekv.attn_decode(kv.pool, b, q, out, scale, ws), stream, reps, 0)
         res.append({"base_fraction": FRACTIONS[k], "mode": ["native", "structured", "general"][dec["modes"][k]],
                     "algorithmic_bytes": decode_bytes(dec["seq_lens"], kv.mirror.tags, HQ, HKV, dec["modes"][k]),
                     **med})
         del ws
-    return {"decode_timeline": res, "library": "libekv_timeline.so (timestamps in the decode kernel)"}
+    seq_lens = dec["seq_lens"]
+    del dec
+    torch.cuda.empty_cache()
+    # the 8-bit pool of the decode_8bit leg (same inputs)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    base = workloads.make_decode_case_torch(seq_lens, HQ, HKV, seed=SEED + 5, outlier_channels=10,
+                                            spare_blocks=64, dtype="e5m2")
+    out8 = torch.empty((B, HQ, D), dtype=torch.float16, device="cuda")
+    res8 = []
+    for k, f in ((1, 0.5), (2, 1.0)):
+        kv = kvpool.PagedKV(base["pool"].clone(), base["block_table"], seq_lens, base["free"], HKV, "e5m2")
+        pairs = workloads.choose_pairs(np.random.default_rng(SEED * 2000 + k), seq_lens, f, "random")
+        kv.demote(pairs, emit_lo=False)
+        kv.commit()
+        mode = kv.relower()
+        b = kv.batch(HQ)
+        ws = ekv.decode_workspace(kv.pool, b)
+        med = _timeline_stats(torch, lib, lambda: ekv.attn_decode(kv.pool, b, base["q"], out8, scale, ws), stream,
+                              reps, 4 * cus)
+        res8.append({"base_fraction": f, "mode": ["native", "structured", "general"][mode], **med})
+        del ws, kv
+    return {"decode_timeline": res, "decode_timeline_8bit": res8,
+            "library": "libekv_timeline.so (timestamps in the decode kernel)"}
 
 
 def decode_70b(torch, ekv, kvpool, workloads, stream, scale, reps=20):
