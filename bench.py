@@ -558,6 +558,7 @@ def _timeline_stats(torch, lib, launch, stream, reps, first_slot):
         lib.ekv_timeline_clear()
         torch.cuda.synchronize()
         e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        busy_queue(torch, stream)
         e0.record(stream)
         launch()
         e1.record(stream)
