@@ -242,25 +242,61 @@ __device__ __forceinline__ void wait_vm(int n) {
 }
 
 // As wait_vm, in steps of 4 (units of the 8-bit format cost 4 loads), as
-// one assembly block: a chain of scalar compares where the first level L
-// with n >= L waits for vmcnt <= L (never above n).  Written as a C switch
-// over its 16 levels, the compiler's control-flow structurizer made it a
-// long run of scalar instructions and taken branches on every step, which
-// the 8-bit elastic path (bound by instruction issue) paid for: 3 % at
-// BASE fraction 1.  n is at most 4 (units in the ring - 1) + the window's
-// loads, below 36 for rings of up to 4 slots.
-#define EKV_WAIT_LEVEL(lbl, cnt)                                         \
-  "s_cmp_lt_i32 %0, " #cnt "\n\t"                                        \
-  "s_cbranch_scc1 " #lbl "f\n\t"                                         \
-  "s_waitcnt vmcnt(" #cnt ")\n\t"                                        \
-  "s_branch 9f\n" #lbl ":\n\t"
+// one assembly block: the largest level L in {0, 4, ..., 32} with L <= n is
+// found by a balanced tree of scalar compares (three or four, at most two
+// taken branches) and vmcnt(L) is awaited (never more than n).  Written as
+// a C switch over its levels, the compiler's control-flow structurizer made
+// it a long run of scalar instructions and taken branches on every step,
+// which the 8-bit elastic path (bound by instruction latency) paid for.  n
+// is at most 4 (units in the ring - 1) + the window's loads, below 36 for
+// rings of up to 4 slots.
 __device__ __forceinline__ void wait_vm4(int n) {
   n = __builtin_amdgcn_readfirstlane(n);
-  asm volatile(EKV_WAIT_LEVEL(1, 32) EKV_WAIT_LEVEL(2, 28) EKV_WAIT_LEVEL(3, 24) EKV_WAIT_LEVEL(4, 20)
-               EKV_WAIT_LEVEL(5, 16) EKV_WAIT_LEVEL(6, 12) EKV_WAIT_LEVEL(7, 8) EKV_WAIT_LEVEL(8, 4)
-               "s_waitcnt vmcnt(0)\n9:" ::"s"(n) : "memory", "scc");
+  asm volatile(
+      "s_cmp_lt_i32 %0, 16\n\t"
+      "s_cbranch_scc1 1f\n\t"
+      "s_cmp_lt_i32 %0, 24\n\t"
+      "s_cbranch_scc1 2f\n\t"
+      "s_cmp_lt_i32 %0, 28\n\t"
+      "s_cbranch_scc1 3f\n\t"
+      "s_cmp_lt_i32 %0, 32\n\t"
+      "s_cbranch_scc1 4f\n\t"
+      "s_waitcnt vmcnt(32)\n\t"
+      "s_branch 9f\n"
+      "4:\n\t"
+      "s_waitcnt vmcnt(28)\n\t"
+      "s_branch 9f\n"
+      "3:\n\t"
+      "s_waitcnt vmcnt(24)\n\t"
+      "s_branch 9f\n"
+      "2:\n\t"
+      "s_cmp_lt_i32 %0, 20\n\t"
+      "s_cbranch_scc1 5f\n\t"
+      "s_waitcnt vmcnt(20)\n\t"
+      "s_branch 9f\n"
+      "5:\n\t"
+      "s_waitcnt vmcnt(16)\n\t"
+      "s_branch 9f\n"
+      "1:\n\t"
+      "s_cmp_lt_i32 %0, 8\n\t"
+      "s_cbranch_scc1 6f\n\t"
+      "s_cmp_lt_i32 %0, 12\n\t"
+      "s_cbranch_scc1 7f\n\t"
+      "s_waitcnt vmcnt(12)\n\t"
+      "s_branch 9f\n"
+      "7:\n\t"
+      "s_waitcnt vmcnt(8)\n\t"
+      "s_branch 9f\n"
+      "6:\n\t"
+      "s_cmp_lt_i32 %0, 4\n\t"
+      "s_cbranch_scc1 8f\n\t"
+      "s_waitcnt vmcnt(4)\n\t"
+      "s_branch 9f\n"
+      "8:\n\t"
+      "s_waitcnt vmcnt(0)\n"
+      "9:" ::"s"(n)
+      : "memory", "scc");
 }
-#undef EKV_WAIT_LEVEL
 
 // ---- 8-bit TARGET / 4-bit BASE slots -------------------------------------
 // The ring is cut into 4 KiB units.  A TARGET pair takes two: its K and its
