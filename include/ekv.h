@@ -341,6 +341,37 @@ ekv_status ekv_stage_blocks(const ekv_pool* pool, int32_t n, const void* const* 
                             const int32_t* h_new_blocks, hipStream_t stream);
 
 /*
+ * Asynchronous promotion as one protocol (App. B.2: reserve the extra
+ * block, restore it from the CPU backing while the BASE mapping stays
+ * executable, publish only after TARGET is materialised), for callers that
+ * drive it from C.  The caller keeps the allocator: it picks the reserved
+ * blocks, owns the pinned backing and decides when to publish.
+ *
+ * ekv_promote_begin: ekv_stage_blocks(pool, n, h_src, h_new_blocks) on
+ * copy_stream, then records `copied` on copy_stream after the copy.
+ * Attention may keep running on the pairs (still BASE, mapping untouched)
+ * on other streams meanwhile; hipEventQuery(copied) tells the caller when
+ * publishing will not wait.
+ *   copied  a hipEvent_t created by the caller (required); re-recorded here.
+ * Arguments and errors otherwise as ekv_stage_blocks; nothing is enqueued
+ * or recorded when the arguments are refused.
+ *
+ * ekv_promote_publish: makes `stream` wait for `copied` (a device-side
+ * wait: the host does not block), then ekv_refine_staged on `stream` --
+ * member 0 rebuilt in place, member 1 rebuilt in the reserved block over the
+ * staged bytes, the table entry and both tags switched to TARGET.  So the
+ * mapping is published only after the bytes it points at have landed,
+ * whatever the host does in between.  Arguments and errors as
+ * ekv_refine_staged (new_blocks: the device copy of h_new_blocks); the
+ * arguments are checked before the wait is enqueued.
+ */
+ekv_status ekv_promote_begin(const ekv_pool* pool, int32_t n, const void* const* h_src,
+                             const int32_t* h_new_blocks, hipEvent_t copied, hipStream_t copy_stream);
+ekv_status ekv_promote_publish(const ekv_pool* pool, int32_t n, const int32_t* pairs, const int32_t* new_blocks,
+                               int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,
+                               hipEvent_t copied, hipStream_t stream);
+
+/*
  * Multi-layer transitions: the same pairs demoted (or refined) in every
  * layer's pool of a model in one launch.  In paged serving every layer has
  * its own pool and all layers share one block table, so a pair is one

@@ -685,6 +685,29 @@ ekv_status ekv_stage_blocks(const ekv_pool* pool, int32_t n, const void* const* 
   });
 }
 
+ekv_status ekv_promote_begin(const ekv_pool* pool, int32_t n, const void* const* h_src,
+                             const int32_t* h_new_blocks, hipEvent_t copied, hipStream_t copy_stream) {
+  return ekv::guard("ekv_promote_begin", [&]() -> ekv_status {
+    if (!copied) return fail(EKV_ERR_INVALID, "ekv_promote_begin: the completion event is required");
+    const ekv_status st = ekv_stage_blocks(pool, n, h_src, h_new_blocks, copy_stream);
+    if (st != EKV_OK) return st;
+    return hip_status(hipEventRecord(copied, copy_stream), "ekv_promote_begin event record");
+  });
+}
+
+ekv_status ekv_promote_publish(const ekv_pool* pool, int32_t n, const int32_t* pairs, const int32_t* new_blocks,
+                               int32_t* block_table, uint8_t* tags, int32_t batch, int32_t max_blocks,
+                               hipEvent_t copied, hipStream_t stream) {
+  return ekv::guard("ekv_promote_publish", [&]() -> ekv_status {
+    if (!copied) return fail(EKV_ERR_INVALID, "ekv_promote_publish: the completion event is required");
+    ekv_status st = check_transition_args(pool, n, pairs, block_table, tags, batch, max_blocks);
+    if (st != EKV_OK) return st;
+    if (n > 0 && !new_blocks) return fail(EKV_ERR_INVALID, "new_blocks is required");
+    if ((st = hip_status(hipStreamWaitEvent(stream, copied, 0), "ekv_promote_publish wait")) != EKV_OK) return st;
+    return ekv_refine_staged(pool, n, pairs, new_blocks, block_table, tags, batch, max_blocks, stream);
+  });
+}
+
 ekv_status ekv_refine_layers(const ekv_pool* pool, const uint64_t* layer_kv, int32_t num_layers, int32_t n,
                              const int32_t* pairs, const int32_t* new_blocks, int32_t* block_table,
                              uint8_t* tags, int32_t batch, int32_t max_blocks, const uint8_t* lo_in,

@@ -80,6 +80,8 @@ SIGNATURES = {
     "ekv_refine": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_refine_staged": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _S]),
     "ekv_stage_blocks": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _S]),
+    "ekv_promote_begin": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _S]),
+    "ekv_promote_publish": (_I, [ctypes.POINTER(Pool), _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_demote_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _I, _I, _P, _P, _S]),
     "ekv_refine_layers": (_I, [ctypes.POINTER(Pool), _P, _I, _I, _P, _P, _P, _P, _I, _I, _P, _S]),
     "ekv_check_transition": (_I, [_I, _P, _I, _P, _P, _P, _I, _I, _I, _I, _P]),
@@ -253,6 +255,42 @@ def stage_blocks(pool, sources, new_blocks, stream=None):
         raise EkvError(ERR_INVALID, "one new block per source")
     _check(lib().ekv_stage_blocks(ctypes.byref(pool), len(new), srcs.ctypes.data_as(ctypes.c_void_p), np_,
                                   _stream(stream)))
+
+
+def _event(event, create_on=None):
+    """The HIP event handle of a torch.cuda.Event.  torch creates the event
+    at its first record; with create_on (a stream) an event not yet created
+    is recorded there once first, otherwise it must exist already."""
+    if event is None:
+        return None
+    if event.cuda_event == 0:
+        if create_on is None:
+            raise EkvError(ERR_INVALID, "the event has never been recorded")
+        event.record(create_on)
+    return ctypes.c_void_p(event.cuda_event)
+
+
+def promote_begin(pool, sources, new_blocks, copied, copy_stream=None):
+    """ekv_promote_begin: stage each source (pinned host or device address)
+    into new_blocks (host int32 array) on copy_stream, then record the
+    torch.cuda.Event `copied` there."""
+    srcs = np.ascontiguousarray([int(a) for a in sources], dtype=np.uint64)
+    new, np_ = _host(new_blocks, np.int32)
+    if len(srcs) != len(new):
+        raise EkvError(ERR_INVALID, "one new block per source")
+    import torch
+    cs = copy_stream if copy_stream is not None else torch.cuda.current_stream()
+    _check(lib().ekv_promote_begin(ctypes.byref(pool), len(new), srcs.ctypes.data_as(ctypes.c_void_p), np_,
+                                   _event(copied, cs), _stream(cs)))
+
+
+def promote_publish(pool, pairs, new_blocks, block_table, tags, copied, stream=None):
+    """ekv_promote_publish: `stream` waits for `copied`, then the staged
+    refinement publishes the pairs (pairs, new_blocks: device tensors)."""
+    bsz, max_blocks = block_table.shape
+    _check(lib().ekv_promote_publish(ctypes.byref(pool), pairs.shape[0], _ptr(pairs), _ptr(new_blocks),
+                                     _ptr(block_table), _ptr(tags), bsz, max_blocks, _event(copied),
+                                     _stream(stream)))
 
 
 def demote_layers(pool, layer_kv, pairs, block_table, tags, freed_out, lo_out=None, stream=None):

@@ -247,18 +247,18 @@ class AsyncPromotion:
         sources = [self.backing[k][0] for k in keys]
         for done in {id(self.backing[k][1]): self.backing[k][1] for k in keys}.values():
             self.copy.wait_event(done)
-        # one copy kernel reads every pair's backing over the host link
+        # one copy kernel reads every pair's backing over the host link;
+        # the library records `ev` after it (ekv_promote_begin)
         start = torch.cuda.Event(enable_timing=True)
         start.record(self.copy)
+        ev = torch.cuda.Event(enable_timing=True)
         try:
-            ekv.stage_blocks(self.kv.pool, [h.data_ptr() for h in sources], new, self.copy)
+            ekv.promote_begin(self.kv.pool, [h.data_ptr() for h in sources], new, ev, self.copy)
         except ekv.EkvError:
             self.kv.mirror.cancel_refine(pairs, new)
             raise
         for k in keys:
             del self.backing[k]
-        ev = torch.cuda.Event(enable_timing=True)
-        ev.record(self.copy)
         self.last_copy = (start, ev)
         self.inflight.append((ev, pairs, new, sources))
         return new
@@ -273,11 +273,11 @@ class AsyncPromotion:
             if not (wait or ev.query()):
                 keep.append((ev, pairs, new, sources))
                 continue
-            stream.wait_event(ev)
             with torch.cuda.stream(stream):
                 pairs_d = self.kv._upload(pairs)
                 new_d = self.kv._upload(new)
-            ekv.refine_staged(self.kv.pool, pairs_d, new_d, self.kv.bt, self.kv.tags, stream)
+            # the stream waits for the copy, then the staged refinement publishes
+            ekv.promote_publish(self.kv.pool, pairs_d, new_d, self.kv.bt, self.kv.tags, ev, stream)
             self.kv.mirror.publish_refine(pairs, new)
             count += len(pairs)
         self.inflight = keep

@@ -178,6 +178,10 @@ void arguments() {
   fresh[1] = 2;
   const ekv_status sb = ekv_stage_blocks(&pool, 2, src, fresh, nullptr);
   expect(sb == EKV_ERR_INVALID || sb == EKV_ERR_HIP, "stage pageable", 0);
+  // the promotion protocol refuses a missing completion event before anything else
+  expect(ekv_promote_begin(&pool, 2, src, fresh, nullptr, nullptr) == EKV_ERR_INVALID, "promote_begin no event", 0);
+  expect(ekv_promote_publish(&pool, 1, pairs, fresh, bt, nullptr, 1, 4, nullptr, nullptr) == EKV_ERR_INVALID,
+         "promote_publish no event", 0);
   expect(std::strlen(ekv_status_string(EKV_ERR_HOST)) > 0, "status string", 0);
   std::free(host);
   std::free(lens);

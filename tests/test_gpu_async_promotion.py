@@ -108,6 +108,71 @@ def test_async_promotion_round_trip(wait):
             assert np.array_equal(got[fbt[s, i], :, :, :rows], case["pool"][case["block_table"][s, i], :, :, :rows])
 
 
+def test_publish_waits_for_a_late_copy_on_the_device():
+    """ekv_promote_begin / ekv_promote_publish: the copy stream is held back
+    by a spin of ~2 ms before the staging copy, and the pairs are published
+    at once on the compute stream with no host wait, then decoded.  The
+    device-side wait keeps the refinement behind the copy: pool, table and
+    tags equal the oracle's refinement, and the decode the oracle's."""
+    torch = require_gpu()
+    lens = [640, 1200, 300]
+    hq, hkv = 8, 2
+    case = workloads.make_decode_case(lens, hq, hkv, seed=72, base_fraction=1.0, spare_blocks=8)
+    host_safety_check(case, case["pool"].shape)
+    kv = kvpool.PagedKV(case["pool"], case["block_table"], case["seq_lens"], case["free"], hkv)
+    eng = kvpool.AsyncPromotion(kv)
+    pairs = case["pairs"]
+    eng.demote(pairs)
+    opool, obt, otg, ofreed, olo = otr.demote(case["pool"], case["block_table"], case["tags"], pairs,
+                                               case["seq_lens"])
+    kv.commit()
+    fifo = otr.FreeFifo(case["free"])
+    fifo.commit_freed(ofreed)
+    torch.cuda.synchronize()
+    print(f"late copy: pairs={len(pairs)}", flush=True)
+    with torch.cuda.stream(eng.copy):
+        torch.cuda._sleep(1 << 22)
+    new = eng.promote(pairs)
+    onew = fifo.acquire(len(pairs))
+    assert np.array_equal(new, onew)
+    assert eng.publish(wait=True) == len(pairs)   # enqueued behind the copy; the host does not wait
+    q = words_to_tensor(case["q"], torch, "bf16")
+    out = _decode(kv, q, hq, torch)
+    torch.cuda.synchronize()
+    rpool, rbt, rtg = otr.refine(opool, obt, otg, pairs, onew, olo, case["seq_lens"])
+    assert np.array_equal(kv.bt.cpu().numpy(), rbt) and np.array_equal(kv.tags.cpu().numpy(), rtg)
+    live = _live(rbt, case["seq_lens"])
+    got = kv.kv.view(-1, 2, hkv, PAGE, 128)[live].cpu().numpy().view(np.uint16)
+    assert np.array_equal(got, rpool[live])
+    check_attention(out.cpu().numpy(), oatt.decode(case["q"], rpool, rbt, rtg, case["seq_lens"]), True)
+
+
+def test_promote_entry_points_refuse_a_missing_event():
+    torch = require_gpu()
+    case = workloads.make_decode_case([256, 256], 8, 2, seed=73, base_fraction=1.0, spare_blocks=8)
+    kv = kvpool.PagedKV(case["pool"], case["block_table"], case["seq_lens"], case["free"], 2)
+    kv.demote(case["pairs"][:1])
+    kv.commit()
+    before = kv.kv.clone()
+    bt_before = kv.bt.clone()
+    pairs_d = torch.from_numpy(np.asarray(case["pairs"][:1], dtype=np.int32)).cuda()
+    new_d = torch.tensor([int(kv.mirror.free[0])], dtype=torch.int32, device="cuda")
+    lib = ekv.lib()
+    bsz, max_blocks = kv.bt.shape
+    st = lib.ekv_promote_publish(ekv.ctypes.byref(kv.pool), 1, ekv._ptr(pairs_d), ekv._ptr(new_d), ekv._ptr(kv.bt),
+                                 ekv._ptr(kv.tags), bsz, max_blocks, None, None)
+    assert st == ekv.ERR_INVALID
+    src = np.ascontiguousarray([kv.kv.data_ptr()], dtype=np.uint64)
+    blocks = np.ascontiguousarray([int(kv.mirror.free[0])], dtype=np.int32)
+    st = lib.ekv_promote_begin(ekv.ctypes.byref(kv.pool), 1, src.ctypes.data_as(ekv.ctypes.c_void_p),
+                               blocks.ctypes.data_as(ekv.ctypes.c_void_p), None, None)
+    assert st == ekv.ERR_INVALID
+    with pytest.raises(ekv.EkvError):   # an event that was never recorded
+        ekv.promote_publish(kv.pool, pairs_d, new_d, kv.bt, kv.tags, torch.cuda.Event())
+    torch.cuda.synchronize()
+    assert torch.equal(kv.kv, before) and torch.equal(kv.bt, bt_before)
+
+
 def test_promotion_needs_backing_and_rejects_double_promotion():
     torch = require_gpu()
     case = workloads.make_decode_case([256, 256], 8, 2, seed=71, base_fraction=1.0, spare_blocks=8)
