@@ -300,6 +300,38 @@ def test_decode_e5m2_8b_weighted_ranges(fraction, permille, monkeypatch):
     print(f"  max abs err {err:.3e} on 64 sequences", flush=True)
 
 
+@pytest.mark.parametrize("fraction", [0.5, 1.0])
+def test_decode_e5m2_weighted_ranges_near_the_minimum_range(fraction):
+    """16 sequences of 4608 tokens, 32/8 heads: 18,432 pairs fill the grid
+    of 2048 workgroups with 9 pairs each on average, just above the minimum
+    range of 8, so the weighted ranges apply at their smallest (11 pairs for
+    the first-slot workgroups, 7 for the others) and most (sequence, KV
+    head)s are cut into many pieces.  Every sequence against the oracle."""
+    torch = require_gpu()
+    seq_lens = np.full(16, 4608, dtype=np.int32)
+    case = workloads.make_decode_case_torch(seq_lens, 32, 8, seed=8, outlier_channels=10, spare_blocks=16,
+                                            dtype="e5m2")
+    pairs = workloads.choose_pairs(np.random.default_rng(2200 + int(2 * fraction)), seq_lens, fraction, "random")
+    kv = kvpool.PagedKV(case["pool"].clone(), case["block_table"], seq_lens, case["free"], 8, "e5m2")
+    kv.demote(pairs, emit_lo=False)
+    kv.commit()
+    kv.relower()
+    batch = kv.batch(32)
+    ws = ekv.decode_workspace(kv.pool, batch)
+    print(f"8-bit weighted ranges near the minimum: f={fraction} pairs={len(pairs)}", flush=True)
+    out = torch.full((16, 32, 128), float("nan"), dtype=torch.float32, device="cuda")
+    ekv.attn_decode(kv.pool, batch, case["q"], out, default_scale(), ws)
+    torch.cuda.synchronize()
+    sample = list(range(16))
+    host, sbt, slens = workloads.extract_sequences(case["pool"], case["block_table"], seq_lens, sample)
+    tg = np.zeros(sbt.shape, dtype=np.uint8)
+    host, sbt, tg, _, _ = ofp8.demote(host, sbt, tg, pairs, slens)
+    q_words = case["q"].view(torch.int16).cpu().numpy().view(np.uint16)
+    ref = ofp8.decode(q_words, host, sbt, tg, slens)
+    err, _ = check_attention(out.cpu().numpy(), ref, True)
+    print(f"  max abs err {err:.3e} on 16 sequences", flush=True)
+
+
 def test_prefill_e5m2_8b_full_size():
     """The chunked-prefill workload over an 8-bit pool as the benchmark runs
     it: 16 x (2048-token prefix, half its pairs BASE, + 512-token chunk), 32
