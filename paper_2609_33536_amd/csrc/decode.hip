@@ -356,12 +356,28 @@ __device__ __forceinline__ constexpr uint32_t word_pair_sel(int k) {
   return 0x0Cu | ((uint32_t)k << 8) | (0x0Cu << 16) | ((uint32_t)(4 + k) << 24);
 }
 
-// 8 nibble elements straight to 16-bit words (the QK^T operand of BASE K):
-// word k holds elements 2k, 2k+1.
-__device__ __forceinline__ u32x4 nib_words(uint32_t w) {
-  const NibPlanes p = nib_planes(w);
-  return u32x4{perm(p.odd, p.even, word_pair_sel(0)), perm(p.odd, p.even, word_pair_sel(1)),
-               perm(p.odd, p.even, word_pair_sel(2)), perm(p.odd, p.even, word_pair_sel(3))};
+// 8-bit pools: the QK^T operands of a 16-dim step hold its 8 elements as
+// 16-bit word pairs (e_j, e_{j+4}), j = 0..3, for K and Q alike (the dot
+// product does not depend on the order, as long as both follow it).  BASE K
+// then takes one packed 16-bit shift (and a mask) per word: 8 nibbles ->
+// 4 words in 6 instructions, where the (e_2j, e_2j+1) order took 7.
+typedef unsigned short u16x2v __attribute__((ext_vector_type(2)));
+__device__ __forceinline__ u32x4 nib_words_x4(uint32_t w) {
+  const u16x2v x = __builtin_bit_cast(u16x2v, w);
+  constexpr uint32_t kTop = 0xF000F000u;   // the top nibble of each 16-bit half
+  return u32x4{__builtin_bit_cast(uint32_t, (u16x2v)(x << 12)), __builtin_bit_cast(uint32_t, (u16x2v)(x << 8)) & kTop,
+               __builtin_bit_cast(uint32_t, (u16x2v)(x << 4)) & kTop, w & kTop};
+}
+// 8 element bytes (a TARGET row or a lone block's, in the byte layout) ->
+// words (b_j << 8, b_{j+4} << 8)
+__device__ __forceinline__ u32x4 byte_words_x4(u32x2 b) {
+  return u32x4{perm(b.y, b.x, word_pair_sel(0)), perm(b.y, b.x, word_pair_sel(1)), perm(b.y, b.x, word_pair_sel(2)),
+               perm(b.y, b.x, word_pair_sel(3))};
+}
+// Q's words (q_2j, q_2j+1) -> (q_j, q_{j+4})
+__device__ __forceinline__ u32x4 q_words_x4(u32x4 w) {
+  return u32x4{perm(w[2], w[0], 0x05040100u), perm(w[2], w[0], 0x07060302u), perm(w[3], w[1], 0x05040100u),
+               perm(w[3], w[1], 0x07060302u)};
 }
 
 // PV A operand j of BASE V straight from the planes of the lane's 4 tokens:
@@ -816,10 +832,12 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
   u32x4 qop[4];
   auto load_q = [&](const char* wb) {
 #pragma unroll
-    for (int k = 0; k < 4; ++k)
+    for (int k = 0; k < 4; ++k) {
       qop[k] = (n < kQCols)
                    ? (*reinterpret_cast<const u32x4*>(wb + kWinQ + (n % G) * 2 * kHeadDim + 16 * (4 * g + k)) ^ q_sign)
                    : u32x4{0u, 0u, 0u, 0u};
+      if constexpr (F8) qop[k] = q_words_x4(qop[k]);
+    }
   };
   load_q(sm.win[0]);
   // Fused append: the physical block of the newest token's block when it
@@ -935,7 +953,7 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
           const u32x4 kn = *reinterpret_cast<const u32x4*>(mb + rk4);
           u32x4 kw[4];
 #pragma unroll
-          for (int q = 0; q < 4; ++q) kw[q] = nib_words(kn[q]);
+          for (int q = 0; q < 4; ++q) kw[q] = nib_words_x4(kn[q]);
           sc[m] = qk_scores<T, false>(kw, qop);
 #pragma unroll
           for (int i = 0; i < 4; ++i)
@@ -966,7 +984,10 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
           const char* mv = vb + m * (kTileBytes / 2) - kTileBytes;   // rv_b counts from the K tile
 #pragma unroll
           for (int i = 0; i < 4; ++i) v[m][i].xy = *reinterpret_cast<const u32x2*>(mv + rv_b[i]);
-          sc[m] = qk_scores<T, true>(k[m], qop);
+          f32x4 s = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int st = 0; st < 4; ++st) s = Mma<T>::qk(byte_words_x4(k[m][st].xy), qop[st], s);
+          sc[m] = s;
         }
         zero_tail_v<2>(v, cb * kPage, ccur.len, g);
         pv_operands<true, 2>(v, pvo);
