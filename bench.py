@@ -375,10 +375,14 @@ def main():
 
     def step(timed):
         rec = []
+        # every pool's append and re-lowering first, then the decodes back to
+        # back: the host's work between a decode's start event and its launch
+        # would otherwise let the queue run dry and count in the event time
         for k, kv in enumerate(pools):
             slots, kn, vn = dec["appends"][k]
             kv.append(slots, kn, vn)
             kv.relower()
+        for k, kv in enumerate(pools):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             e0.record(stream)
             ekv.attn_decode(kv.pool, batches[k], q, outs[k], scale, ws)
