@@ -189,11 +189,13 @@ ekv_status ekv_decode_workspace_init(void* ws, size_t ws_bytes, hipStream_t stre
  *   q    device [batch][num_q_heads][head_dim], pool dtype
  *   out  device [batch][num_q_heads][head_dim], out_dtype = pool dtype or EKV_DTYPE_FP32
  *   ws   device scratch of at least ekv_decode_workspace_bytes() bytes,
- *        prepared by ekv_decode_workspace_init (or zero-filled) before its
- *        first use; calls sharing one ws must be ordered on one stream
+ *        16-byte aligned, prepared by ekv_decode_workspace_init (or
+ *        zero-filled) before its first use; calls sharing one ws must be
+ *        ordered on one stream
  * A sequence of length 0 yields zeros.
- * Errors: EKV_ERR_INVALID (NULL pointers, sizes, workspace too small,
- * NATIVE mode expected but tags needed), EKV_ERR_UNSUPPORTED, EKV_ERR_HIP.
+ * Errors: EKV_ERR_INVALID (NULL pointers, sizes, workspace too small or
+ * misaligned, NATIVE mode expected but tags needed), EKV_ERR_UNSUPPORTED,
+ * EKV_ERR_HIP.
  */
 ekv_status ekv_attn_decode(const ekv_pool* pool, const ekv_batch* batch, const void* q,
                            void* out, int32_t out_dtype, float scale, void* ws, size_t ws_bytes,

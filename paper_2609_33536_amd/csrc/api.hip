@@ -294,6 +294,8 @@ ekv_status decode_call(const ekv_pool* pool, const ekv_batch* batch, const void*
     if ((st = plan_decode(pool, batch, group, false, &plan)) != EKV_OK) return st;
     if (!ws || ws_bytes < plan.total)
       return fail(EKV_ERR_INVALID, "workspace of %zu bytes needed, %zu given", plan.total, ws_bytes);
+    if (reinterpret_cast<uintptr_t>(ws) % 16)   // the partial rows move in 16-byte accesses
+      return fail(EKV_ERR_INVALID, "%s: ws must be 16-byte aligned", who);
   }
   if ((st = plan_decode(pool, batch, group, true, &plan)) != EKV_OK) return st;
   if (plan.total > ws_bytes)   // (the static scratch: sized by the device's own grid)

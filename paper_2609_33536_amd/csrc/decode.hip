@@ -89,11 +89,6 @@ __device__ __forceinline__ float2 load_agent_f2(const float* p) {
   return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
 }
 
-__device__ __forceinline__ f32x4 load_agent_f4(const float* p) {
-  const float2 a = load_agent_f2(p), b = load_agent_f2(p + 2);
-  return f32x4{a.x, a.y, b.x, b.y};
-}
-
 __device__ __forceinline__ float wave_max(float x) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) x = fmaxf(x, __shfl_xor(x, off));
@@ -119,69 +114,125 @@ __device__ __forceinline__ int piece_slot(int w_first, int first_odd, int k) {
   return 2 * (w_first + k) + (k == 0 ? first_odd : 0);
 }
 
+// A slot holds a piece's G partial rows as 32 G chunks of 16 bytes.  The
+// writing lane (n, g), n < G, holds dims 32 g .. 32 g + 31 of head n; its
+// chunk ci (dims 32 g + 4 ci .. + 3) sits at chunk ci * 4 G + n + G g, so
+// each of its 8 store instructions covers 4 G consecutive chunks (whole
+// 64-byte lines).  Chunk q of a slot: ci = q / 4G, n = q % G, g = (q % 4G) / G.
+// The stores and loads carry the agent-scope cache policy (sc1: written
+// through to, and read from, the memory side, which every XCD sees), as the
+// relaxed agent-scope 8-byte atomics do; 16 bytes a lane and whole lines a
+// store instruction, where 8-byte stores with a row-major layout cost a
+// 32-byte write request per lane (four times the partial bytes in HBM
+// writes, and ~5 % of an f = 1 launch's time).  The workspace is 16-byte
+// aligned (checked at the entry point).
+__device__ __forceinline__ void store_agent_f4(float* p, f32x4 v) {
+  asm volatile("global_store_dwordx4 %0, %1, off sc1" ::"v"(p), "v"(v) : "memory");
+}
+__device__ __forceinline__ f32x4 load_agent_row4(const float* p) {
+  f32x4 v;
+  asm volatile("global_load_dwordx4 %0, %1, off sc1" : "=v"(v) : "v"(p) : "memory");
+  return v;
+}
+// Completes this wave's loads; the registers are tied to the wait so that no
+// use of them is scheduled before it.
+__device__ __forceinline__ void wait_rows(f32x4 (&v)[16]) {
+  asm volatile("s_waitcnt vmcnt(0)"
+               : "+v"(v[0]), "+v"(v[1]), "+v"(v[2]), "+v"(v[3]), "+v"(v[4]), "+v"(v[5]), "+v"(v[6]), "+v"(v[7]),
+                 "+v"(v[8]), "+v"(v[9]), "+v"(v[10]), "+v"(v[11]), "+v"(v[12]), "+v"(v[13]), "+v"(v[14]), "+v"(v[15])
+               :
+               : "memory");
+}
+
 // Merge the nsplit (<= 64) partials of the G heads of one (sequence, KV
 // head): out = sum_k w_k o_k / sum_k w_k l_k with w_k = exp2(m_k - max m).
-// Lane k holds split k's (max, sum); for the numerators lane (c, par) =
-// (lane & 31, lane >> 5) owns head-dim columns 4c..4c+3 of the splits with
-// parity par.  The (max, sum) loads and the first 16 row loads are issued
-// together, so a merge of up to 2 * kB splits costs one memory round trip.
+// Lane k holds split k's (max, sum).  The numerators follow the slot
+// layout: a load of the wave reads 64 consecutive chunks of one split (or,
+// for G = 1, the 32 chunks of two splits), so lane L owns head L % G and the
+// chunks L + 64 t.  The (max, sum) loads and the first 16 chunk loads are
+// issued together: a merge of up to one batch of splits costs one memory
+// round trip.
 template <typename T, int G>
 __device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int w_first, int first_odd, int lane) {
-  constexpr int kB = G >= 16 ? 1 : 16 / G;     // split pairs per batch
-  const int c = lane & 31, par = lane >> 5;
+  constexpr int kT = G >= 2 ? G / 2 : 1;        // loads per split (G = 1: one load covers two splits)
+  constexpr int kSB = G >= 2 ? 16 / kT : 32;    // splits per batch of 16 loads
   float2 mlk[G];
 #pragma unroll
   for (int h = 0; h < G; ++h)
     mlk[h] = lane < nsplit ? load_agent_f2(a.ws_ml + 2 * ((size_t)piece_slot(w_first, first_odd, lane) * G + h))
                            : make_float2(-__builtin_inff(), 0.f);
-  f32x4 v[G][kB];
+  // split and chunk of load i of the batch at k0
+  auto split_of = [&](int k0, int i) { return G >= 2 ? k0 + i / kT : k0 + 2 * i + (lane >> 5); };
+  auto chunk_of = [&](int i) { return G >= 2 ? lane + 64 * (i % kT) : (lane & 31); };
+  f32x4 v[16];
+  int kb0 = 0;
   auto load_batch = [&](int k0) {
+    kb0 = k0;
 #pragma unroll
-    for (int h = 0; h < G; ++h) {
-      const float* o = a.ws_o + (size_t)h * kHeadDim + 4 * c;
-#pragma unroll
-      for (int b = 0; b < kB; ++b) {
-        const int k = k0 + 2 * b + par;
-        v[h][b] = k < nsplit ? load_agent_f4(o + (size_t)piece_slot(w_first, first_odd, k) * G * kHeadDim)
-                             : f32x4{0.f, 0.f, 0.f, 0.f};
-      }
+    for (int i = 0; i < 16; ++i) {
+      const int k = min(split_of(k0, i), nsplit - 1);   // a split that exists (zeroed below if past the last)
+      v[i] = load_agent_row4(a.ws_o + (size_t)piece_slot(w_first, first_odd, k) * G * kHeadDim + 4 * chunk_of(i));
     }
   };
   load_batch(0);
-  float wk[G], inv_den[G];
-  f32x4 num[G];
+  const int my_h = lane % G;
+  float wk[G], my_inv = 0.f;
 #pragma unroll
   for (int h = 0; h < G; ++h) {
     const float mmax = wave_max(mlk[h].x);
     wk[h] = lane < nsplit ? fast_exp2(mlk[h].x - mmax) : 0.f;
-    inv_den[h] = 1.0f / wave_sum(wk[h] * mlk[h].y);
-    num[h] = f32x4{0.f, 0.f, 0.f, 0.f};
+    const float inv = 1.0f / wave_sum(wk[h] * mlk[h].y);
+    my_inv = h == my_h ? inv : my_inv;
   }
+  f32x4 num[kT];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) num[t] = f32x4{0.f, 0.f, 0.f, 0.f};
   for (int k0 = 0;;) {
+    wait_rows(v);
 #pragma unroll
-    for (int h = 0; h < G; ++h)
+    for (int i = 0; i < 16; ++i)
+      if (split_of(k0, i) >= nsplit) v[i] = f32x4{0.f, 0.f, 0.f, 0.f};
+    if constexpr (G >= 2) {
 #pragma unroll
-      for (int b = 0; b < kB; ++b) {
-        const int k = k0 + 2 * b;
-        const float w0 = k < 64 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[h]), k)) : 0.f;
-        const float w1 = k + 1 < 64 ? __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[h]), k + 1)) : 0.f;
-        num[h] += (par ? w1 : w0) * v[h][b];
+      for (int sp = 0; sp < kSB; ++sp) {
+        const int k = min(k0 + sp, 63);
+        float w = 0.f;
+#pragma unroll
+        for (int h = 0; h < G; ++h) {
+          const float wh = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[h]), k));
+          w = h == my_h ? wh : w;
+        }
+#pragma unroll
+        for (int t = 0; t < kT; ++t) num[t] += w * v[sp * kT + t];
       }
-    k0 += 2 * kB;
+    } else {
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        const int k = k0 + 2 * i;
+        const float w0 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[0]), min(k, 63)));
+        const float w1 = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[0]), min(k + 1, 63)));
+        num[0] += ((lane >> 5) ? w1 : w0) * v[i];
+      }
+    }
+    k0 += kSB;
     if (k0 >= nsplit) break;
     load_batch(k0);
   }
-#pragma unroll
-  for (int h = 0; h < G; ++h) {
-    f32x4 tot;
+  if constexpr (G == 1) {   // the two halves of the wave summed splits of opposite parity
 #pragma unroll
     for (int e = 0; e < 4; ++e) {
-      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(num[h][e]), __float_as_uint(num[h][e]),
+      const auto sw = __builtin_amdgcn_permlane32_swap(__float_as_uint(num[0][e]), __float_as_uint(num[0][e]),
                                                        false, false);
-      tot[e] = (__uint_as_float(sw[0]) + __uint_as_float(sw[1])) * inv_den[h];
+      num[0][e] = __uint_as_float(sw[0]) + __uint_as_float(sw[1]);
     }
-    if (par == 0) {
-      const size_t idx = (head0 + h) * kHeadDim + 4 * c;
+  }
+  if (G >= 2 || lane < 32) {
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      const int q = chunk_of(t);
+      const int ci = q / (4 * G), g = (q % (4 * G)) / G;
+      const f32x4 tot = num[t] * my_inv;
+      const size_t idx = (head0 + my_h) * kHeadDim + 32 * g + 4 * ci;
       store_pair<T>(a.out, idx, tot[0], tot[1], a.out_fp32);
       store_pair<T>(a.out, idx + 2, tot[2], tot[3], a.out_fp32);
     }
@@ -193,7 +244,9 @@ template <typename T, int G>
 __device__ void merge_head_serial(const DecodeArgs& a, size_t head, int h, int nsplit, int w_first, int first_odd,
                                   int lane) {
   const float* ml = a.ws_ml + 2 * h;
-  const float* o = a.ws_o + (size_t)h * kHeadDim + 2 * lane;
+  // dims 2 lane, 2 lane + 1: chunk (c % 8) * 4G + h + G (c / 8) of the slot, c = lane / 2
+  const int c = lane >> 1;
+  const float* o = a.ws_o + 4 * ((c & 7) * 4 * G + h + G * (c >> 3)) + 2 * (lane & 1);
   float mmax = -__builtin_inff();
   for (int k0 = 0; k0 < nsplit; k0 += 64)
     if (k0 + lane < nsplit) mmax = fmaxf(mmax, load_agent_f2(ml + 2 * (size_t)piece_slot(w_first, first_odd, k0 + lane) * G).x);
@@ -891,13 +944,16 @@ __global__ __launch_bounds__(64) void decode_kernel(DecodeArgs a) {
     } else {
       // this workgroup's slot for the piece: 2w if the (sequence, KV head)
       // contains its first pair, else 2w + 1
-      const size_t row = (size_t)(2 * (int)blockIdx.x + (first > start ? 1 : 0)) * G + n;
+      const size_t slot = (size_t)(2 * (int)blockIdx.x + (first > start ? 1 : 0));
+      const size_t row = slot * G + n;
       if (n < G) {
-        float* dst = a.ws_o + row * kHeadDim + 32 * g;
+        // chunk ci = 2 r + half of this lane at chunk ci * 4G + n + G g of the slot
+        float* dst = a.ws_o + slot * G * kHeadDim + 4 * (n + G * g);
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-#pragma unroll
-          for (int j = 0; j < 8; j += 2) store_agent_f2(dst + 8 * r + j, st.o[j][r], st.o[j + 1][r]);
+        for (int r = 0; r < 4; ++r) {
+          store_agent_f4(dst + (2 * r) * 16 * G, f32x4{st.o[0][r], st.o[1][r], st.o[2][r], st.o[3][r]});
+          store_agent_f4(dst + (2 * r + 1) * 16 * G, f32x4{st.o[4][r], st.o[5][r], st.o[6][r], st.o[7][r]});
+        }
         if (g == 0) store_agent_f2(a.ws_ml + 2 * row, st.m, l);
       }
       pend_head0[pend_n] = head0;

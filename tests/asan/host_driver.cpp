@@ -154,6 +154,8 @@ void arguments() {
   expect(need > 0, "workspace size", 0);
   expect(ekv_attn_decode(&pool, &batch, host, host, EKV_DTYPE_BF16, 1.f, host, need - 1, nullptr) == EKV_ERR_INVALID,
          "decode small workspace", 0);
+  expect(ekv_attn_decode(&pool, &batch, host, host, EKV_DTYPE_BF16, 1.f, host + 8, need, nullptr) == EKV_ERR_INVALID,
+         "decode misaligned workspace", 0);
   expect(ekv_attn_decode(nullptr, &batch, host, host, 0, 1.f, host, need, nullptr) == EKV_ERR_INVALID, "decode NULL", 0);
   expect(ekv_attn_decode(&pool, &batch, host, host, 0, NAN, host, need, nullptr) == EKV_ERR_INVALID, "decode scale", 0);
   expect(ekv_attn_decode_append(&pool, &batch, host, nullptr, host, host, 0, 1.f, host, need, nullptr) == EKV_ERR_INVALID,

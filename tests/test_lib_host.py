@@ -155,6 +155,9 @@ def test_argument_errors_before_device_work(lib):
     assert need > 0
     assert lib.ekv_attn_decode(ctypes.byref(pool), ctypes.byref(batch), 1, 1, 0, 1.0, 1, need - 1,
                                None) == ekv.ERR_INVALID
+    # the workspace's partial rows move in 16-byte accesses: a misaligned ws is refused
+    st_ = lib.ekv_attn_decode(ctypes.byref(pool), ctypes.byref(batch), 1, 1, 0, 1.0, 0x1008, need, None)
+    assert st_ == ekv.ERR_INVALID and b"aligned" in lib.ekv_last_error()
     assert lib.ekv_demote(ctypes.byref(pool), 1, None, None, None, 1, 4, None, None, None) == ekv.ERR_INVALID
     assert lib.ekv_refine(ctypes.byref(pool), 1, 1, None, 1, 1, 1, 4, None, None) == ekv.ERR_INVALID
 
