@@ -1230,7 +1230,7 @@ Residency residency(K kernel, std::atomic<int>* cache) {
 // BASE fraction 1).  So the first-slot workgroups take ranges of
 // kHeavyPermille / 1000 times the mean and the others share the rest
 // (EKV_HEAVY_PERMILLE overrides; 1000 gives equal ranges).
-constexpr int kHeavyPermille = 1200;
+constexpr int kHeavyPermille = 1150;
 int heavy_permille() {
   if (const char* env = getenv("EKV_HEAVY_PERMILLE")) return std::max(1000, std::min(1900, atoi(env)));
   return kHeavyPermille;
