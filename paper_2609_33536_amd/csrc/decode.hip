@@ -165,9 +165,7 @@ __device__ void merge_splits(const DecodeArgs& a, size_t head0, int nsplit, int 
   auto split_of = [&](int k0, int i) { return G >= 2 ? k0 + i / kT : k0 + 2 * i + (lane >> 5); };
   auto chunk_of = [&](int i) { return G >= 2 ? lane + 64 * (i % kT) : (lane & 31); };
   f32x4 v[16];
-  int kb0 = 0;
   auto load_batch = [&](int k0) {
-    kb0 = k0;
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int k = min(split_of(k0, i), nsplit - 1);   // a split that exists (zeroed below if past the last)
@@ -386,13 +384,6 @@ __device__ __forceinline__ void dma_member0_bytes(const char* tile0, const uint3
   for (int r = 0; r < 2; ++r)
     __builtin_amdgcn_global_load_lds(static_cast<const void*>(tile0 + lane_offset(off[r])), (lds_ptr)(dst + 1024 * r), 16,
                                      0, kStreamOnce);
-}
-
-// 4 bytes of nibbles (element 2k low, 2k+1 high in byte k) -> 8 element
-// bytes, each nibble in the high half with a zero low half.
-__device__ __forceinline__ u32x2 expand4(uint32_t w) {
-  const uint32_t even = (w << 4) & 0xF0F0F0F0u, odd = w & 0xF0F0F0F0u;
-  return u32x2{perm(odd, even, 0x05010400u), perm(odd, even, 0x07030602u)};
 }
 
 // The same 4 bytes of nibbles as two byte planes, each nibble in the high
