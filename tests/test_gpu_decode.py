@@ -114,6 +114,18 @@ def test_decode_work_partition(min_chunk):
     _run(c, 32, 8, min_chunk=min_chunk)
 
 
+@pytest.mark.parametrize("group", [1, 2, 8, 16])
+def test_decode_merges_every_group(group):
+    """One-pair ranges: the 141-pair (sequence, KV head)s of the 4500-token
+    sequence merge 141 pieces each (the serial path), the 63-pair ones 63
+    (the batched path), the 10-pair ones 10; the slot layout of the partial
+    rows depends on the group size."""
+    hkv = 2
+    c = workloads.make_decode_case([4500, 300, 2000], hkv * group, hkv, seed=120 + group, base_fraction=0.5,
+                                   spare_blocks=2)
+    _run(c, hkv * group, hkv, min_chunk=1)
+
+
 def test_structured_and_general_paths_agree():
     """Oldest pairs BASE (structured); same inputs forced through the tag table."""
     c = workloads.make_decode_case([512, 1024, 768, 96], 16, 2, seed=4, base_fraction=0.5,
